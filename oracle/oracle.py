@@ -1,0 +1,131 @@
+"""Python front end of the fp64 CPU oracle (test infrastructure only).
+
+Only ``tests/``, the smoke check and the CPU-baseline leg of the benchmark may
+import this module.  It loads ``liboracle.so`` built from ``tod_oracle.c`` by
+:func:`build` and exposes numpy-level wrappers.  Nothing here is shared with
+the HIP path.
+
+Functions:
+  knn(xq, xr, k, exclude_self, rows=None) -> (idx int64 [m,k], dist fp64 [m,k])
+  knn_self(x, k, rows=None)               -> kNN of X against itself, self excluded
+  lof(idx, dist)                          -> (lof, lrd, kdist), fp64 [n]
+  lof_rows(x, k, rows)                    -> (lof, lrd, kdist) for the listed rows
+  knn_score(dist)                         -> distance to the k-th neighbour
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tod_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile tod_oracle.c with gcc (fp64, no fused multiply-add)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = [
+            "gcc", "-O2", "-std=c11", "-D_GNU_SOURCE", "-ffp-contract=off", "-fno-fast-math",
+            "-fPIC", "-shared", "-pthread", _SRC, "-o", tmp, "-lm",
+        ]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+    lib.oracle_knn.argtypes = [vp, i64, vp, i64, i64, i32, i32, vp, i64, i32, vp, vp]
+    lib.oracle_knn.restype = ctypes.c_int
+    lib.oracle_lof.argtypes = [i64, i32, vp, vp, vp, vp, vp]
+    lib.oracle_lof.restype = ctypes.c_int
+    lib.oracle_lof_rows.argtypes = [vp, i64, i64, i32, vp, i64, i32, vp, vp, vp]
+    lib.oracle_lof_rows.restype = ctypes.c_int
+    lib.oracle_default_threads.argtypes = []
+    lib.oracle_default_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def default_threads() -> int:
+    return int(_load().oracle_default_threads())
+
+
+def _f32(a) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    if a.ndim != 2:
+        raise ValueError("expected a 2-D array")
+    return a
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def knn(xq, xr, k: int, exclude_self: bool = False, rows=None, threads: int = 0):
+    """k nearest references of each query row, sorted by (distance, index)."""
+    xq, xr = _f32(xq), _f32(xr)
+    if xq.shape[1] != xr.shape[1]:
+        raise ValueError("dimension mismatch")
+    lib = _load()
+    if rows is not None:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        m = rows.shape[0]
+    else:
+        m = xq.shape[0]
+    idx = np.empty((m, k), dtype=np.int64)
+    dist = np.empty((m, k), dtype=np.float64)
+    rc = lib.oracle_knn(
+        _ptr(xq), xq.shape[0], _ptr(xr), xr.shape[0], xq.shape[1], int(k), int(bool(exclude_self)),
+        _ptr(rows) if rows is not None else None, m, int(threads), _ptr(idx), _ptr(dist))
+    if rc != 0:
+        raise ValueError("oracle_knn rejected its arguments (rc=%d)" % rc)
+    return idx, dist
+
+
+def knn_self(x, k: int, rows=None, threads: int = 0):
+    """kNN of X against itself with each point's own row excluded."""
+    return knn(x, x, k, exclude_self=True, rows=rows, threads=threads)
+
+
+def knn_score(dist) -> np.ndarray:
+    """kNN outlier score: distance to the k-th nearest neighbour."""
+    return np.asarray(dist)[:, -1].copy()
+
+
+def lof(idx, dist):
+    """LOF of every point from complete kNN lists; returns (lof, lrd, kdist)."""
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    dist = np.ascontiguousarray(dist, dtype=np.float64)
+    n, k = idx.shape
+    out = [np.empty(n, dtype=np.float64) for _ in range(3)]
+    rc = _load().oracle_lof(n, k, _ptr(idx), _ptr(dist), _ptr(out[2]), _ptr(out[1]), _ptr(out[0]))
+    if rc != 0:
+        raise ValueError("oracle_lof failed (rc=%d)" % rc)
+    return out[0], out[1], out[2]
+
+
+def lof_rows(x, k: int, rows, threads: int = 0):
+    """LOF of the listed rows of X, computed from their 2-hop neighbourhoods."""
+    x = _f32(x)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    m = rows.shape[0]
+    out = [np.empty(m, dtype=np.float64) for _ in range(3)]
+    rc = _load().oracle_lof_rows(_ptr(x), x.shape[0], x.shape[1], int(k), _ptr(rows), m,
+                                 int(threads), _ptr(out[0]), _ptr(out[1]), _ptr(out[2]))
+    if rc != 0:
+        raise ValueError("oracle_lof_rows failed (rc=%d)" % rc)
+    return out[0], out[1], out[2]

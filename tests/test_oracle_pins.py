@@ -1,0 +1,265 @@
+"""Pins for the fp64 CPU oracle: it is checked against hand-derived values,
+exact rational brute force, closed forms and invariances, never against
+itself or the HIP path."""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from paper_2110_14007_amd import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _parse_line_fixture():
+    out = {}
+    with open(os.path.join(GOLDEN, "line10.txt")) as f:
+        for raw in f:
+            raw = raw.strip()
+            if not raw or raw.startswith("#"):
+                continue
+            parts = raw.split()
+            k, field, vals = int(parts[0]), parts[1], parts[2:]
+            assert len(vals) == 10
+            if field == "idx":
+                out[(k, field)] = [[int(t) for t in v.split(",")] for v in vals]
+            else:
+                out[(k, field)] = [Fraction(v) for v in vals]
+    return out
+
+
+@pytest.mark.parametrize("k", [2, 3])
+@pytest.mark.parametrize("d", [1, 4])
+def test_line_golden(oracle_mod, k, d):
+    gold = _parse_line_fixture()
+    x = workloads.line(10, d)
+    idx, dist = oracle_mod.knn_self(x, k)
+    assert idx.tolist() == gold[(k, "idx")]
+    assert dist[:, -1].tolist() == [float(v) for v in gold[(k, "kdist")]]
+    lof, lrd, kdist = oracle_mod.lof(idx, dist)
+    np.testing.assert_array_equal(kdist, [float(v) for v in gold[(k, "kdist")]])
+    np.testing.assert_allclose(lrd, [float(v) for v in gold[(k, "lrd")]], rtol=1e-9)
+    np.testing.assert_allclose(lof, [float(v) for v in gold[(k, "lof")]], rtol=1e-9)
+    # The kNN-OD score is the distance to the k-th neighbour.
+    np.testing.assert_array_equal(oracle_mod.knn_score(dist), kdist)
+
+
+def _steps_from_boundary(side, coords):
+    return np.minimum(coords, side - 1 - coords).min(axis=1)
+
+
+@pytest.mark.parametrize("k", [4, 8])
+def test_lattice_closed_forms(oracle_mod, k):
+    side = 9
+    x = workloads.lattice(side, 2)
+    idx, dist = oracle_mod.knn_self(x, k)
+    lof, lrd, kdist = oracle_mod.lof(idx, dist)
+    depth = _steps_from_boundary(side, x.astype(int))
+    r, c = x[:, 0].astype(int), x[:, 1].astype(int)
+    on_row_edge = (r == 0) | (r == side - 1)
+    on_col_edge = (c == 0) | (c == side - 1)
+    corner = on_row_edge & on_col_edge
+    edge = (on_row_edge | on_col_edge) & ~corner
+    interior = depth >= 1
+    if k == 4:
+        # 4 axis neighbours at 1; an edge point has 3 at 1 then diagonals at
+        # sqrt(2); a corner has 2 at 1, one at sqrt(2), then two at 2.
+        np.testing.assert_array_equal(kdist[interior], 1.0)
+        np.testing.assert_array_equal(kdist[edge], math.sqrt(2.0))
+        np.testing.assert_array_equal(kdist[corner], 2.0)
+    else:
+        # 4 at distance 1 and 4 diagonals at sqrt(2) fill k = 8 exactly.
+        np.testing.assert_array_equal(kdist[interior], math.sqrt(2.0))
+    # LOF = 1 wherever the two-hop neighbourhood sees no boundary effect.
+    deep = depth >= 3
+    assert deep.sum() == 9
+    np.testing.assert_allclose(lof[deep], 1.0, rtol=0, atol=1e-12)
+    assert np.all(np.abs(lof[~deep] - 1.0) > 1e-6)
+
+
+def test_lattice_tiebreak_k5(oracle_mod):
+    x = workloads.lattice(9, 2)
+    idx, dist = oracle_mod.knn_self(x, 5)
+    p = 4 * 9 + 4
+    # Axis neighbours (3,4),(4,3),(4,5),(5,4) at 1, then the lowest-index
+    # diagonal (3,3) among four tied at sqrt(2).
+    assert idx[p].tolist() == [31, 39, 41, 49, 30]
+    np.testing.assert_array_equal(dist[p], [1, 1, 1, 1, math.sqrt(2.0)])
+
+
+def test_lattice_3d_k6(oracle_mod):
+    side = 7
+    x = workloads.lattice(side, 3)
+    idx, dist = oracle_mod.knn_self(x, 6)
+    lof, _, kdist = oracle_mod.lof(idx, dist)
+    depth = _steps_from_boundary(side, x.astype(int))
+    np.testing.assert_array_equal(kdist[depth >= 1], 1.0)
+    np.testing.assert_allclose(lof[depth >= 3], 1.0, rtol=0, atol=1e-12)
+    assert np.all(np.abs(lof[depth < 3] - 1.0) > 1e-6)
+
+
+def _exact_knn(xq, xr, k, exclude_self):
+    """Exact rational brute force: every fp32 value is a dyadic rational."""
+    fq = [[Fraction(float(v)) for v in row] for row in xq]
+    fr = [[Fraction(float(v)) for v in row] for row in xr]
+    idx, dist = [], []
+    for i, q in enumerate(fq):
+        cand = []
+        for j, r in enumerate(fr):
+            if exclude_self and i == j:
+                continue
+            cand.append((sum((a - b) * (a - b) for a, b in zip(q, r)), j))
+        cand.sort()
+        idx.append([j for _, j in cand[:k]])
+        dist.append([math.sqrt(float(d2)) for d2, _ in cand[:k]])
+    return np.array(idx), np.array(dist)
+
+
+def _tiny_cases():
+    rng = np.random.default_rng(12345)
+    cases = []
+    for case in range(24):
+        n = int(rng.integers(2, 51))
+        d = int(rng.choice([1, 2, 3, 8]))
+        kind = case % 3
+        if kind == 0:
+            x = rng.standard_normal((n, d)).astype(np.float32)
+        elif kind == 1:  # small integers: many exact ties
+            x = rng.integers(-3, 4, (n, d)).astype(np.float32)
+        else:  # wide dynamic range, duplicates
+            x = (rng.standard_normal((n, d)) * 10.0 ** rng.integers(-3, 4, (n, 1))).astype(
+                np.float32)
+            x[n // 2] = x[0]
+        k = int(rng.integers(1, n))  # 1 .. n-1
+        cases.append((x, k))
+    return cases
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_exact_rational_bruteforce_self(oracle_mod, case):
+    x, k = _tiny_cases()[case]
+    ei, ed = _exact_knn(x, x, k, True)
+    idx, dist = oracle_mod.knn_self(x, k)
+    np.testing.assert_array_equal(idx, ei)
+    np.testing.assert_allclose(dist, ed, rtol=1e-14, atol=0)
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_exact_rational_bruteforce_cross(oracle_mod, case):
+    rng = np.random.default_rng(777 + case)
+    nq, nr = int(rng.integers(1, 30)), int(rng.integers(1, 40))
+    d = int(rng.choice([1, 3, 8]))
+    xq = rng.integers(-2, 3, (nq, d)).astype(np.float32) if case % 2 else \
+        rng.standard_normal((nq, d)).astype(np.float32)
+    xr = rng.integers(-2, 3, (nr, d)).astype(np.float32) if case % 2 else \
+        rng.standard_normal((nr, d)).astype(np.float32)
+    k = int(rng.integers(1, nr + 1))
+    ei, ed = _exact_knn(xq, xr, k, False)
+    idx, dist = oracle_mod.knn(xq, xr, k)
+    np.testing.assert_array_equal(idx, ei)
+    np.testing.assert_allclose(dist, ed, rtol=1e-14, atol=0)
+
+
+def test_one_dimensional_sorted_neighbours(oracle_mod):
+    # In 1-D the k nearest neighbours of a point are a contiguous window of
+    # the sorted order; check the oracle against that textbook property.
+    rng = np.random.default_rng(5)
+    v = rng.permutation(np.arange(200, dtype=np.float32) * 0.37 + rng.random(200).astype(
+        np.float32) * 0.01)
+    x = v[:, None].astype(np.float32)
+    k = 7
+    idx, _ = oracle_mod.knn_self(x, k)
+    order = np.argsort(v, kind="stable")
+    rank = np.empty_like(order)
+    rank[order] = np.arange(len(v))
+    for i in range(len(v)):
+        ranks = np.sort(rank[idx[i]])
+        window = np.concatenate([ranks, [rank[i]]])
+        window.sort()
+        assert window[-1] - window[0] == k  # k neighbours + self are contiguous
+
+
+def test_permutation_invariance(oracle_mod):
+    rng = np.random.default_rng(99)
+    x = rng.standard_normal((300, 5)).astype(np.float32)
+    perm = rng.permutation(300)
+    k = 6
+    idx, dist = oracle_mod.knn_self(x, k)
+    lof, _, _ = oracle_mod.lof(idx, dist)
+    pidx, pdist = oracle_mod.knn_self(x[perm], k)
+    plof, _, _ = oracle_mod.lof(pidx, pdist)
+    # row r of the permuted problem is original row perm[r]
+    np.testing.assert_array_equal(perm[pidx], idx[perm])
+    np.testing.assert_array_equal(pdist, dist[perm])
+    np.testing.assert_allclose(plof, lof[perm], rtol=1e-13)
+
+
+def test_power_of_two_scaling(oracle_mod):
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((250, 7)).astype(np.float32)
+    k = 5
+    idx, dist = oracle_mod.knn_self(x, k)
+    lof, _, _ = oracle_mod.lof(idx, dist)
+    sidx, sdist = oracle_mod.knn_self(x * np.float32(64.0), k)
+    slof, _, _ = oracle_mod.lof(sidx, sdist)
+    np.testing.assert_array_equal(sidx, idx)
+    np.testing.assert_array_equal(sdist, dist * 64.0)
+    np.testing.assert_allclose(slof, lof, rtol=1e-8)
+
+
+def test_duplicates_convention(oracle_mod):
+    # Two coincident points are each other's 1-NN at distance 0: reach is 0
+    # and the 1e-10 guard gives lrd = 1e10 instead of a division by zero.
+    x = np.array([[0, 0], [0, 0], [5, 0], [5, 1], [9, 9]], np.float32)
+    idx, dist = oracle_mod.knn_self(x, 1)
+    assert idx[:2, 0].tolist() == [1, 0]
+    lof, lrd, kdist = oracle_mod.lof(idx, dist)
+    assert kdist[0] == 0.0 and kdist[1] == 0.0
+    np.testing.assert_allclose(lrd[:2], 1e10)
+    np.testing.assert_allclose(lof[:2], 1.0)
+    assert np.all(np.isfinite(lof))
+
+
+def test_lof_rows_matches_full_lists(oracle_mod):
+    x, _ = workloads.generate("C1")
+    k = 10
+    idx, dist = oracle_mod.knn_self(x, k)
+    lof, lrd, kdist = oracle_mod.lof(idx, dist)
+    rows = workloads.sample_rows("C1", count=64)
+    rl, rlrd, rk = oracle_mod.lof_rows(x, k, rows)
+    np.testing.assert_array_equal(rk, kdist[rows])
+    np.testing.assert_array_equal(rlrd, lrd[rows])
+    np.testing.assert_array_equal(rl, lof[rows])
+
+
+def test_outliers_score_high(oracle_mod):
+    # Sanity only (no published value): on C1 the uniform outliers should
+    # dominate the top of both rankings.
+    x, y = workloads.generate("C1")
+    idx, dist = oracle_mod.knn_self(x, 10)
+    score = oracle_mod.knn_score(dist)
+    lof, _, _ = oracle_mod.lof(idx, dist)
+    top = np.argsort(-score)[:100]
+    assert y[top].mean() > 0.9
+    top = np.argsort(-lof)[:100]
+    assert y[top].mean() > 0.8
+
+
+def test_oracle_rejects_bad_arguments(oracle_mod):
+    x = np.zeros((5, 2), np.float32)
+    with pytest.raises(ValueError):
+        oracle_mod.knn_self(x, 5)  # k > n - 1
+    with pytest.raises(ValueError):
+        oracle_mod.knn(x, x, 0)
+
+
+def test_workload_shapes_small():
+    for name in ("C1", "C2", "C3", "C4", "C5"):
+        x, y = workloads.generate(name, n=3000)
+        w = workloads.WORKLOADS[name]
+        assert x.shape == (3000, w.d) and x.dtype == np.float32
+        assert y.shape == (3000,) and 0 < y.sum() < 3000
+        x2, _ = workloads.generate(name, n=3000)
+        np.testing.assert_array_equal(x, x2)
