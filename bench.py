@@ -1,0 +1,148 @@
+"""Throughput of the kNN-OD / LOF hot path on one MI355X.
+
+One step = one tod_lof call on the whole workload: prep, fused distance tiles
+with top-K' selection, certificate + exact recheck, fallback, kNN-OD score
+and LOF for every point.  Inputs are resident in HBM before timing starts.
+
+Prints ONE JSON line (see the design doc for the field definitions).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "kNN-OD scored points/sec and distance-pairs/sec (1 MI355X); % of MFMA/HBM roofline"
+# Peaks used for the roofline fraction (MI355X: 256 CUs x 4 SIMD, 2.4 GHz).
+PEAK_MFMA_F16 = 2500.0      # TFLOP/s, dense fp16 / bf16 MFMA
+PEAK_VALU_F32_FMA = 78.6    # TFLOP/s, non-packed v_fma_f32: 256*4*16 lanes*2 flop*2.4e9
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="C2")
+    ap.add_argument("--precision", default="auto")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="target wall time of the oracle baseline sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(x, k, target_s):
+    """The oracle (exact fp64 brute force) on a bounded sample of query rows."""
+    import numpy as np
+
+    from oracle import oracle
+    n = x.shape[0]
+    rng = np.random.default_rng(2024)
+    rows_done, t_total = 0, 0.0
+    batch = 512
+    while t_total < target_s and rows_done < n:
+        m = min(batch, n - rows_done)
+        rows = np.sort(rng.choice(n, size=m, replace=False)).astype(np.int64)
+        t0 = time.perf_counter()
+        oracle.knn_self(x, k, rows=rows)
+        t_total += time.perf_counter() - t0
+        rows_done += m
+        if t_total < target_s / 8:
+            batch *= 2
+    return {
+        "value": rows_done / t_total,
+        "unit": "points/s",
+        "cores": oracle.default_threads(),
+        "kind": "oracle",
+        "sample": "exact fp64 kNN (k=%d) of %d sampled query rows against all %d reference "
+                  "rows in %.1f s; the LOF tail, O(n k), is excluded" % (k, rows_done, n, t_total),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: --gpus %d is not supported (the path has no "
+              "multi-GPU mode in this build)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2110_14007_amd import tod, workloads
+
+    w = workloads.WORKLOADS[args.workload]
+    x_host, _ = workloads.generate(args.workload)
+    n, d, k = x_host.shape[0], x_host.shape[1], w.k
+    dev = torch.device("cuda:0")
+    x = torch.from_numpy(x_host).to(dev)
+    opts = tod.options(precision=args.precision, query_block=w.query_block)
+    ws = tod.Workspace()
+    out = (torch.empty(n, dtype=torch.float32, device=dev),
+           torch.empty(n, dtype=torch.float32, device=dev))
+    for _ in range(args.warmup):
+        tod.tod_lof(x, k, opts, workspace=ws, out=out)
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        st = tod.new_stats()
+        tod.tod_lof(x, k, opts, workspace=ws, out=out, stats=st)
+        stats.append(st.as_dict())
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    value = n / (ms_step * 1e-3)
+    pairs_s = float(n) * float(n) / (ms_step * 1e-3)
+
+    def avg(key):
+        return float(np.mean([s[key] for s in stats]))
+
+    prec = stats[0]["precision"]
+    launches = stats[0]["tile_launches"]
+    tile_ms = avg("ms_tile") / launches  # average duration of one tile launch
+    flops_per_launch = 2.0 * d * float(n) * float(n) / launches
+    achieved = flops_per_launch / (tile_ms * 1e-3) / 1e12
+    if prec == "fp32":
+        bound, peak = "alu", PEAK_VALU_F32_FMA
+    else:
+        bound, peak = "mfma", PEAK_MFMA_F16
+    roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+                "kernel": "tile_kernel<%s,K'=%d>" % (prec, stats[0]["kprime"]),
+                "launch_ms": round(tile_ms, 4)}
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "points/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+f64" if prec == "fp32" else "%s+f64" % prec.replace("fp", "f"),
+        "data": "synthetic",
+        "config": {"workload": "%s: %s" % (w.name, w.description), "n": n, "d": d, "k": k,
+                   "filter_precision": prec, "kprime": stats[0]["kprime"],
+                   "ref_splits": stats[0]["ref_splits"], "query_block": stats[0]["query_block"],
+                   "parallelism": "single GPU"},
+        "pairs_per_s": pairs_s,
+        "phase_ms": {key: round(avg(key), 4) for key in
+                     ("ms_prep", "ms_tile", "ms_recheck", "ms_fallback", "ms_score", "ms_total")},
+        "rows_fallback": stats[0]["rows_fallback"],
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(x_host, k, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

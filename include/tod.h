@@ -1,0 +1,158 @@
+/*
+ * tod.h - C ABI of libtod, an MI355X (gfx950) implementation of the exact
+ * kNN / LOF outlier-detection hot path of TOD (Zhao, Chen, Jia; arXiv
+ * 2110.14007).
+ *
+ * The library computes, for query rows X_q and reference rows X_r:
+ *   - the k nearest references of every query (the paper's kNN functional
+ *     operator = cdist fused with topk, Sections 4.2 and 6.1), exact under
+ *     the lexicographic key (distance, reference index), so ties go to the
+ *     lower index;
+ *   - the kNN-OD outlier score (distance to the k-th neighbour, Table 1);
+ *   - the LOF outlier score (Table 1; Breunig et al. 2000, with exactly k
+ *     neighbours and lrd = 1 / (mean reach-distance + 1e-10)).
+ *
+ * It follows the paper's provable quantization (Section 5.2): inputs are
+ * quantised (fp32 / fp16 / bf16 after centring and power-of-two scaling),
+ * distances are evaluated in that precision to shortlist K' candidates per
+ * query, a certificate checks that no excluded reference can reach the
+ * exact k-th distance, and rows that fail it are recomputed exactly
+ * (Section 5.2, step iii).  Distances are fused with selection so the n x n
+ * matrix never exists (Section 6.1, operator fusion); queries stream through
+ * in blocks and references in splits (Section 6, automatic batching).
+ *
+ * Conventions shared by every entry point:
+ *   - Every data pointer is a DEVICE pointer (HIP), owned by the caller.
+ *     Inputs are fp32, row-major, contiguous, 16-byte aligned.
+ *   - The library allocates no device memory: the caller passes a workspace
+ *     of at least tod_workspace_size() bytes (256-byte aligned).
+ *   - Distances are Euclidean (not squared).  Index outputs are 0-based rows
+ *     of the reference set.  Output rows are sorted by (distance, index).
+ *   - Arguments are validated on the host before any HIP call; on an
+ *     argument error nothing is launched and outputs are untouched.
+ *   - Calls are blocking: they return after the work queued on `stream`
+ *     (a hipStream_t, or NULL for the default stream) has finished, so the
+ *     returned status is final.  The library keeps no state between calls;
+ *     calls on different streams with different workspaces may overlap.
+ *   - On any error other than TOD_OK, output contents are unspecified.
+ */
+#ifndef TOD_H
+#define TOD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TOD_OK = 0,
+  TOD_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, k out of range, bad struct_size */
+  TOD_ERR_NONFINITE = 2,   /* NaN or Inf in the input (the rounding analysis needs finite data) */
+  TOD_ERR_WORKSPACE = 3,   /* workspace smaller than tod_workspace_size() or misaligned */
+  TOD_ERR_UNSUPPORTED = 4, /* k > 256, d > 4096, or more than 2^31 - 1 rows */
+  TOD_ERR_HIP = 5,         /* a HIP launch or runtime call failed; see tod_last_error() */
+  TOD_ERR_INTERNAL = 6
+} tod_status;
+
+/* Precision of the shortlist filter (the exact recheck always works from the
+ * original fp32 rows with fp64 accumulation). */
+typedef enum {
+  TOD_PREC_AUTO = 0,
+  TOD_PREC_FP32 = 1, /* fp32 FMA distance tile */
+  TOD_PREC_FP16 = 2, /* fp16 MFMA distance tile, fp32 accumulate */
+  TOD_PREC_BF16 = 3  /* bf16 MFMA distance tile, fp32 accumulate */
+} tod_precision;
+
+typedef struct {
+  uint32_t struct_size;  /* must be sizeof(tod_options) */
+  int32_t precision;     /* tod_precision; AUTO picks by d */
+  int32_t exclude_self;  /* tod_knn only: drop reference j == query i (requires xq == xr, nq == nr) */
+  int32_t shortlist;     /* K' (candidates per query kept by the filter); 0 = planner */
+  int64_t query_block;   /* query rows per block (rounded up to 32); 0 = planner */
+  int32_t ref_splits;    /* reference splits processed in parallel; 0 = planner */
+  float margin_scale;    /* >= 1: multiplies every error term of the certificate; 1 = default */
+  int32_t force_fallback;/* debug: treat every row as uncertified (exact recomputation) */
+  int32_t no_recheck;    /* debug: return the filter's shortlist order without verification */
+} tod_options;
+
+/* Plan and per-phase timings of one call (filled when a non-NULL pointer is
+ * passed; timings are measured with HIP events on the call's stream). */
+typedef struct {
+  uint32_t struct_size;   /* must be sizeof(tod_stats) */
+  int32_t precision;      /* resolved tod_precision */
+  int32_t kprime;         /* shortlist length K' */
+  int32_t ref_splits;     /* S */
+  int64_t query_block;    /* B_q */
+  int64_t blocks;         /* number of query blocks */
+  int64_t rows_certified; /* rows whose shortlist passed the certificate */
+  int64_t rows_fallback;  /* rows recomputed exactly */
+  int64_t tile_launches;  /* launches of the fused distance + selection kernel */
+  float ms_prep, ms_tile, ms_recheck, ms_fallback, ms_score, ms_total;
+} tod_stats;
+
+/* Fill *opts with defaults (AUTO precision, planner-chosen sizes). */
+void tod_default_options(tod_options* opts);
+
+/*
+ * Workspace bytes needed by tod_knn (lof = 0) or tod_lof (lof = 1) for these
+ * sizes and options.  Returns 0 if the arguments are invalid or unsupported.
+ */
+size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof,
+                          const tod_options* opts);
+
+/*
+ * kNN: for each of the nq query rows xq[nq x d], the k nearest rows of
+ * xr[nr x d] (Section 4.2, kNN = cdist + topk; exact as in Section 7's
+ * exactness claim).
+ *   idx_out[nq x k]  int64, reference row ids sorted by (distance, id)
+ *   dist_out[nq x k] fp32, Euclidean distances (rounded from fp64)
+ * opts may be NULL (defaults).  stats may be NULL.
+ * Requires 1 <= k <= nr - exclude_self, k <= 256, d <= 4096.
+ */
+tod_status tod_knn(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                   int32_t k, const tod_options* opts, void* workspace, size_t ws_bytes,
+                   void* stream, int64_t* idx_out, float* dist_out, tod_stats* stats);
+
+/*
+ * kNN-OD scores of X against itself (each point's own row excluded):
+ *   score_out[n] = distance to the k-th nearest neighbour (Table 1, kNN).
+ * idx_out[n x k] and dist_out[n x k] are optional (NULL to skip).
+ */
+tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
+                         const tod_options* opts, void* workspace, size_t ws_bytes,
+                         void* stream, float* score_out, int64_t* idx_out, float* dist_out,
+                         tod_stats* stats);
+
+/*
+ * LOF of X against itself (Table 1; Breunig et al. 2000, exactly k
+ * neighbours, self excluded):
+ *   lof_out[n]       fp32 LOF scores (computed in fp64)
+ *   knn_score_out[n] optional: kNN-OD score from the same neighbour lists
+ *   idx_out, dist_out optional neighbour lists as in tod_knn
+ */
+tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
+                   void* workspace, size_t ws_bytes, void* stream, float* lof_out,
+                   float* knn_score_out, int64_t* idx_out, float* dist_out, tod_stats* stats);
+
+/*
+ * Host-only planner (Section 6 automatic batching): fills *plan with the
+ * precision, K', query block, reference splits and block count that tod_knn
+ * would use, without touching the GPU.  Only the plan fields of tod_stats
+ * are written.
+ */
+tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,
+                    tod_stats* plan);
+
+/* Static string naming a status code. */
+const char* tod_status_string(tod_status status);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char* tod_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TOD_H */

@@ -1,0 +1,417 @@
+// Host side of libtod: argument validation, the batching planner, the
+// workspace layout and the launch sequence of one call.
+//
+// One call runs, in stream order:
+//   prep       centre, scale, quantise, norms and radii          (Section 5.2 step i)
+//   per query block (automatic batching, Section 6):
+//     tile     fused distance tile + top-K' per reference split   (Sections 5.2 ii, 6.1)
+//     recheck  merge splits, exact recheck, certificate           (Section 5.2 iii)
+//   fallback   exact scan of rows that failed the certificate     (Section 5.2 iii)
+//   lof        LOF from the exact lists (tod_lof only)            (Table 1)
+// then one stream synchronisation to read the status flags back.
+#include <math.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "tod_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tod_status fail(tod_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+int64_t next_pow2(int64_t v) {
+  int64_t p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+constexpr int64_t kMaxRows = 0x7fffffffLL;
+constexpr int64_t kMaxD = 4096;
+constexpr int32_t kMaxK = 256;
+constexpr int32_t kMaxKPrime = 256;
+
+tod_status resolve_options(const tod_options* in, tod_options* out) {
+  tod_default_options(out);
+  if (!in) return TOD_OK;
+  if (in->struct_size != sizeof(tod_options))
+    return fail(TOD_ERR_INVALID_ARG, "tod_options.struct_size does not match this library");
+  *out = *in;
+  if (out->precision < TOD_PREC_AUTO || out->precision > TOD_PREC_BF16)
+    return fail(TOD_ERR_INVALID_ARG, "unknown precision");
+  if (out->shortlist < 0 || out->shortlist > kMaxKPrime)
+    return fail(TOD_ERR_INVALID_ARG, "shortlist must be in [0, 256]");
+  if (out->query_block < 0) return fail(TOD_ERR_INVALID_ARG, "query_block must be >= 0");
+  if (out->ref_splits < 0 || out->ref_splits > 64)
+    return fail(TOD_ERR_INVALID_ARG, "ref_splits must be in [0, 64]");
+  if (out->margin_scale == 0.0f) out->margin_scale = 1.0f;
+  if (!(out->margin_scale >= 1.0f) || isinf(out->margin_scale))
+    return fail(TOD_ERR_INVALID_ARG, "margin_scale must be a finite value >= 1");
+  return TOD_OK;
+}
+
+tod_status check_sizes(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t excl) {
+  if (nq <= 0 || nr <= 0) return fail(TOD_ERR_INVALID_ARG, "row counts must be positive");
+  if (d <= 0) return fail(TOD_ERR_INVALID_ARG, "d must be positive");
+  if (k <= 0) return fail(TOD_ERR_INVALID_ARG, "k must be positive");
+  if (nq > kMaxRows || nr > kMaxRows)
+    return fail(TOD_ERR_UNSUPPORTED, "more than 2^31 - 1 rows");
+  if (d > kMaxD) return fail(TOD_ERR_UNSUPPORTED, "d > 4096");
+  if (k > kMaxK) return fail(TOD_ERR_UNSUPPORTED, "k > 256");
+  if ((int64_t)k > nr - (excl ? 1 : 0))
+    return fail(TOD_ERR_INVALID_ARG, "k exceeds the number of candidate references");
+  return TOD_OK;
+}
+
+}  // namespace
+
+namespace tod {
+
+tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, int32_t self,
+                     const tod_options& o, Plan* p, const char** why) {
+  *why = "";
+  memset(p, 0, sizeof(*p));
+  p->nq = nq;
+  p->nr = nr;
+  p->d = d;
+  p->k = k;
+  p->lof = lof;
+  p->self = self;
+  p->exclude_self = o.exclude_self ? 1 : 0;
+  // Filter precision: fp32 FMA below d = 64; fp16 MFMA up to 255; bf16 MFMA
+  // from 256 (the contraction is long enough to pay for MFMA tiles).
+  int32_t prec = o.precision;
+  if (prec == TOD_PREC_AUTO) prec = d < 64 ? TOD_PREC_FP32 : (d < 256 ? TOD_PREC_FP16 : TOD_PREC_BF16);
+  p->precision = prec;
+  // Shortlist length K': a power of two >= k with room for the certificate's
+  // margin (k + 4 at fp32, 2k at fp16/bf16).
+  int64_t kp;
+  if (o.shortlist > 0) {
+    kp = o.shortlist;
+  } else {
+    kp = prec == TOD_PREC_FP32 ? k + 4 : 2 * (int64_t)k;
+  }
+  if (kp < k) kp = k;
+  kp = next_pow2(kp < 16 ? 16 : kp);
+  if (kp > kMaxKPrime) kp = kMaxKPrime;
+  p->kprime = (int32_t)kp;
+  p->dpad = (int32_t)round_up(d, prec == TOD_PREC_FP32 ? 4 : 16);
+  p->esize = prec == TOD_PREC_FP32 ? 4 : 2;
+  p->nq_pad = round_up(nq, 32);
+  p->nr_pad = round_up(nr, 32);
+  // Query blocks (Section 6 direct batching along samples).
+  int64_t qb = o.query_block > 0 ? round_up(o.query_block, 32) : p->nq_pad;
+  if (qb > p->nq_pad) qb = p->nq_pad;
+  p->query_block = qb;
+  p->blocks = (nq + qb - 1) / qb;
+  // Reference splits (Section 6 customised cdist batching): enough waves to
+  // fill 256 CUs x 4 SIMDs several times over, but at least 2048 references
+  // per split.
+  const int64_t waves = (qb + 31) / 32;
+  int64_t s;
+  if (o.ref_splits > 0) {
+    s = o.ref_splits;
+  } else {
+    const int64_t target = 8192;
+    s = (target + waves - 1) / waves;
+    const int64_t cap = nr / 2048 > 1 ? nr / 2048 : 1;
+    if (s > cap) s = cap;
+    if (s > 16) s = 16;
+  }
+  if (s < 1) s = 1;
+  int64_t len = round_up((nr + s - 1) / s, 32);
+  s = (nr + len - 1) / len;
+  p->splits = (int32_t)s;
+  p->split_len = len;
+  p->waves_per_group = kp >= 128 ? 1 : 2;
+  return TOD_OK;
+}
+
+Layout make_layout(const Plan& p) {
+  Layout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  L.colpart_blocks = colsum_blocks(p.nr);
+  L.ctrl = take(sizeof(Ctrl));
+  L.mu64 = take(sizeof(double) * p.d);
+  L.mu32 = take(sizeof(float) * p.d);
+  L.colpart = take(sizeof(double) * p.d * L.colpart_blocks);
+  L.xq_r = take((size_t)p.nr_pad * p.dpad * p.esize);
+  L.xq_q = p.self ? L.xq_r : take((size_t)p.nq_pad * p.dpad * p.esize);
+  L.hn_r = take(sizeof(float) * p.nr_pad);
+  L.n64_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
+  L.rho_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
+  L.partial = take(sizeof(uint64_t) * p.query_block * p.splits * p.kprime);
+  L.worklist = take(sizeof(int32_t) * p.nq);
+  if (p.lof) {
+    L.idx32 = take(sizeof(int32_t) * p.nq * p.k);
+    L.d64 = take(sizeof(double) * p.nq * p.k);
+    L.lrd = take(sizeof(double) * p.nq);
+  } else {
+    L.idx32 = L.d64 = L.lrd = 0;
+  }
+  L.total = off;
+  return L;
+}
+
+}  // namespace tod
+
+namespace {
+
+using tod::Args;
+using tod::Layout;
+using tod::Plan;
+
+struct Timers {
+  bool on = false;
+  std::vector<hipEvent_t> ev;
+  hipEvent_t mark(hipStream_t st) {
+    if (!on) return nullptr;
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    (void)hipEventRecord(e, st);
+    ev.push_back(e);
+    return e;
+  }
+  static float ms(hipEvent_t a, hipEvent_t b) {
+    float t = 0.0f;
+    if (a && b && hipEventElapsedTime(&t, a, b) == hipSuccess) return t;
+    return 0.0f;
+  }
+  ~Timers() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  }
+};
+
+tod_status hip_fail(hipError_t e, const char* where) {
+  return fail(TOD_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d, int32_t k,
+               const tod_options* opts_in, int32_t force_excl, int32_t lof, void* ws,
+               size_t ws_bytes, void* stream, int64_t* idx_out, float* dist_out,
+               float* score_out, float* lof_out, tod_stats* stats) {
+  g_last_error.clear();
+  tod_options o;
+  tod_status st = resolve_options(opts_in, &o);
+  if (st != TOD_OK) return st;
+  if (force_excl) o.exclude_self = 1;
+  if (stats && stats->struct_size != sizeof(tod_stats))
+    return fail(TOD_ERR_INVALID_ARG, "tod_stats.struct_size does not match this library");
+  if (!xq || !xr) return fail(TOD_ERR_INVALID_ARG, "null input pointer");
+  if (!ws) return fail(TOD_ERR_INVALID_ARG, "null workspace");
+  st = check_sizes(nq, nr, d, k, o.exclude_self);
+  if (st != TOD_OK) return st;
+  const int32_t self = (xq == xr && nq == nr) ? 1 : 0;
+  if (o.exclude_self && !self)
+    return fail(TOD_ERR_INVALID_ARG, "exclude_self requires the query set to be the reference set");
+  if (((uintptr_t)xq | (uintptr_t)xr) & 15)
+    return fail(TOD_ERR_INVALID_ARG, "input pointers must be 16-byte aligned");
+  if ((uintptr_t)ws & 255) return fail(TOD_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  Plan p;
+  const char* why = "";
+  st = tod::make_plan(nq, nr, d, k, lof, self, o, &p, &why);
+  if (st != TOD_OK) return fail(st, why);
+  const Layout L = tod::make_layout(p);
+  if (ws_bytes < L.total)
+    return fail(TOD_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) +
+                                       " bytes, got " + std::to_string(ws_bytes));
+  char* base = (char*)ws;
+  Args a;
+  memset(&a, 0, sizeof(a));
+  a.xq = xq;
+  a.xr = xr;
+  a.nq = nq;
+  a.nr = nr;
+  a.d = (int32_t)d;
+  a.dpad = p.dpad;
+  a.k = k;
+  a.kprime = p.kprime;
+  a.splits = p.splits;
+  a.split_len = p.split_len;
+  a.exclude_self = p.exclude_self;
+  a.precision = p.precision;
+  a.margin_scale = o.margin_scale;
+  a.force_fallback = o.force_fallback ? 1 : 0;
+  a.no_recheck = o.no_recheck ? 1 : 0;
+  a.ctrl = (tod::Ctrl*)(base + L.ctrl);
+  a.mu64 = (double*)(base + L.mu64);
+  a.mu32 = (float*)(base + L.mu32);
+  a.colpart = (double*)(base + L.colpart);
+  a.xq_r = base + L.xq_r;
+  a.xq_q = base + L.xq_q;
+  a.hn_r = (float*)(base + L.hn_r);
+  a.n64_q = (double*)(base + L.n64_q);
+  a.rho_q = (double*)(base + L.rho_q);
+  a.partial = (uint64_t*)(base + L.partial);
+  a.worklist = (int32_t*)(base + L.worklist);
+  a.idx32 = lof ? (int32_t*)(base + L.idx32) : nullptr;
+  a.d64 = lof ? (double*)(base + L.d64) : nullptr;
+  a.lrd = lof ? (double*)(base + L.lrd) : nullptr;
+  a.idx_out = idx_out;
+  a.dist_out = dist_out;
+  a.score_out = score_out;
+  a.lof_out = lof_out;
+
+  hipStream_t s = (hipStream_t)stream;
+  Timers tm;
+  tm.on = stats != nullptr;
+  hipEvent_t e0 = tm.mark(s);
+  hipError_t he = tod::launch_prep(p, a, s);
+  if (he != hipSuccess) return hip_fail(he, "prep launch");
+  hipEvent_t e_prep = tm.mark(s);
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> tile_ev;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> rc_ev;
+  for (int64_t b = 0; b < p.blocks; ++b) {
+    const int64_t q0 = b * p.query_block;
+    const int64_t rows = nq - q0 < p.query_block ? nq - q0 : p.query_block;
+    hipEvent_t ts = tm.mark(s);
+    he = tod::launch_tile(p, a, q0, rows, s);
+    if (he != hipSuccess) return hip_fail(he, "tile launch");
+    hipEvent_t te = tm.mark(s);
+    he = tod::launch_recheck(p, a, q0, rows, s);
+    if (he != hipSuccess) return hip_fail(he, "recheck launch");
+    hipEvent_t re = tm.mark(s);
+    tile_ev.emplace_back(ts, te);
+    rc_ev.emplace_back(te, re);
+  }
+  hipEvent_t e_rc = tm.mark(s);
+  he = tod::launch_fallback(p, a, s);
+  if (he != hipSuccess) return hip_fail(he, "fallback launch");
+  hipEvent_t e_fb = tm.mark(s);
+  if (lof) {
+    he = tod::launch_lof(p, a, s);
+    if (he != hipSuccess) return hip_fail(he, "lof launch");
+  }
+  hipEvent_t e_end = tm.mark(s);
+  tod::Ctrl host;
+  he = hipMemcpyAsync(&host, a.ctrl, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (he != hipSuccess) return hip_fail(he, "status readback");
+  he = hipStreamSynchronize(s);
+  if (he != hipSuccess) return hip_fail(he, "stream synchronize");
+  if (stats) {
+    stats->precision = p.precision;
+    stats->kprime = p.kprime;
+    stats->ref_splits = p.splits;
+    stats->query_block = p.query_block;
+    stats->blocks = p.blocks;
+    stats->rows_certified = (int64_t)host.certified;
+    stats->rows_fallback = (int64_t)host.worklist_count;
+    stats->tile_launches = p.blocks;
+    stats->ms_prep = Timers::ms(e0, e_prep);
+    float t = 0.0f, r = 0.0f;
+    for (auto& pr : tile_ev) t += Timers::ms(pr.first, pr.second);
+    for (auto& pr : rc_ev) r += Timers::ms(pr.first, pr.second);
+    stats->ms_tile = t;
+    stats->ms_recheck = r;
+    stats->ms_fallback = Timers::ms(e_rc, e_fb);
+    stats->ms_score = Timers::ms(e_fb, e_end);
+    stats->ms_total = Timers::ms(e0, e_end);
+  }
+  if (host.nonfinite) return fail(TOD_ERR_NONFINITE, "input contains NaN or Inf");
+  return TOD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void tod_default_options(tod_options* o) {
+  if (!o) return;
+  memset(o, 0, sizeof(*o));
+  o->struct_size = sizeof(tod_options);
+  o->precision = TOD_PREC_AUTO;
+  o->margin_scale = 1.0f;
+}
+
+size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof,
+                          const tod_options* opts) {
+  tod_options o;
+  if (resolve_options(opts, &o) != TOD_OK) return 0;
+  if (lof) o.exclude_self = 1;
+  if (check_sizes(nq, nr, d, k, o.exclude_self) != TOD_OK) return 0;
+  if (lof && nq != nr) return 0;
+  Plan p;
+  const char* why;
+  // lof = 0 sizes for separate query and reference sets (enough for any
+  // tod_knn / tod_knn_score call); lof = 1 for X against itself.
+  if (tod::make_plan(nq, nr, d, k, lof ? 1 : 0, lof ? 1 : 0, o, &p, &why) != TOD_OK) return 0;
+  return tod::make_layout(p).total;
+}
+
+tod_status tod_knn(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                   int32_t k, const tod_options* opts, void* workspace, size_t ws_bytes,
+                   void* stream, int64_t* idx_out, float* dist_out, tod_stats* stats) {
+  if (!idx_out || !dist_out) return fail(TOD_ERR_INVALID_ARG, "null output pointer");
+  return run(xq, nq, xr, nr, d, k, opts, 0, 0, workspace, ws_bytes, stream, idx_out, dist_out,
+             nullptr, nullptr, stats);
+}
+
+tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
+                         const tod_options* opts, void* workspace, size_t ws_bytes,
+                         void* stream, float* score_out, int64_t* idx_out, float* dist_out,
+                         tod_stats* stats) {
+  if (!score_out) return fail(TOD_ERR_INVALID_ARG, "null score output");
+  return run(x, n, x, n, d, k, opts, 1, 0, workspace, ws_bytes, stream, idx_out, dist_out,
+             score_out, nullptr, stats);
+}
+
+tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
+                   void* workspace, size_t ws_bytes, void* stream, float* lof_out,
+                   float* knn_score_out, int64_t* idx_out, float* dist_out, tod_stats* stats) {
+  if (!lof_out) return fail(TOD_ERR_INVALID_ARG, "null LOF output");
+  return run(x, n, x, n, d, k, opts, 1, 1, workspace, ws_bytes, stream, idx_out, dist_out,
+             knn_score_out, lof_out, stats);
+}
+
+tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,
+                    tod_stats* plan) {
+  g_last_error.clear();
+  if (!plan || plan->struct_size != sizeof(tod_stats))
+    return fail(TOD_ERR_INVALID_ARG, "plan must point to a tod_stats with struct_size set");
+  tod_options o;
+  tod_status st = resolve_options(opts, &o);
+  if (st != TOD_OK) return st;
+  st = check_sizes(nq, nr, d, k, o.exclude_self);
+  if (st != TOD_OK) return st;
+  Plan p;
+  const char* why;
+  st = tod::make_plan(nq, nr, d, k, 0, o.exclude_self ? 1 : 0, o, &p, &why);
+  if (st != TOD_OK) return fail(st, why);
+  plan->precision = p.precision;
+  plan->kprime = p.kprime;
+  plan->ref_splits = p.splits;
+  plan->query_block = p.query_block;
+  plan->blocks = p.blocks;
+  plan->tile_launches = p.blocks;
+  return TOD_OK;
+}
+
+const char* tod_status_string(tod_status s) {
+  switch (s) {
+    case TOD_OK: return "TOD_OK";
+    case TOD_ERR_INVALID_ARG: return "TOD_ERR_INVALID_ARG";
+    case TOD_ERR_NONFINITE: return "TOD_ERR_NONFINITE";
+    case TOD_ERR_WORKSPACE: return "TOD_ERR_WORKSPACE";
+    case TOD_ERR_UNSUPPORTED: return "TOD_ERR_UNSUPPORTED";
+    case TOD_ERR_HIP: return "TOD_ERR_HIP";
+    case TOD_ERR_INTERNAL: return "TOD_ERR_INTERNAL";
+  }
+  return "TOD_ERR_UNKNOWN";
+}
+
+const char* tod_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

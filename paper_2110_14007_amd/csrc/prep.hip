@@ -1,0 +1,216 @@
+// Input quantisation: step (i) of provable quantization (Section 5.2).
+//
+// Every row x is replaced for the filter by xhat = Q(s * (x - mu)), where mu
+// is the fp32-rounded column mean of the references (centring shrinks the
+// norms that enter the rounding bound), s is a power of two that puts
+// max |s (x - mu)| just below 2^14 (exact scaling; Section 5.3 scales the
+// input for the same reason), and Q rounds to the filter precision with
+// values below the smallest normal flushed to zero.  Distances are invariant
+// under the translation and s is exact, so ||x_i - x_j|| * s is exactly the
+// distance between the real vectors c = s (x - mu).
+//
+// Per row the kernel also records, in fp64:
+//   N    = ||xhat||^2                          (query rows: for the certificate)
+//   hn   = -0.5 * fl32(N)                      (reference rows: accumulator seed)
+//   rho  >= ||c - xhat||                       (quantisation radius, rounded up)
+// and over the references the maxima Nmax = max N and Pmax = max rho.
+#include <math.h>
+
+#include "tod_internal.h"
+
+namespace tod {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ void init_ctrl_kernel(Ctrl* ctrl) {
+  uint32_t* w = reinterpret_cast<uint32_t*>(ctrl);
+  for (int i = threadIdx.x; i < (int)(sizeof(Ctrl) / 4); i += blockDim.x) w[i] = 0;
+}
+
+// Column partial sums of the references over contiguous row ranges
+// (deterministic: fixed ranges, fixed reduction order).
+__global__ void __launch_bounds__(kThreads)
+colsum_partial_kernel(const float* __restrict__ x, int64_t n, int d, int64_t rows_per_block,
+                      double* __restrict__ part) {
+  __shared__ double red[kThreads];
+  const int cpp = d < kThreads ? d : kThreads;  // columns per pass
+  const int rsub = kThreads / cpp;              // row lanes per column
+  const int tid = threadIdx.x;
+  const int c_off = tid % cpp, r_off = tid / cpp;
+  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+  const int64_t r1 = r0 + rows_per_block < n ? r0 + rows_per_block : n;
+  for (int cbase = 0; cbase < d; cbase += cpp) {
+    const int c = cbase + c_off;
+    double s = 0.0;
+    if (r_off < rsub && c < d)
+      for (int64_t r = r0 + r_off; r < r1; r += rsub) s += (double)x[r * d + c];
+    red[tid] = s;
+    __syncthreads();
+    if (tid < cpp && cbase + tid < d) {
+      double t = 0.0;
+      for (int i = 0; i < rsub; ++i) t += red[i * cpp + tid];
+      part[(int64_t)blockIdx.x * d + cbase + tid] = t;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void colsum_final_kernel(const double* __restrict__ part, int nb, int d, int64_t n,
+                                    double* __restrict__ mu64, float* __restrict__ mu32) {
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    double t = 0.0;
+    for (int b = 0; b < nb; ++b) t += part[(int64_t)b * d + c];
+    const double m = t / (double)n;
+    mu64[c] = m;
+    mu32[c] = (float)m;
+  }
+}
+
+// max |x - mu| (fp32 bits, rounded up) and the non-finite flag.
+__global__ void __launch_bounds__(kThreads)
+maxabs_kernel(const float* __restrict__ x, int64_t rows, int d, const float* __restrict__ mu32,
+              Ctrl* ctrl) {
+  __shared__ float red[kThreads];
+  float m = 0.0f;
+  bool bad = false;
+  const int64_t total = rows * d;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const float v = x[i];
+    if (!isfinite(v)) {
+      bad = true;
+    } else {
+      const double diff = fabs((double)v - (double)mu32[i % d]);
+      float f = (float)diff;
+      if ((double)f < diff) f = nextafterf(f, INFINITY);
+      m = fmaxf(m, f);
+    }
+  }
+  if (bad) atomicOr(&ctrl->nonfinite, 1u);
+  red[threadIdx.x] = m;
+  __syncthreads();
+  for (int w = kThreads / 2; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + w]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) atomicMax(&ctrl->maxabs_bits, __float_as_uint(red[0]));
+}
+
+template <typename T>
+__device__ __forceinline__ T quantise(double c);
+
+template <>
+__device__ __forceinline__ float quantise<float>(double c) {
+  float f = (float)c;
+  return fabsf(f) < 1.17549435e-38f ? 0.0f : f;
+}
+
+template <>
+__device__ __forceinline__ _Float16 quantise<_Float16>(double c) {
+  _Float16 h = (_Float16)(float)c;
+  return fabsf((float)h) < 6.103515625e-05f ? (_Float16)0.0f : h;
+}
+
+template <>
+__device__ __forceinline__ __bf16 quantise<__bf16>(double c) {
+  __bf16 b = (__bf16)(float)c;
+  return fabsf((float)b) < 1.17549435e-38f ? (__bf16)0.0f : b;
+}
+
+// One thread per row.  Rows in [n, n_pad) are zero-filled so that the tile
+// kernels may read whole 32-row tiles.
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, int dpad,
+                const float* __restrict__ mu32, Ctrl* ctrl, T* __restrict__ xq,
+                float* __restrict__ hn, double* __restrict__ n64, double* __restrict__ rho,
+                int is_ref) {
+  const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= n_pad) return;
+  T* out = xq + row * dpad;
+  if (row >= n) {
+    for (int t = 0; t < dpad; ++t) out[t] = (T)0.0f;
+    if (hn) hn[row] = 0.0f;
+    if (n64) n64[row] = 0.0;
+    if (rho) rho[row] = 0.0;
+    return;
+  }
+  const double s = scale_from_maxabs(ctrl->maxabs_bits);
+  const float* in = x + row * d;
+  double nsq = 0.0, r2 = 0.0, c2 = 0.0;
+  for (int t = 0; t < d; ++t) {
+    const double c = s * ((double)in[t] - (double)mu32[t]);
+    const T q = quantise<T>(c);
+    const double qd = (double)(float)q;
+    out[t] = q;
+    nsq += qd * qd;
+    r2 += (c - qd) * (c - qd);
+    c2 += c * c;
+  }
+  for (int t = d; t < dpad; ++t) out[t] = (T)0.0f;
+  // Round the radius up: covers the fp64 rounding of c and of the sums.
+  const double rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
+  if (is_ref) {
+    hn[row] = -0.5f * (float)nsq;
+    atomicMax((unsigned long long*)&ctrl->nmax_bits, (unsigned long long)__double_as_longlong(nsq));
+    atomicMax((unsigned long long*)&ctrl->pmax_bits,
+              (unsigned long long)__double_as_longlong(rho_up));
+  }
+  if (n64) n64[row] = nsq;
+  if (rho) rho[row] = rho_up;
+}
+
+template <typename T>
+hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
+  const int64_t blocks_r = (p.nr_pad + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_r), dim3(kThreads), 0, st, a.xr,
+                     p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r, a.hn_r,
+                     p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : (double*)nullptr, 1);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.self) return e;
+  const int64_t blocks_q = (p.nq_pad + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_q), dim3(kThreads), 0, st, a.xq,
+                     p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q, (float*)nullptr,
+                     a.n64_q, a.rho_q, 0);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int32_t colsum_blocks(int64_t nr) {
+  int64_t rpb = nr / 1024 + 1;
+  if (rpb < 512) rpb = 512;
+  return (int32_t)((nr + rpb - 1) / rpb);
+}
+
+hipError_t launch_prep(const Plan& p, const Args& a, hipStream_t st) {
+  hipLaunchKernelGGL(init_ctrl_kernel, dim3(1), dim3(64), 0, st, a.ctrl);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int32_t nb = colsum_blocks(p.nr);
+  const int64_t rpb = (p.nr + nb - 1) / nb;
+  hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(kThreads), 0, st, a.xr, p.nr,
+                     (int)p.d, rpb, a.colpart);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3(1), dim3(kThreads), 0, st, a.colpart, nb,
+                     (int)p.d, p.nr, a.mu64, a.mu32);
+  const auto grid_for = [](int64_t total) {
+    int64_t g = (total + kThreads * 4 - 1) / (kThreads * 4);
+    return (unsigned)(g < 1 ? 1 : (g > 4096 ? 4096 : g));
+  };
+  hipLaunchKernelGGL(maxabs_kernel, dim3(grid_for(p.nr * p.d)), dim3(kThreads), 0, st, a.xr,
+                     p.nr, (int)p.d, a.mu32, a.ctrl);
+  if (!p.self)
+    hipLaunchKernelGGL(maxabs_kernel, dim3(grid_for(p.nq * p.d)), dim3(kThreads), 0, st, a.xq,
+                       p.nq, (int)p.d, a.mu32, a.ctrl);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  switch (p.precision) {
+    case TOD_PREC_FP32: return launch_quantise<float>(p, a, st);
+    case TOD_PREC_FP16: return launch_quantise<_Float16>(p, a, st);
+    default: return launch_quantise<__bf16>(p, a, st);
+  }
+}
+
+}  // namespace tod

@@ -1,0 +1,502 @@
+// Fused distance tiles + per-row top-K' selection, certificate with exact
+// recheck, and exact fallback (the kNN functional operator of Section 4.2
+// evaluated with provable quantization, Section 5.2, and operator fusion,
+// Section 6.1).
+//
+// Distance tile.  For query i and reference j the filter ranks
+//     key_ij = fl32(N_j) - 2 <xhat_i, xhat_j>
+// (the right-hand expansion of Eq. (dist-decomp) without the row constant
+// ||xhat_i||^2).  A wave owns 32 queries and walks its reference split in
+// 32-row tiles; each lane ends a tile holding 16 accumulators for one query:
+//     acc = -N_j/2 + <xhat_i, xhat_j>,    key = -2 * acc   (exact scaling).
+// fp16/bf16 use v_mfma_f32_32x32x16_{f16,bf16} (rows = references,
+// columns = queries, fp32 accumulate); fp32 uses VALU FMA chains.
+//
+// Selection.  Each query keeps a sorted list of its K' best (key, index)
+// entries in LDS and a per-lane threshold in acc space.  A tile costs one
+// max-reduction and one compare per lane unless some lane beats its
+// threshold; survivors go to a per-(query, half-wave) LDS queue, and full
+// queues are merged into the lists with wave64 bitonic networks.  The n x n
+// matrix never exists (Section 6.1's fused cdist + topk).
+//
+// Certificate (step iii of Section 5.2, re-derived for top-k).  After the
+// reference splits are merged, the K'-th key h bounds every excluded
+// reference: key_ij >= h.  With the fp32 accumulation bound
+//     |key_ij - (N_j - 2<xhat_i, xhat_j>)| <= gamma_{d+2} (N_i + 2 Nmax) + 2^-23 Nmax
+// and the quantisation radii, every excluded j satisfies
+//     s ||x_i - x_j|| >= sqrt(N_i + h - e) - rho_i - Pmax = LB.
+// The K' candidates are re-measured exactly (fp64 from the original fp32
+// rows, the same direct-difference sum as the definition) and sorted by
+// (D, j); if LB > s * D_(k) no excluded reference can enter the top k and the
+// row is final.  Otherwise the row goes to the exact fallback scan.
+#include <math.h>
+
+#include "tod_internal.h"
+#include "wave.h"
+
+namespace tod {
+
+namespace {
+
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kQueueHalf = 32;   // queue slots per (query, half-wave)
+constexpr int kQueueSlots = 64;  // queue slots per query
+
+// Make this wave's LDS writes visible to its other lanes.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// Reference row (0..31 within the tile) held by accumulator r of `lane`.
+template <int PREC>
+__device__ __forceinline__ int tile_row(int r, int lane) {
+  if constexpr (PREC == TOD_PREC_FP32) {
+    return 16 * (lane >> 5) + r;
+  } else {
+    // 32x32 MFMA accumulator layout: column = lane % 32, row as below.
+    return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+  }
+}
+
+// acc[r] = hn[ref] + <xhat_query, xhat_ref> for this lane's 16 pairs.
+template <int PREC>
+__device__ __forceinline__ void tile_acc(const Args& a, int64_t q0, int64_t t0, int lane,
+                                         float (&acc)[16]) {
+  const int dpad = a.dpad;
+  if constexpr (PREC == TOD_PREC_FP32) {
+    const float* qp = (const float*)a.xq_q + (q0 + (lane & 31)) * dpad;
+    const int64_t rb = t0 + 16 * (lane >> 5);
+    const float* R = (const float*)a.xq_r + rb * dpad;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = a.hn_r[rb + r];
+    for (int kc = 0; kc < dpad; kc += 4) {
+      const float4 qv = *reinterpret_cast<const float4*>(qp + kc);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float4 rv = *reinterpret_cast<const float4*>(R + (int64_t)r * dpad + kc);
+        acc[r] = fmaf(qv.x, rv.x, acc[r]);
+        acc[r] = fmaf(qv.y, rv.y, acc[r]);
+        acc[r] = fmaf(qv.z, rv.z, acc[r]);
+        acc[r] = fmaf(qv.w, rv.w, acc[r]);
+      }
+    }
+  } else {
+    floatx16 c;
+    const float* hn = a.hn_r + t0 + 4 * (lane >> 5);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 v = *reinterpret_cast<const float4*>(hn + 8 * g);
+      c[4 * g + 0] = v.x;
+      c[4 * g + 1] = v.y;
+      c[4 * g + 2] = v.z;
+      c[4 * g + 3] = v.w;
+    }
+    const int64_t roff = (t0 + (lane & 31)) * dpad + 8 * (lane >> 5);
+    const int64_t qoff = (q0 + (lane & 31)) * dpad + 8 * (lane >> 5);
+    if constexpr (PREC == TOD_PREC_FP16) {
+      const _Float16* rp = (const _Float16*)a.xq_r + roff;
+      const _Float16* qp = (const _Float16*)a.xq_q + qoff;
+      for (int kc = 0; kc < dpad; kc += 16) {
+        const half8_t av = *reinterpret_cast<const half8_t*>(rp + kc);
+        const half8_t bv = *reinterpret_cast<const half8_t*>(qp + kc);
+        c = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, c, 0, 0, 0);
+      }
+    } else {
+      const __bf16* rp = (const __bf16*)a.xq_r + roff;
+      const __bf16* qp = (const __bf16*)a.xq_q + qoff;
+      for (int kc = 0; kc < dpad; kc += 16) {
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(rp + kc);
+        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(qp + kc);
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, c, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = c[r];
+  }
+}
+
+// Merge every non-empty queue of this wave's 32 queries into their lists and
+// refresh the thresholds of the lanes that own those queries.
+template <int KP>
+__device__ void flush_all(uint64_t* lbuf, const uint64_t* qbuf, int& cnt, float& thr, int lane) {
+  constexpr int EL = KP >= 64 ? KP / 64 : 1;
+  wave_lds_sync();
+  for (int q = 0; q < 32; ++q) {
+    const int c0 = __shfl(cnt, q, 64);
+    const int c1 = __shfl(cnt, q + 32, 64);
+    if (c0 + c1 == 0) continue;
+    const int pos = lane & 31;
+    uint64_t qe[1];
+    qe[0] = pos < ((lane >> 5) ? c1 : c0) ? qbuf[q * kQueueSlots + lane] : kEmpty;
+    bitonic_sort<1>(qe, lane);
+    uint64_t list[EL];
+#pragma unroll
+    for (int r = 0; r < EL; ++r) {
+      const int e = r * 64 + lane;
+      list[r] = e < KP ? lbuf[q * KP + e] : kEmpty;
+    }
+    merge_queue<EL>(list, qe[0], lane);
+#pragma unroll
+    for (int r = 0; r < EL; ++r) {
+      const int e = r * 64 + lane;
+      if (e < KP) lbuf[q * KP + e] = list[r];
+    }
+    const uint64_t t = shfl64(list[(KP - 1) >> 6], (KP - 1) & 63);
+    const float tv = t == kEmpty ? -INFINITY : -0.5f * key_of(t);
+    if ((lane & 31) == q) {
+      thr = tv;
+      cnt = 0;
+    }
+  }
+  wave_lds_sync();
+}
+
+template <int PREC, int KP, int W>
+__global__ void __launch_bounds__(W * 64)
+tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
+  extern __shared__ uint64_t smem[];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  uint64_t* lbuf = smem + (size_t)wave * (32 * KP + 32 * kQueueSlots);
+  uint64_t* qbuf = lbuf + 32 * KP;
+  if (a.ctrl->nonfinite) return;
+  const int64_t group = (int64_t)blockIdx.x * W + wave;
+  if (group * 32 >= q_rows) return;
+  const int64_t q0 = q_begin + group * 32;
+  const int split = blockIdx.y;
+  const int64_t r_begin = (int64_t)split * a.split_len;
+  const int64_t r_end = r_begin + a.split_len < a.nr ? r_begin + a.split_len : a.nr;
+  for (int i = lane; i < 32 * KP; i += 64) lbuf[i] = kEmpty;
+  wave_lds_sync();
+  float thr = -INFINITY;  // acc-space threshold: a pair survives iff acc > thr
+  int cnt = 0;            // entries in this lane's queue half
+  const int myq = lane & 31;
+  uint64_t* myqueue = qbuf + myq * kQueueSlots + (lane >> 5) * kQueueHalf;
+  const bool selfq = a.exclude_self != 0;
+  for (int64_t t0 = r_begin; t0 < r_end; t0 += 32) {
+    float acc[16];
+    tile_acc<PREC>(a, q0, t0, lane, acc);
+    const bool diag = selfq && t0 == q0;
+    if (diag || t0 + 32 > r_end) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = tile_row<PREC>(r, lane);
+        if (t0 + row >= r_end || (diag && row == myq)) acc[r] = -INFINITY;
+      }
+    }
+    float m = acc[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) m = fmaxf(m, acc[r]);
+    if (__ballot(m > thr)) {
+      // Room for up to 16 more entries in every queue half.
+      if (__ballot(cnt > kQueueHalf - 16)) flush_all<KP>(lbuf, qbuf, cnt, thr, lane);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (acc[r] > thr) {
+          myqueue[cnt] = make_entry(-2.0f * acc[r], (uint32_t)(t0 + tile_row<PREC>(r, lane)));
+          ++cnt;
+        }
+      }
+    }
+  }
+  flush_all<KP>(lbuf, qbuf, cnt, thr, lane);
+  for (int q = 0; q < 32; ++q) {
+    const int64_t ql = group * 32 + q;
+    if (ql >= q_rows) break;
+    uint64_t* dst = a.partial + (ql * a.splits + split) * KP;
+    for (int e = lane; e < KP; e += 64) dst[e] = lbuf[q * KP + e];
+  }
+}
+
+// Squared distance from the original fp32 rows: fp64, direct differences,
+// sequential sum, no fused multiply-add (the definition, evaluated exactly as
+// written).
+__device__ __forceinline__ double exact_d2(const float* __restrict__ p,
+                                           const float* __restrict__ q, int d) {
+#pragma clang fp contract(off)
+  double s = 0.0;
+  for (int t = 0; t < d; ++t) {
+    const double df = (double)p[t] - (double)q[t];
+    const double sq = df * df;
+    s = s + sq;
+  }
+  return s;
+}
+
+// Lower bound test of the certificate (see file header).  Returns true when
+// no reference outside the shortlist can be among the k nearest.
+__device__ bool certified(const Args& a, int64_t qi, uint64_t hent, double tau2) {
+  if (hent == kEmpty) return true;  // the shortlist holds every reference
+  const double h = (double)key_of(hent);
+  const double ni = a.n64_q[qi];
+  const double rho_i = a.rho_q[qi];
+  const double nmax = __longlong_as_double((long long)a.ctrl->nmax_bits);
+  const double pmax = __longlong_as_double((long long)a.ctrl->pmax_bits);
+  const double s = scale_from_maxabs(a.ctrl->maxabs_bits);
+  const double u = 0x1p-23;  // per-addition allowance (2x the fp32 unit roundoff)
+  const double t = (double)a.d + 2.0;
+  const double gam = t * u / (1.0 - t * u);
+  const double ms = (double)a.margin_scale;
+  const double err = ms * (gam * (ni + 2.0 * nmax) * (1.0 + 1e-6) + u * nmax +
+                           (double)a.d * 0x1p-120) +
+                     1e-12 * (ni + fabs(h));
+  const double arg = ni + h - err;
+  const double lb = (arg > 0.0 ? sqrt(arg) : 0.0) - ms * (rho_i + pmax);
+  return lb * (1.0 - 1e-9) > s * sqrt(tau2) * (1.0 + 1e-9);
+}
+
+// Write one neighbour (rank < k) of query qi to every requested output.
+__device__ __forceinline__ void emit(const Args& a, int64_t qi, int rank, uint32_t j, double d2) {
+  const int64_t pos = qi * a.k + rank;
+  const double dd = sqrt(d2);
+  if (a.idx_out) a.idx_out[pos] = (int64_t)j;
+  if (a.dist_out) a.dist_out[pos] = (float)dd;
+  if (a.idx32) {
+    a.idx32[pos] = (int32_t)j;
+    a.d64[pos] = dd;
+  }
+  if (rank == a.k - 1 && a.score_out) a.score_out[qi] = (float)dd;
+}
+
+template <int KP, int W>
+__global__ void __launch_bounds__(W * 64)
+recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
+  constexpr int EL = KP >= 64 ? KP / 64 : 1;
+  __shared__ double sd2[W][KP];
+  __shared__ uint32_t sj[W][KP];
+  __shared__ double stau[W];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t ql = (int64_t)blockIdx.x * W + wave;
+  if (ql >= q_rows || a.ctrl->nonfinite) return;
+  const int64_t qi = q_begin + ql;
+  // Final aggregation of the per-split candidate lists (Section 6.1).
+  const uint64_t* src = a.partial + ql * a.splits * KP;
+  uint64_t list[EL];
+#pragma unroll
+  for (int r = 0; r < EL; ++r) {
+    const int e = r * 64 + lane;
+    list[r] = e < KP ? src[e] : kEmpty;
+  }
+  for (int s = 1; s < a.splits; ++s) {
+    uint64_t other[EL];
+#pragma unroll
+    for (int r = 0; r < EL; ++r) {
+      const int e = r * 64 + lane;
+      other[r] = e < KP ? src[(int64_t)s * KP + e] : kEmpty;
+    }
+    merge_lists<EL>(list, other, lane);
+  }
+  const uint64_t hent = shfl64(list[(KP - 1) >> 6], (KP - 1) & 63);
+  // Exact distances of the candidates.
+  const float* qrow = a.xq + qi * a.d;
+  double myd2[EL];
+  uint32_t myj[EL];
+#pragma unroll
+  for (int r = 0; r < EL; ++r) {
+    const int e = r * 64 + lane;
+    myd2[r] = INFINITY;
+    myj[r] = 0xffffffffu;
+    if (e < KP) {
+      if (list[r] != kEmpty) {
+        myj[r] = index_of(list[r]);
+        myd2[r] = exact_d2(qrow, a.xr + (int64_t)myj[r] * a.d, a.d);
+      }
+      sd2[wave][e] = myd2[r];
+      sj[wave][e] = myj[r];
+    }
+  }
+  wave_lds_sync();
+  // Rank of each candidate under (D^2, j).
+  int rank[EL];
+#pragma unroll
+  for (int r = 0; r < EL; ++r) {
+    const int e = r * 64 + lane;
+    int c = 0;
+    if (a.no_recheck) {
+      c = e;  // debug: keep the filter's order
+    } else if (e < KP) {
+      for (int e2 = 0; e2 < KP; ++e2) {
+        const double o = sd2[wave][e2];
+        const uint32_t oj = sj[wave][e2];
+        c += (o < myd2[r] || (o == myd2[r] && oj < myj[r])) ? 1 : 0;
+      }
+    }
+    rank[r] = c;
+    if (e < KP && c == a.k - 1) stau[wave] = myd2[r];
+  }
+  wave_lds_sync();
+  const double tau2 = stau[wave];
+  bool ok = a.no_recheck ? true : certified(a, qi, hent, tau2);
+  if (a.force_fallback && !a.no_recheck) ok = false;
+  if (ok) {
+#pragma unroll
+    for (int r = 0; r < EL; ++r) {
+      const int e = r * 64 + lane;
+      if (e < KP && rank[r] < a.k) emit(a, qi, rank[r], myj[r], myd2[r]);
+    }
+    if (lane == 0) atomicAdd((unsigned long long*)&a.ctrl->certified, 1ull);
+  } else if (lane == 0) {
+    const uint32_t w = atomicAdd(&a.ctrl->worklist_count, 1u);
+    a.worklist[w] = (int32_t)qi;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exact fallback: a brute-force fp64 scan of every reference for the rows in
+// the worklist ("recalculate on the subset where the verification fails",
+// Section 5.2).  One workgroup per row, grid-strided over the worklist.
+// ---------------------------------------------------------------------------
+constexpr int kFbThreads = 256;
+constexpr int kFbTop = 256;    // sorted best list occupies [0, kFbTop)
+constexpr int kFbSize = 1024;  // candidates are appended in [kFbTop, kFbSize)
+
+__device__ __forceinline__ bool lex_less(uint64_t d1, uint32_t j1, uint64_t d2, uint32_t j2) {
+  return d1 < d2 || (d1 == d2 && j1 < j2);
+}
+
+__device__ void fb_sort(uint64_t* kd, uint32_t* kj) {
+  for (int size = 2; size <= kFbSize; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < kFbSize / 2; i += kFbThreads) {
+        const int lo = 2 * stride * (i / stride) + (i % stride);
+        const int hi = lo + stride;
+        const bool asc = (lo & size) == 0;
+        const bool swap = asc ? lex_less(kd[hi], kj[hi], kd[lo], kj[lo])
+                              : lex_less(kd[lo], kj[lo], kd[hi], kj[hi]);
+        if (swap) {
+          const uint64_t td = kd[lo];
+          kd[lo] = kd[hi];
+          kd[hi] = td;
+          const uint32_t tj = kj[lo];
+          kj[lo] = kj[hi];
+          kj[hi] = tj;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kFbThreads) fallback_kernel(Args a) {
+  __shared__ uint64_t kd[kFbSize];
+  __shared__ uint32_t kj[kFbSize];
+  __shared__ int bufcnt;
+  if (a.ctrl->nonfinite) return;
+  const uint32_t count = a.ctrl->worklist_count;
+  const int tid = threadIdx.x;
+  const int k = a.k;
+  for (uint32_t w = blockIdx.x; w < count; w += gridDim.x) {
+    const int64_t qi = a.worklist[w];
+    for (int i = tid; i < kFbSize; i += kFbThreads) {
+      kd[i] = kEmpty;
+      kj[i] = 0xffffffffu;
+    }
+    if (tid == 0) bufcnt = 0;
+    __syncthreads();
+    uint64_t thr_d = kEmpty;
+    uint32_t thr_j = 0xffffffffu;
+    const float* qrow = a.xq + qi * a.d;
+    for (int64_t base = 0; base < a.nr; base += kFbThreads) {
+      const int64_t j = base + tid;
+      if (j < a.nr && !(a.exclude_self && j == qi)) {
+        const double d2 = exact_d2(qrow, a.xr + j * a.d, a.d);
+        const uint64_t db = (uint64_t)__double_as_longlong(d2);
+        if (lex_less(db, (uint32_t)j, thr_d, thr_j)) {
+          const int slot = atomicAdd(&bufcnt, 1);
+          kd[kFbTop + slot] = db;
+          kj[kFbTop + slot] = (uint32_t)j;
+        }
+      }
+      __syncthreads();
+      const bool last = base + kFbThreads >= a.nr;
+      if (bufcnt > kFbSize - kFbTop - kFbThreads || (last && bufcnt > 0)) {
+        fb_sort(kd, kj);
+        for (int i = k + tid; i < kFbSize; i += kFbThreads) {
+          kd[i] = kEmpty;
+          kj[i] = 0xffffffffu;
+        }
+        thr_d = kd[k - 1];
+        thr_j = kj[k - 1];
+        __syncthreads();
+        if (tid == 0) bufcnt = 0;
+      }
+      __syncthreads();
+    }
+    if (tid < k) emit(a, qi, tid, kj[tid], __longlong_as_double((long long)kd[tid]));
+    __syncthreads();
+  }
+}
+
+template <int PREC, int KP, int W>
+hipError_t launch_tile_t(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                         hipStream_t st) {
+  const size_t lds = (size_t)W * (32 * KP + 32 * kQueueSlots) * sizeof(uint64_t);
+  const auto kern = tile_kernel<PREC, KP, W>;
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t groups = (q_rows + 31) / 32;
+  const dim3 grid((unsigned)((groups + W - 1) / W), (unsigned)p.splits);
+  hipLaunchKernelGGL(kern, grid, dim3(W * 64), lds, st, a, q_begin, q_rows);
+  return hipGetLastError();
+}
+
+template <int PREC>
+hipError_t launch_tile_p(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                         hipStream_t st) {
+  switch (p.kprime) {
+    case 16: return launch_tile_t<PREC, 16, 2>(p, a, q_begin, q_rows, st);
+    case 32: return launch_tile_t<PREC, 32, 2>(p, a, q_begin, q_rows, st);
+    case 64: return launch_tile_t<PREC, 64, 2>(p, a, q_begin, q_rows, st);
+    case 128: return launch_tile_t<PREC, 128, 1>(p, a, q_begin, q_rows, st);
+    case 256: return launch_tile_t<PREC, 256, 1>(p, a, q_begin, q_rows, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int KP>
+hipError_t launch_recheck_t(const Args& a, int64_t q_begin, int64_t q_rows, hipStream_t st) {
+  constexpr int W = 4;
+  const dim3 grid((unsigned)((q_rows + W - 1) / W));
+  hipLaunchKernelGGL((recheck_kernel<KP, W>), grid, dim3(W * 64), 0, st, a, q_begin, q_rows);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                       hipStream_t st) {
+  switch (p.precision) {
+    case TOD_PREC_FP32: return launch_tile_p<TOD_PREC_FP32>(p, a, q_begin, q_rows, st);
+    case TOD_PREC_FP16: return launch_tile_p<TOD_PREC_FP16>(p, a, q_begin, q_rows, st);
+    case TOD_PREC_BF16: return launch_tile_p<TOD_PREC_BF16>(p, a, q_begin, q_rows, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                          hipStream_t st) {
+  switch (p.kprime) {
+    case 16: return launch_recheck_t<16>(a, q_begin, q_rows, st);
+    case 32: return launch_recheck_t<32>(a, q_begin, q_rows, st);
+    case 64: return launch_recheck_t<64>(a, q_begin, q_rows, st);
+    case 128: return launch_recheck_t<128>(a, q_begin, q_rows, st);
+    case 256: return launch_recheck_t<256>(a, q_begin, q_rows, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t st) {
+  int64_t g = p.nq < 2048 ? p.nq : 2048;
+  if (g < 1) g = 1;
+  hipLaunchKernelGGL(fallback_kernel, dim3((unsigned)g), dim3(kFbThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace tod

@@ -1,0 +1,114 @@
+// Internal declarations shared by the host driver (api.cpp) and the HIP
+// kernels of libtod.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/tod.h"
+
+namespace tod {
+
+// ---------------------------------------------------------------------------
+// Plan (automatic batching, Section 6): every size the kernels depend on.
+// ---------------------------------------------------------------------------
+struct Plan {
+  int64_t nq, nr, d;
+  int32_t k;
+  int32_t precision;   // resolved tod_precision (never AUTO)
+  int32_t kprime;      // K' (16, 32, 64, 128 or 256)
+  int32_t splits;      // S: reference splits
+  int64_t split_len;   // references per split (multiple of 32)
+  int64_t query_block; // B_q (multiple of 32)
+  int64_t blocks;      // ceil(nq / B_q)
+  int32_t dpad;        // d rounded up to the filter kernel's K granularity
+  int32_t esize;       // bytes per quantised element (4 or 2)
+  int64_t nq_pad, nr_pad; // row counts padded to 32
+  int32_t waves_per_group; // waves per workgroup of the tile kernel
+  int32_t self;        // query set == reference set (one quantised copy)
+  int32_t exclude_self;
+  int32_t lof;         // LOF buffers needed
+};
+
+// Workspace regions (byte offsets from the workspace base, 256-aligned).
+struct Layout {
+  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, worklist, idx32,
+      d64, lrd, total;
+  int32_t colpart_blocks;
+};
+
+// Control block at the start of the workspace (device side).
+struct Ctrl {
+  uint32_t nonfinite;       // set to 1 if any input value is NaN/Inf
+  uint32_t maxabs_bits;     // max |x - mu| over both sets, fp32 bits (non-negative)
+  uint64_t nmax_bits;       // max ||xhat_j||^2 over references, fp64 bits
+  uint64_t pmax_bits;       // max rho_j over references, fp64 bits
+  uint32_t worklist_count;  // rows appended for exact recomputation
+  uint32_t pad0;
+  uint64_t certified;       // rows certified by the shortlist test
+  uint64_t pad[4];
+};
+
+// Everything a kernel needs to know about the problem.
+struct Args {
+  const float* xq;  // original fp32 queries [nq x d]
+  const float* xr;  // original fp32 references [nr x d]
+  int64_t nq, nr;
+  int32_t d, dpad, k, kprime;
+  int32_t splits;
+  int64_t split_len;
+  int32_t exclude_self;
+  int32_t precision;
+  float margin_scale;
+  int32_t force_fallback, no_recheck;
+  // workspace views
+  Ctrl* ctrl;
+  double* mu64;
+  float* mu32;
+  double* colpart;
+  void* xq_r;       // quantised references [nr_pad x dpad]
+  void* xq_q;       // quantised queries [nq_pad x dpad] (== xq_r when self)
+  float* hn_r;      // -0.5 * fl32(||xhat_j||^2) per reference [nr_pad]
+  double* n64_q;    // ||xhat_i||^2 per query (fp64) [nq_pad]
+  double* rho_q;    // quantisation radius per query, rounded up [nq_pad]
+  double* rho_r_dummy;
+  uint64_t* partial;   // per (query in block, split) sorted K' lists
+  int32_t* worklist;   // global query ids that failed the certificate
+  int32_t* idx32;      // [nq x k] neighbour ids (LOF)
+  double* d64;         // [nq x k] exact distances (LOF)
+  double* lrd;         // [nq] LOF scratch
+  // outputs (nullable)
+  int64_t* idx_out;
+  float* dist_out;
+  float* score_out;
+  float* lof_out;
+};
+
+// Power-of-two scale s with s * maxabs < 2^14 (exact scaling of the centred
+// rows; the fp16 range then holds every quantised value and product).
+__device__ __forceinline__ double scale_from_maxabs(uint32_t bits) {
+  const float m = __uint_as_float(bits);
+  if (!(m > 0.0f)) return 1.0;
+  const int e = isinf(m) ? 128 : ilogbf(m);  // m < 2^(e+1)
+  return ldexp(1.0, 13 - e);
+}
+
+// Number of blocks of the column-mean reduction (also sizes its workspace).
+int32_t colsum_blocks(int64_t nr);
+
+// Kernel launchers (return hipSuccess or the launch error).
+hipError_t launch_prep(const Plan& p, const Args& a, hipStream_t s);
+hipError_t launch_tile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                       hipStream_t s);
+hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                          hipStream_t s);
+hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);
+hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t s);
+
+// Planner and layout (host only, no HIP calls).
+tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, int32_t self,
+                     const tod_options& o, Plan* plan, const char** why);
+Layout make_layout(const Plan& p);
+
+}  // namespace tod

@@ -1,0 +1,272 @@
+"""Python binding of libtod's C ABI (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of its own: torch supplies device memory and the current HIP
+stream; all work runs in the library's HIP kernels.  Importing this module
+raises ImportError if ``libtod.so`` has not been built (there is no CPU or
+PyTorch fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtod.so")
+
+TOD_OK = 0
+TOD_ERR_INVALID_ARG = 1
+TOD_ERR_NONFINITE = 2
+TOD_ERR_WORKSPACE = 3
+TOD_ERR_UNSUPPORTED = 4
+TOD_ERR_HIP = 5
+TOD_ERR_INTERNAL = 6
+
+PREC_AUTO, PREC_FP32, PREC_FP16, PREC_BF16 = 0, 1, 2, 3
+PRECISIONS = {"auto": PREC_AUTO, "fp32": PREC_FP32, "fp16": PREC_FP16, "bf16": PREC_BF16}
+PRECISION_NAMES = {v: k for k, v in PRECISIONS.items()}
+
+SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
+           "tod_plan", "tod_status_string", "tod_last_error")
+
+
+class tod_options(ctypes.Structure):
+    _fields_ = [
+        ("struct_size", ctypes.c_uint32),
+        ("precision", ctypes.c_int32),
+        ("exclude_self", ctypes.c_int32),
+        ("shortlist", ctypes.c_int32),
+        ("query_block", ctypes.c_int64),
+        ("ref_splits", ctypes.c_int32),
+        ("margin_scale", ctypes.c_float),
+        ("force_fallback", ctypes.c_int32),
+        ("no_recheck", ctypes.c_int32),
+    ]
+
+
+class tod_stats(ctypes.Structure):
+    _fields_ = [
+        ("struct_size", ctypes.c_uint32),
+        ("precision", ctypes.c_int32),
+        ("kprime", ctypes.c_int32),
+        ("ref_splits", ctypes.c_int32),
+        ("query_block", ctypes.c_int64),
+        ("blocks", ctypes.c_int64),
+        ("rows_certified", ctypes.c_int64),
+        ("rows_fallback", ctypes.c_int64),
+        ("tile_launches", ctypes.c_int64),
+        ("ms_prep", ctypes.c_float),
+        ("ms_tile", ctypes.c_float),
+        ("ms_recheck", ctypes.c_float),
+        ("ms_fallback", ctypes.c_float),
+        ("ms_score", ctypes.c_float),
+        ("ms_total", ctypes.c_float),
+    ]
+
+    def as_dict(self) -> dict:
+        out = {name: getattr(self, name) for name, _ in self._fields_ if name != "struct_size"}
+        out["precision"] = PRECISION_NAMES.get(self.precision, self.precision)
+        return out
+
+
+class TodError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__("%s failed: %s (%s)" % (where, status_string(status), detail))
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            "libtod.so is not built (expected at %s); run __graft_entry__.build() or "
+            "python paper_2110_14007_amd/build.py" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    opt_p, st_p = ctypes.POINTER(tod_options), ctypes.POINTER(tod_stats)
+    lib.tod_default_options.argtypes = [opt_p]
+    lib.tod_default_options.restype = None
+    lib.tod_workspace_size.argtypes = [i64, i64, i64, i32, i32, opt_p]
+    lib.tod_workspace_size.restype = sz
+    lib.tod_knn.argtypes = [vp, i64, vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, st_p]
+    lib.tod_knn.restype = ctypes.c_int
+    lib.tod_knn_score.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, st_p]
+    lib.tod_knn_score.restype = ctypes.c_int
+    lib.tod_lof.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, vp, st_p]
+    lib.tod_lof.restype = ctypes.c_int
+    lib.tod_plan.argtypes = [i64, i64, i64, i32, opt_p, st_p]
+    lib.tod_plan.restype = ctypes.c_int
+    lib.tod_status_string.argtypes = [ctypes.c_int]
+    lib.tod_status_string.restype = ctypes.c_char_p
+    lib.tod_last_error.argtypes = []
+    lib.tod_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+_lib = _load()
+
+
+def status_string(status: int) -> str:
+    return _lib.tod_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return _lib.tod_last_error().decode()
+
+
+def options(precision="auto", exclude_self=False, shortlist=0, query_block=0, ref_splits=0,
+            margin_scale=1.0, force_fallback=False, no_recheck=False) -> tod_options:
+    o = tod_options()
+    _lib.tod_default_options(ctypes.byref(o))
+    o.precision = PRECISIONS[precision] if isinstance(precision, str) else int(precision)
+    o.exclude_self = int(bool(exclude_self))
+    o.shortlist = int(shortlist)
+    o.query_block = int(query_block)
+    o.ref_splits = int(ref_splits)
+    o.margin_scale = float(margin_scale)
+    o.force_fallback = int(bool(force_fallback))
+    o.no_recheck = int(bool(no_recheck))
+    return o
+
+
+def new_stats() -> tod_stats:
+    s = tod_stats()
+    s.struct_size = ctypes.sizeof(tod_stats)
+    return s
+
+
+def _check(status: int, where: str):
+    if status != TOD_OK:
+        raise TodError(status, where, last_error())
+
+
+def tod_workspace_size(nq: int, nr: int, d: int, k: int, lof: bool = False, opts=None) -> int:
+    return int(_lib.tod_workspace_size(int(nq), int(nr), int(d), int(k), int(bool(lof)),
+                                       ctypes.byref(opts) if opts is not None else None))
+
+
+def tod_plan(nq: int, nr: int, d: int, k: int, opts=None) -> dict:
+    s = new_stats()
+    _check(_lib.tod_plan(int(nq), int(nr), int(d), int(k),
+                         ctypes.byref(opts) if opts is not None else None, ctypes.byref(s)),
+           "tod_plan")
+    return {"precision": PRECISION_NAMES[s.precision], "kprime": s.kprime,
+            "ref_splits": s.ref_splits, "query_block": s.query_block, "blocks": s.blocks}
+
+
+# ---------------------------------------------------------------------------
+# torch-facing wrappers
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev_matrix(x, name):
+    torch = _torch()
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) torch tensor" % name)
+    if x.dtype != torch.float32 or x.dim() != 2 or not x.is_contiguous():
+        raise TypeError("%s must be a contiguous 2-D float32 tensor" % name)
+    return x
+
+
+class Workspace:
+    """Reusable device workspace (torch uint8 buffer, grown on demand)."""
+
+    def __init__(self, device=None):
+        self.buf = None
+        self.device = device
+
+    def get(self, nbytes: int, device):
+        torch = _torch()
+        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != device:
+            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        return self.buf
+
+
+def _ws(workspace, nbytes, device):
+    if workspace is None:
+        workspace = Workspace()
+    buf = workspace.get(nbytes, device)
+    return ctypes.c_void_p(buf.data_ptr()), ctypes.c_size_t(buf.numel())
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _p(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def tod_knn(xq, xr, k: int, opts=None, workspace=None, stream=None, stats=None):
+    """k nearest rows of xr for every row of xq -> (idx int64 [nq,k], dist fp32 [nq,k])."""
+    torch = _torch()
+    _dev_matrix(xq, "xq")
+    _dev_matrix(xr, "xr")
+    nq, d = xq.shape
+    nr = xr.shape[0]
+    if xr.shape[1] != d:
+        raise ValueError("xq and xr must have the same number of columns")
+    idx = torch.empty((nq, k), dtype=torch.int64, device=xq.device)
+    dist = torch.empty((nq, k), dtype=torch.float32, device=xq.device)
+    need = tod_workspace_size(nq, nr, d, k, False, opts)
+    wsp, wsn = _ws(workspace, need, xq.device)
+    st = _lib.tod_knn(_p(xq), nq, _p(xr), nr, d, int(k),
+                      ctypes.byref(opts) if opts is not None else None, wsp, wsn,
+                      _stream(stream), _p(idx), _p(dist),
+                      ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_knn")
+    return idx, dist
+
+
+def tod_knn_score(x, k: int, opts=None, workspace=None, stream=None, stats=None,
+                  return_lists: bool = False):
+    """kNN-OD score of every row of x (self excluded); optionally the lists too."""
+    torch = _torch()
+    _dev_matrix(x, "x")
+    n, d = x.shape
+    score = torch.empty((n,), dtype=torch.float32, device=x.device)
+    idx = dist = None
+    if return_lists:
+        idx = torch.empty((n, k), dtype=torch.int64, device=x.device)
+        dist = torch.empty((n, k), dtype=torch.float32, device=x.device)
+    need = tod_workspace_size(n, n, d, k, False, opts)
+    wsp, wsn = _ws(workspace, need, x.device)
+    st = _lib.tod_knn_score(_p(x), n, d, int(k), ctypes.byref(opts) if opts is not None else None,
+                            wsp, wsn, _stream(stream), _p(score), _p(idx), _p(dist),
+                            ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_knn_score")
+    return (score, idx, dist) if return_lists else score
+
+
+def tod_lof(x, k: int, opts=None, workspace=None, stream=None, stats=None,
+            return_lists: bool = False, out=None):
+    """LOF and kNN-OD scores of every row of x -> (lof fp32 [n], knn_score fp32 [n][, idx, dist])."""
+    torch = _torch()
+    _dev_matrix(x, "x")
+    n, d = x.shape
+    if out is None:
+        lof = torch.empty((n,), dtype=torch.float32, device=x.device)
+        score = torch.empty((n,), dtype=torch.float32, device=x.device)
+    else:
+        lof, score = out
+    idx = dist = None
+    if return_lists:
+        idx = torch.empty((n, k), dtype=torch.int64, device=x.device)
+        dist = torch.empty((n, k), dtype=torch.float32, device=x.device)
+    need = tod_workspace_size(n, n, d, k, True, opts)
+    wsp, wsn = _ws(workspace, need, x.device)
+    st = _lib.tod_lof(_p(x), n, d, int(k), ctypes.byref(opts) if opts is not None else None,
+                      wsp, wsn, _stream(stream), _p(lof), _p(score), _p(idx), _p(dist),
+                      ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_lof")
+    return (lof, score, idx, dist) if return_lists else (lof, score)
+
+
+def raw_library():
+    """The loaded ctypes library (for ABI tests)."""
+    return _lib

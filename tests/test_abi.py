@@ -1,0 +1,119 @@
+"""CPU checks of the C ABI: the library loads, exports every symbol that
+include/tod.h declares, its structs match the binding, and invalid
+arguments are rejected on the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def tod():
+    from paper_2110_14007_amd import tod
+    return tod
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "tod.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tod_[a-z_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(tod):
+    names = _declared_functions()
+    assert {"tod_knn", "tod_knn_score", "tod_lof", "tod_workspace_size"} <= set(names)
+    lib = tod.raw_library()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(tod.SYMBOLS)
+
+
+def test_no_oracle_or_torch_in_library():
+    # The product library links neither the oracle nor torch.
+    import subprocess
+    out = subprocess.run(["ldd", os.path.join(ROOT, "paper_2110_14007_amd", "libtod.so")],
+                         capture_output=True, text=True).stdout
+    assert "oracle" not in out and "torch" not in out and "c10" not in out
+    src = "".join(open(os.path.join(ROOT, "paper_2110_14007_amd", "csrc", f)).read()
+                  for f in os.listdir(os.path.join(ROOT, "paper_2110_14007_amd", "csrc")))
+    assert "oracle" not in src.lower()
+
+
+def test_struct_sizes_match(tod):
+    # tod_plan checks tod_stats.struct_size; tod_options is checked too.
+    plan = tod.tod_plan(1000, 1000, 16, 10, tod.options())
+    assert plan["kprime"] >= 10
+    bad = tod.options()
+    bad.struct_size = 12
+    with pytest.raises(tod.TodError) as e:
+        tod.tod_plan(1000, 1000, 16, 10, bad)
+    assert e.value.status == tod.TOD_ERR_INVALID_ARG
+
+
+def test_status_strings(tod):
+    assert tod.status_string(0) == "TOD_OK"
+    assert tod.status_string(3) == "TOD_ERR_WORKSPACE"
+    assert tod.status_string(99) == "TOD_ERR_UNKNOWN"
+
+
+FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: validation rejects first
+
+
+def _knn(tod, nq=100, nr=100, d=8, k=5, opts=None, ws=FAKE, ws_bytes=1 << 30, xq=FAKE, xr=FAKE,
+         idx=FAKE, dist=FAKE):
+    lib = tod.raw_library()
+    return lib.tod_knn(xq, nq, xr, nr, d, k, ctypes.byref(opts) if opts else None, ws, ws_bytes,
+                       None, idx, dist, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(nq=0), 1), (dict(nr=-1), 1), (dict(d=0), 1), (dict(k=0), 1), (dict(k=101), 1),
+    (dict(k=300, nr=1000), 4), (dict(d=5000), 4), (dict(nq=1 << 31), 4),
+    (dict(xq=None), 1), (dict(idx=None), 1), (dict(dist=None), 1), (dict(ws=None), 1),
+])
+def test_invalid_arguments_rejected(tod, kw, status):
+    assert _knn(tod, **kw) == status
+    assert tod.last_error() != ""
+
+
+def test_exclude_self_needs_same_set(tod):
+    o = tod.options(exclude_self=True)
+    other = ctypes.c_void_p(0x200000)
+    assert _knn(tod, opts=o, xr=other) == tod.TOD_ERR_INVALID_ARG
+    # k = nr is fine without self exclusion but not with it
+    assert _knn(tod, k=100, opts=o) == tod.TOD_ERR_INVALID_ARG
+
+
+def test_bad_options_rejected(tod):
+    for kw in (dict(precision=7), dict(shortlist=300), dict(shortlist=-1), dict(ref_splits=65),
+               dict(margin_scale=0.5), dict(query_block=-3)):
+        o = tod.options()
+        for key, v in kw.items():
+            setattr(o, key, v)
+        assert _knn(tod, opts=o) == tod.TOD_ERR_INVALID_ARG, kw
+
+
+def test_workspace_too_small_and_misaligned(tod):
+    need = tod.tod_workspace_size(100, 100, 8, 5)
+    assert need > 0
+    other = ctypes.c_void_p(0x200000)  # separate query and reference sets
+    assert _knn(tod, xr=other, ws_bytes=need - 1) == tod.TOD_ERR_WORKSPACE
+    assert "workspace too small" in tod.last_error()
+    assert _knn(tod, ws=ctypes.c_void_p(0x100010)) == tod.TOD_ERR_WORKSPACE
+
+
+def test_misaligned_inputs(tod):
+    assert _knn(tod, xq=ctypes.c_void_p(0x100004)) == tod.TOD_ERR_INVALID_ARG
+
+
+def test_score_and_lof_entry_points_validate(tod):
+    lib = tod.raw_library()
+    assert lib.tod_knn_score(FAKE, 100, 8, 5, None, FAKE, 1 << 30, None, None, None, None,
+                             None) == 1
+    assert lib.tod_lof(FAKE, 100, 8, 100, None, FAKE, 1 << 30, None, FAKE, None, None, None,
+                       None) == 1
+    assert lib.tod_lof(FAKE, 100, 8, 5, None, FAKE, 100, None, FAKE, None, None, None,
+                       None) == tod.TOD_ERR_WORKSPACE

@@ -1,0 +1,53 @@
+"""CPU checks of the batching planner (no GPU needed)."""
+import pytest
+
+from paper_2110_14007_amd import workloads
+
+
+@pytest.fixture(scope="module")
+def tod():
+    from paper_2110_14007_amd import tod
+    return tod
+
+
+@pytest.mark.parametrize("name,prec,kp,blocks", [
+    ("C1", "fp32", 16, 1), ("C2", "fp32", 32, 1), ("C3", "fp16", 32, 16), ("C4", "bf16", 128, 1),
+    ("C5", "fp32", 16, 1)])
+def test_plan_of_each_workload(tod, name, prec, kp, blocks):
+    w = workloads.WORKLOADS[name]
+    o = tod.options(exclude_self=True, query_block=w.query_block)
+    p = tod.tod_plan(w.n, w.n, w.d, w.k, o)
+    assert p["precision"] == prec
+    assert p["kprime"] == kp and p["kprime"] >= w.k
+    assert p["blocks"] == blocks
+    if w.query_block:
+        assert p["query_block"] == w.query_block
+    assert 1 <= p["ref_splits"] <= 16
+
+
+def test_explicit_options_respected(tod):
+    o = tod.options(precision="bf16", shortlist=40, query_block=100, ref_splits=5)
+    p = tod.tod_plan(1000, 3000, 20, 7, o)
+    assert p["precision"] == "bf16"
+    assert p["kprime"] == 64  # next power of two >= 40
+    assert p["query_block"] == 128  # rounded up to a multiple of 32
+    assert p["blocks"] == 8
+    assert p["ref_splits"] == 5
+
+
+@pytest.mark.parametrize("k", [1, 5, 20, 64, 100, 200, 256])
+def test_kprime_covers_k(tod, k):
+    for prec in ("fp32", "fp16", "bf16"):
+        p = tod.tod_plan(5000, 5000, 16, k, tod.options(precision=prec))
+        assert k <= p["kprime"] <= 256
+        assert p["kprime"] & (p["kprime"] - 1) == 0
+
+
+def test_workspace_grows_with_problem(tod):
+    a = tod.tod_workspace_size(10000, 10000, 32, 10)
+    b = tod.tod_workspace_size(20000, 20000, 32, 10)
+    c = tod.tod_workspace_size(20000, 20000, 32, 10, lof=True)
+    assert 0 < a < b
+    assert c > 0
+    assert tod.tod_workspace_size(10, 10, 4, 11) == 0  # k > nr
+    assert tod.tod_workspace_size(10, 12, 4, 5, lof=True) == 0  # LOF needs nq == nr
