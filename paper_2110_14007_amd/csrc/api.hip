@@ -103,7 +103,17 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   kp = next_pow2(kp < 16 ? 16 : kp);
   if (kp > kMaxKPrime) kp = kMaxKPrime;
   p->kprime = (int32_t)kp;
-  p->dpad = (int32_t)round_up(d, prec == TOD_PREC_FP32 ? 4 : 16);
+  // Row stride of the quantised copies.  Small rows are padded to a power of
+  // two so that the tile kernel can keep the query operand in registers.
+  if (prec == TOD_PREC_FP32) {
+    const int64_t dp = round_up(d, 4);
+    p->dpad_t = dp <= 64 ? (int32_t)next_pow2(dp < 8 ? 8 : dp) : 0;
+    p->dpad = p->dpad_t ? p->dpad_t : (int32_t)dp;
+  } else {
+    const int64_t dp = round_up(d, 16);
+    p->dpad_t = dp <= 128 ? (int32_t)next_pow2(dp) : 0;
+    p->dpad = p->dpad_t ? p->dpad_t : (int32_t)dp;
+  }
   p->esize = prec == TOD_PREC_FP32 ? 4 : 2;
   p->nq_pad = round_up(nq, 32);
   p->nr_pad = round_up(nr, 32);
@@ -112,15 +122,16 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   if (qb > p->nq_pad) qb = p->nq_pad;
   p->query_block = qb;
   p->blocks = (nq + qb - 1) / qb;
-  // Reference splits (Section 6 customised cdist batching): enough waves to
-  // fill 256 CUs x 4 SIMDs several times over, but at least 2048 references
-  // per split.
+  // Reference splits (Section 6 customised cdist batching): enough waves for
+  // two per SIMD on 256 CUs x 4 SIMDs, but at least 2048 references per
+  // split (every split keeps its own K' list per query, so splits cost
+  // selection work).
   const int64_t waves = (qb + 31) / 32;
   int64_t s;
   if (o.ref_splits > 0) {
     s = o.ref_splits;
   } else {
-    const int64_t target = 8192;
+    const int64_t target = 2048;
     s = (target + waves - 1) / waves;
     const int64_t cap = nr / 2048 > 1 ? nr / 2048 : 1;
     if (s > cap) s = cap;
@@ -131,7 +142,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   s = (nr + len - 1) / len;
   p->splits = (int32_t)s;
   p->split_len = len;
-  p->waves_per_group = kp >= 128 ? 1 : 2;
+  p->waves_per_group = kp <= 32 ? 4 : (kp == 64 ? 2 : 1);
   return TOD_OK;
 }
 

@@ -38,178 +38,13 @@ namespace tod {
 
 namespace {
 
-typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kQueueHalf = 32;   // queue slots per (query, half-wave)
-constexpr int kQueueSlots = 64;  // queue slots per query
 
 // Make this wave's LDS writes visible to its other lanes.
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-}
-
-// Reference row (0..31 within the tile) held by accumulator r of `lane`.
-template <int PREC>
-__device__ __forceinline__ int tile_row(int r, int lane) {
-  if constexpr (PREC == TOD_PREC_FP32) {
-    return 16 * (lane >> 5) + r;
-  } else {
-    // 32x32 MFMA accumulator layout: column = lane % 32, row as below.
-    return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-  }
-}
-
-// acc[r] = hn[ref] + <xhat_query, xhat_ref> for this lane's 16 pairs.
-template <int PREC>
-__device__ __forceinline__ void tile_acc(const Args& a, int64_t q0, int64_t t0, int lane,
-                                         float (&acc)[16]) {
-  const int dpad = a.dpad;
-  if constexpr (PREC == TOD_PREC_FP32) {
-    const float* qp = (const float*)a.xq_q + (q0 + (lane & 31)) * dpad;
-    const int64_t rb = t0 + 16 * (lane >> 5);
-    const float* R = (const float*)a.xq_r + rb * dpad;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = a.hn_r[rb + r];
-    for (int kc = 0; kc < dpad; kc += 4) {
-      const float4 qv = *reinterpret_cast<const float4*>(qp + kc);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float4 rv = *reinterpret_cast<const float4*>(R + (int64_t)r * dpad + kc);
-        acc[r] = fmaf(qv.x, rv.x, acc[r]);
-        acc[r] = fmaf(qv.y, rv.y, acc[r]);
-        acc[r] = fmaf(qv.z, rv.z, acc[r]);
-        acc[r] = fmaf(qv.w, rv.w, acc[r]);
-      }
-    }
-  } else {
-    floatx16 c;
-    const float* hn = a.hn_r + t0 + 4 * (lane >> 5);
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const float4 v = *reinterpret_cast<const float4*>(hn + 8 * g);
-      c[4 * g + 0] = v.x;
-      c[4 * g + 1] = v.y;
-      c[4 * g + 2] = v.z;
-      c[4 * g + 3] = v.w;
-    }
-    const int64_t roff = (t0 + (lane & 31)) * dpad + 8 * (lane >> 5);
-    const int64_t qoff = (q0 + (lane & 31)) * dpad + 8 * (lane >> 5);
-    if constexpr (PREC == TOD_PREC_FP16) {
-      const _Float16* rp = (const _Float16*)a.xq_r + roff;
-      const _Float16* qp = (const _Float16*)a.xq_q + qoff;
-      for (int kc = 0; kc < dpad; kc += 16) {
-        const half8_t av = *reinterpret_cast<const half8_t*>(rp + kc);
-        const half8_t bv = *reinterpret_cast<const half8_t*>(qp + kc);
-        c = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, c, 0, 0, 0);
-      }
-    } else {
-      const __bf16* rp = (const __bf16*)a.xq_r + roff;
-      const __bf16* qp = (const __bf16*)a.xq_q + qoff;
-      for (int kc = 0; kc < dpad; kc += 16) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t*>(rp + kc);
-        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(qp + kc);
-        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, c, 0, 0, 0);
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = c[r];
-  }
-}
-
-// Merge every non-empty queue of this wave's 32 queries into their lists and
-// refresh the thresholds of the lanes that own those queries.
-template <int KP>
-__device__ void flush_all(uint64_t* lbuf, const uint64_t* qbuf, int& cnt, float& thr, int lane) {
-  constexpr int EL = KP >= 64 ? KP / 64 : 1;
-  wave_lds_sync();
-  for (int q = 0; q < 32; ++q) {
-    const int c0 = __shfl(cnt, q, 64);
-    const int c1 = __shfl(cnt, q + 32, 64);
-    if (c0 + c1 == 0) continue;
-    const int pos = lane & 31;
-    uint64_t qe[1];
-    qe[0] = pos < ((lane >> 5) ? c1 : c0) ? qbuf[q * kQueueSlots + lane] : kEmpty;
-    bitonic_sort<1>(qe, lane);
-    uint64_t list[EL];
-#pragma unroll
-    for (int r = 0; r < EL; ++r) {
-      const int e = r * 64 + lane;
-      list[r] = e < KP ? lbuf[q * KP + e] : kEmpty;
-    }
-    merge_queue<EL>(list, qe[0], lane);
-#pragma unroll
-    for (int r = 0; r < EL; ++r) {
-      const int e = r * 64 + lane;
-      if (e < KP) lbuf[q * KP + e] = list[r];
-    }
-    const uint64_t t = shfl64(list[(KP - 1) >> 6], (KP - 1) & 63);
-    const float tv = t == kEmpty ? -INFINITY : -0.5f * key_of(t);
-    if ((lane & 31) == q) {
-      thr = tv;
-      cnt = 0;
-    }
-  }
-  wave_lds_sync();
-}
-
-template <int PREC, int KP, int W>
-__global__ void __launch_bounds__(W * 64)
-tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
-  extern __shared__ uint64_t smem[];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  uint64_t* lbuf = smem + (size_t)wave * (32 * KP + 32 * kQueueSlots);
-  uint64_t* qbuf = lbuf + 32 * KP;
-  if (a.ctrl->nonfinite) return;
-  const int64_t group = (int64_t)blockIdx.x * W + wave;
-  if (group * 32 >= q_rows) return;
-  const int64_t q0 = q_begin + group * 32;
-  const int split = blockIdx.y;
-  const int64_t r_begin = (int64_t)split * a.split_len;
-  const int64_t r_end = r_begin + a.split_len < a.nr ? r_begin + a.split_len : a.nr;
-  for (int i = lane; i < 32 * KP; i += 64) lbuf[i] = kEmpty;
-  wave_lds_sync();
-  float thr = -INFINITY;  // acc-space threshold: a pair survives iff acc > thr
-  int cnt = 0;            // entries in this lane's queue half
-  const int myq = lane & 31;
-  uint64_t* myqueue = qbuf + myq * kQueueSlots + (lane >> 5) * kQueueHalf;
-  const bool selfq = a.exclude_self != 0;
-  for (int64_t t0 = r_begin; t0 < r_end; t0 += 32) {
-    float acc[16];
-    tile_acc<PREC>(a, q0, t0, lane, acc);
-    const bool diag = selfq && t0 == q0;
-    if (diag || t0 + 32 > r_end) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = tile_row<PREC>(r, lane);
-        if (t0 + row >= r_end || (diag && row == myq)) acc[r] = -INFINITY;
-      }
-    }
-    float m = acc[0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) m = fmaxf(m, acc[r]);
-    if (__ballot(m > thr)) {
-      // Room for up to 16 more entries in every queue half.
-      if (__ballot(cnt > kQueueHalf - 16)) flush_all<KP>(lbuf, qbuf, cnt, thr, lane);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (acc[r] > thr) {
-          myqueue[cnt] = make_entry(-2.0f * acc[r], (uint32_t)(t0 + tile_row<PREC>(r, lane)));
-          ++cnt;
-        }
-      }
-    }
-  }
-  flush_all<KP>(lbuf, qbuf, cnt, thr, lane);
-  for (int q = 0; q < 32; ++q) {
-    const int64_t ql = group * 32 + q;
-    if (ql >= q_rows) break;
-    uint64_t* dst = a.partial + (ql * a.splits + split) * KP;
-    for (int e = lane; e < KP; e += 64) dst[e] = lbuf[q * KP + e];
-  }
 }
 
 // Squared distance from the original fp32 rows: fp64, direct differences,
@@ -431,35 +266,6 @@ __global__ void __launch_bounds__(kFbThreads) fallback_kernel(Args a) {
   }
 }
 
-template <int PREC, int KP, int W>
-hipError_t launch_tile_t(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                         hipStream_t st) {
-  const size_t lds = (size_t)W * (32 * KP + 32 * kQueueSlots) * sizeof(uint64_t);
-  const auto kern = tile_kernel<PREC, KP, W>;
-  if (lds > 65536) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  const int64_t groups = (q_rows + 31) / 32;
-  const dim3 grid((unsigned)((groups + W - 1) / W), (unsigned)p.splits);
-  hipLaunchKernelGGL(kern, grid, dim3(W * 64), lds, st, a, q_begin, q_rows);
-  return hipGetLastError();
-}
-
-template <int PREC>
-hipError_t launch_tile_p(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                         hipStream_t st) {
-  switch (p.kprime) {
-    case 16: return launch_tile_t<PREC, 16, 2>(p, a, q_begin, q_rows, st);
-    case 32: return launch_tile_t<PREC, 32, 2>(p, a, q_begin, q_rows, st);
-    case 64: return launch_tile_t<PREC, 64, 2>(p, a, q_begin, q_rows, st);
-    case 128: return launch_tile_t<PREC, 128, 1>(p, a, q_begin, q_rows, st);
-    case 256: return launch_tile_t<PREC, 256, 1>(p, a, q_begin, q_rows, st);
-    default: return hipErrorInvalidValue;
-  }
-}
-
 template <int KP>
 hipError_t launch_recheck_t(const Args& a, int64_t q_begin, int64_t q_rows, hipStream_t st) {
   constexpr int W = 4;
@@ -473,9 +279,9 @@ hipError_t launch_recheck_t(const Args& a, int64_t q_begin, int64_t q_rows, hipS
 hipError_t launch_tile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                        hipStream_t st) {
   switch (p.precision) {
-    case TOD_PREC_FP32: return launch_tile_p<TOD_PREC_FP32>(p, a, q_begin, q_rows, st);
-    case TOD_PREC_FP16: return launch_tile_p<TOD_PREC_FP16>(p, a, q_begin, q_rows, st);
-    case TOD_PREC_BF16: return launch_tile_p<TOD_PREC_BF16>(p, a, q_begin, q_rows, st);
+    case TOD_PREC_FP32: return launch_tile_f32(p, a, q_begin, q_rows, st);
+    case TOD_PREC_FP16: return launch_tile_f16(p, a, q_begin, q_rows, st);
+    case TOD_PREC_BF16: return launch_tile_bf16(p, a, q_begin, q_rows, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -22,7 +22,9 @@ struct Plan {
   int64_t split_len;   // references per split (multiple of 32)
   int64_t query_block; // B_q (multiple of 32)
   int64_t blocks;      // ceil(nq / B_q)
-  int32_t dpad;        // d rounded up to the filter kernel's K granularity
+  int32_t dpad;        // row stride of the quantised copies (elements)
+  int32_t dpad_t;      // tile kernel specialisation: dpad if the query operand fits in
+                       // registers (fp32: 8..64, fp16/bf16: 16..128), else 0
   int32_t esize;       // bytes per quantised element (4 or 2)
   int64_t nq_pad, nr_pad; // row counts padded to 32
   int32_t waves_per_group; // waves per workgroup of the tile kernel
@@ -101,6 +103,12 @@ int32_t colsum_blocks(int64_t nr);
 hipError_t launch_prep(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_tile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                        hipStream_t s);
+hipError_t launch_tile_f32(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                           hipStream_t s);
+hipError_t launch_tile_f16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                           hipStream_t s);
+hipError_t launch_tile_bf16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                            hipStream_t s);
 hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                           hipStream_t s);
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);
