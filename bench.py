@@ -34,7 +34,29 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle baseline sample")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="instead of the benchmark, run a plain device-to-device copy of this "
+                         "many MiB (calibrates the HBM byte counters against a known size)")
     return ap.parse_args()
+
+
+def copy_calibration(mib, steps):
+    """A plain copy kernel of known size: reads and writes mib MiB per launch."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.arange(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    print(json.dumps({"copy_mib": mib, "bytes_read": n * 4, "bytes_written": n * 4,
+                      "ms_per_copy": round(ms, 4),
+                      "GB_s": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
 def cpu_baseline(x, k, target_s):
@@ -71,6 +93,9 @@ def main():
         print("bench.py measures one GPU only: --gpus %d is not supported (the path has no "
               "multi-GPU mode in this build)" % args.gpus, file=sys.stderr)
         sys.exit(2)
+    if args.copy_mib:
+        copy_calibration(args.copy_mib, args.steps)
+        return
     import numpy as np
     import torch
 
