@@ -21,7 +21,7 @@ if ROOT not in sys.path:
 METRIC = "kNN-OD scored points/sec and distance-pairs/sec (1 MI355X); % of MFMA/HBM roofline"
 # Peaks used for the roofline fraction (MI355X: 256 CUs x 4 SIMD, 2.4 GHz).
 PEAK_MFMA_F16 = 2500.0      # TFLOP/s, dense fp16 / bf16 MFMA
-PEAK_VALU_F32_FMA = 78.6    # TFLOP/s, non-packed v_fma_f32: 256*4*16 lanes*2 flop*2.4e9
+PEAK_VALU_F32 = 157.3       # TFLOP/s, published fp32 vector peak (packed FMA)
 
 
 def parse():
@@ -60,31 +60,66 @@ def copy_calibration(mib, steps):
 
 
 def cpu_baseline(x, k, target_s):
-    """The oracle (exact fp64 brute force) on a bounded sample of query rows."""
+    """The oracle (exact fp64 brute force) on a bounded sample of query rows.
+
+    Rows are taken in a seeded random order without repetition, in batches
+    that double until about target_s seconds of oracle time have been spent.
+    """
     import numpy as np
 
     from oracle import oracle
     n = x.shape[0]
-    rng = np.random.default_rng(2024)
+    order = np.random.default_rng(2024).permutation(n).astype(np.int64)
     rows_done, t_total = 0, 0.0
-    batch = 512
+    batch = 256
     while t_total < target_s and rows_done < n:
         m = min(batch, n - rows_done)
-        rows = np.sort(rng.choice(n, size=m, replace=False)).astype(np.int64)
+        rows = np.sort(order[rows_done:rows_done + m])
         t0 = time.perf_counter()
         oracle.knn_self(x, k, rows=rows)
         t_total += time.perf_counter() - t0
         rows_done += m
-        if t_total < target_s / 8:
+        if t_total < target_s / 4:
             batch *= 2
     return {
         "value": rows_done / t_total,
         "unit": "points/s",
         "cores": oracle.default_threads(),
         "kind": "oracle",
-        "sample": "exact fp64 kNN (k=%d) of %d sampled query rows against all %d reference "
-                  "rows in %.1f s; the LOF tail, O(n k), is excluded" % (k, rows_done, n, t_total),
+        "sample": "exact fp64 kNN (k=%d) of %d distinct seeded-random query rows against all %d "
+                  "reference rows, %.1f s of oracle time; the O(n k) LOF tail is not timed"
+                  % (k, rows_done, n, t_total),
     }
+
+
+def kernel_sources_digest():
+    """sha256 over the HIP sources; a counter record applies only to this digest."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2110_14007_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        h.update(name.encode())
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when the summary is missing or was taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", "hbm_counters_%s.txt" % workload)
+    if not os.path.exists(path):
+        return None
+    digest, traffic = None, None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("csrc_sha256:"):
+                digest = line.split()[1]
+            elif line.startswith("traffic_bytes_per_launch:") and kernel in line:
+                traffic = float(line.split()[1])
+    if digest != kernel_sources_digest():
+        return None
+    return traffic
 
 
 def main():
@@ -134,13 +169,14 @@ def main():
     flops_per_launch = 2.0 * d * float(n) * float(n) / launches
     achieved = flops_per_launch / (tile_ms * 1e-3) / 1e12
     if prec == "fp32":
-        bound, peak = "alu", PEAK_VALU_F32_FMA
+        bound, peak = "alu", PEAK_VALU_F32
     else:
         bound, peak = "mfma", PEAK_MFMA_F16
+    kname = "tile_kernel<%s,K'=%d>" % (prec, stats[0]["kprime"])
     roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
-                "kernel": "tile_kernel<%s,K'=%d>" % (prec, stats[0]["kprime"]),
-                "launch_ms": round(tile_ms, 4)}
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                "traffic": recorded_traffic(args.workload, kname),
+                "kernel": kname, "launch_ms": round(tile_ms, 4)}
     line = {
         "metric": METRIC,
         "value": round(value, 1),
