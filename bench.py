@@ -172,7 +172,7 @@ def main():
         bound, peak = "alu", PEAK_VALU_F32
     else:
         bound, peak = "mfma", PEAK_MFMA_F16
-    kname = "tile_kernel<%s,K'=%d>" % (prec, stats[0]["kprime"])
+    kname = "tile<%s,K'=%d>" % (prec, stats[0]["kprime"])
     roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak,
                 "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                 "traffic": recorded_traffic(args.workload, kname),

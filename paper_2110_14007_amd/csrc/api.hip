@@ -86,18 +86,24 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   p->lof = lof;
   p->self = self;
   p->exclude_self = o.exclude_self ? 1 : 0;
-  // Filter precision: fp32 FMA below d = 64; fp16 MFMA up to 255; bf16 MFMA
-  // from 256 (the contraction is long enough to pay for MFMA tiles).
+  // Filter precision (provable quantization, Section 5.2 step ii).  Up to
+  // d = 128 the fp16 MFMA filter with the register-resident shortlist is the
+  // fastest exact path at every size measured; above, the bf16 MFMA filter.
   int32_t prec = o.precision;
-  if (prec == TOD_PREC_AUTO) prec = d < 64 ? TOD_PREC_FP32 : (d < 256 ? TOD_PREC_FP16 : TOD_PREC_BF16);
+  if (prec == TOD_PREC_AUTO) prec = d <= 128 ? TOD_PREC_FP16 : TOD_PREC_BF16;
   p->precision = prec;
   // Shortlist length K': a power of two >= k with room for the certificate's
-  // margin (k + 4 at fp32, 2k at fp16/bf16).
+  // margin.  The margin a row needs grows with the filter's rounding error:
+  // k + 4 at fp32, k + max(8, k/4) at fp16, 2k at bf16.
   int64_t kp;
   if (o.shortlist > 0) {
     kp = o.shortlist;
+  } else if (prec == TOD_PREC_FP32) {
+    kp = k + 4;
+  } else if (prec == TOD_PREC_FP16) {
+    kp = k + (k / 4 > 8 ? (k + 3) / 4 : 8);
   } else {
-    kp = prec == TOD_PREC_FP32 ? k + 4 : 2 * (int64_t)k;
+    kp = 2 * (int64_t)k;
   }
   if (kp < k) kp = k;
   kp = next_pow2(kp < 16 ? 16 : kp);
@@ -143,6 +149,10 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   p->splits = (int32_t)s;
   p->split_len = len;
   p->waves_per_group = kp <= 32 ? 4 : (kp == 64 ? 2 : 1);
+  // The register-list MFMA kernel covers fp16 / bf16 filters whose query
+  // operand fits in registers and whose shortlist is 16, 32 or 64 long.
+  p->tile_kind = (prec != TOD_PREC_FP32 && p->dpad_t != 0 && kp <= 64) ? 1 : 0;
+  if (p->tile_kind == 1) p->waves_per_group = 4;
   return TOD_OK;
 }
 
@@ -166,6 +176,10 @@ Layout make_layout(const Plan& p) {
   L.rho_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
   L.partial = take(sizeof(uint64_t) * p.query_block * p.splits * p.kprime);
   L.worklist = take(sizeof(int32_t) * p.nq);
+  // Chunk lists exist only when fewer than kFbGrid rows fail, so kFbGrid
+  // lists of k entries always suffice.
+  L.fbpart = take(sizeof(uint2) * (size_t)tod::kFbGrid * p.k);
+  L.fbidx = take(sizeof(uint32_t) * (size_t)tod::kFbGrid * p.k);
   if (p.lof) {
     L.idx32 = take(sizeof(int32_t) * p.nq * p.k);
     L.d64 = take(sizeof(double) * p.nq * p.k);
@@ -268,6 +282,8 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.rho_q = (double*)(base + L.rho_q);
   a.partial = (uint64_t*)(base + L.partial);
   a.worklist = (int32_t*)(base + L.worklist);
+  a.fbpart = (uint2*)(base + L.fbpart);
+  a.fbidx = (uint32_t*)(base + L.fbidx);
   a.idx32 = lof ? (int32_t*)(base + L.idx32) : nullptr;
   a.d64 = lof ? (double*)(base + L.d64) : nullptr;
   a.lrd = lof ? (double*)(base + L.lrd) : nullptr;

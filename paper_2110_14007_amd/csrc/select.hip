@@ -181,9 +181,14 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 }
 
 // ---------------------------------------------------------------------------
-// Exact fallback: a brute-force fp64 scan of every reference for the rows in
-// the worklist ("recalculate on the subset where the verification fails",
-// Section 5.2).  One workgroup per row, grid-strided over the worklist.
+// Exact fallback ("recalculate on the subset where the verification fails",
+// Section 5.2): a brute-force fp64 scan of every reference for the rows in the
+// worklist.  The scan is spread over (row, reference chunk) pairs so that a
+// handful of failing rows still fills the GPU: with c failing rows each row is
+// cut into P = clamp(kFbGrid / c, 1, kFbMaxChunks) chunks.  A chunk keeps its
+// k smallest (D^2, j) in LDS; with P == 1 it is the answer, otherwise the P
+// sorted chunk lists go to the workspace and fallback_merge_kernel picks the
+// k smallest of them per row.
 // ---------------------------------------------------------------------------
 constexpr int kFbThreads = 256;
 constexpr int kFbTop = 256;    // sorted best list occupies [0, kFbTop)
@@ -191,6 +196,12 @@ constexpr int kFbSize = 1024;  // candidates are appended in [kFbTop, kFbSize)
 
 __device__ __forceinline__ bool lex_less(uint64_t d1, uint32_t j1, uint64_t d2, uint32_t j2) {
   return d1 < d2 || (d1 == d2 && j1 < j2);
+}
+
+__device__ __forceinline__ int fb_chunks(uint32_t count) {
+  if (count == 0) return 1;
+  const uint32_t p = kFbGrid / count;
+  return p < 1 ? 1 : (p > (uint32_t)kFbMaxChunks ? kFbMaxChunks : (int)p);
 }
 
 __device__ void fb_sort(uint64_t* kd, uint32_t* kj) {
@@ -216,16 +227,22 @@ __device__ void fb_sort(uint64_t* kd, uint32_t* kj) {
   }
 }
 
-__global__ void __launch_bounds__(kFbThreads) fallback_kernel(Args a) {
+__global__ void __launch_bounds__(kFbThreads) fallback_scan_kernel(Args a) {
   __shared__ uint64_t kd[kFbSize];
   __shared__ uint32_t kj[kFbSize];
   __shared__ int bufcnt;
   if (a.ctrl->nonfinite) return;
   const uint32_t count = a.ctrl->worklist_count;
+  const int P = fb_chunks(count);
+  const int64_t clen = (a.nr + P - 1) / P;
   const int tid = threadIdx.x;
   const int k = a.k;
-  for (uint32_t w = blockIdx.x; w < count; w += gridDim.x) {
+  for (int64_t pair = blockIdx.x; pair < (int64_t)count * P; pair += gridDim.x) {
+    const int64_t w = pair / P;
+    const int c = (int)(pair % P);
     const int64_t qi = a.worklist[w];
+    const int64_t j0 = (int64_t)c * clen;
+    const int64_t j1 = j0 + clen < a.nr ? j0 + clen : a.nr;
     for (int i = tid; i < kFbSize; i += kFbThreads) {
       kd[i] = kEmpty;
       kj[i] = 0xffffffffu;
@@ -235,9 +252,9 @@ __global__ void __launch_bounds__(kFbThreads) fallback_kernel(Args a) {
     uint64_t thr_d = kEmpty;
     uint32_t thr_j = 0xffffffffu;
     const float* qrow = a.xq + qi * a.d;
-    for (int64_t base = 0; base < a.nr; base += kFbThreads) {
+    for (int64_t base = j0; base < j1; base += kFbThreads) {
       const int64_t j = base + tid;
-      if (j < a.nr && !(a.exclude_self && j == qi)) {
+      if (j < j1 && !(a.exclude_self && j == qi)) {
         const double d2 = exact_d2(qrow, a.xr + j * a.d, a.d);
         const uint64_t db = (uint64_t)__double_as_longlong(d2);
         if (lex_less(db, (uint32_t)j, thr_d, thr_j)) {
@@ -247,7 +264,7 @@ __global__ void __launch_bounds__(kFbThreads) fallback_kernel(Args a) {
         }
       }
       __syncthreads();
-      const bool last = base + kFbThreads >= a.nr;
+      const bool last = base + kFbThreads >= j1;
       if (bufcnt > kFbSize - kFbTop - kFbThreads || (last && bufcnt > 0)) {
         fb_sort(kd, kj);
         for (int i = k + tid; i < kFbSize; i += kFbThreads) {
@@ -261,8 +278,65 @@ __global__ void __launch_bounds__(kFbThreads) fallback_kernel(Args a) {
       }
       __syncthreads();
     }
-    if (tid < k) emit(a, qi, tid, kj[tid], __longlong_as_double((long long)kd[tid]));
+    if (P == 1) {
+      if (tid < k) emit(a, qi, tid, kj[tid], __longlong_as_double((long long)kd[tid]));
+    } else if (tid < k) {
+      uint2* dst = a.fbpart + pair * k + tid;
+      const uint64_t e = kd[tid];
+      // (D^2 bits, index); an unfilled slot keeps the all-ones sentinel
+      dst[0] = make_uint2((uint32_t)(e >> 32), (uint32_t)e);
+      a.fbidx[pair * k + tid] = kj[tid];
+    }
     __syncthreads();
+  }
+}
+
+// One wave per worklist row: the k smallest of its P sorted chunk lists, by
+// repeatedly taking the smallest list head (ties to the lower index).
+__global__ void __launch_bounds__(64) fallback_merge_kernel(Args a) {
+  if (a.ctrl->nonfinite) return;
+  const uint32_t count = a.ctrl->worklist_count;
+  const int P = fb_chunks(count);
+  if (P == 1) return;
+  const int lane = threadIdx.x;
+  const int k = a.k;
+  for (int64_t w = blockIdx.x; w < (int64_t)count; w += gridDim.x) {
+    const int64_t qi = a.worklist[w];
+    int pos = 0;  // next unread entry of this lane's list (lanes >= P hold none)
+    auto head = [&](uint64_t& d, uint32_t& j) {
+      if (lane < P && pos < k) {
+        const int64_t at = (w * P + lane) * k + pos;
+        const uint2 v = a.fbpart[at];
+        d = ((uint64_t)v.x << 32) | v.y;
+        j = a.fbidx[at];
+      } else {
+        d = kEmpty;
+        j = 0xffffffffu;
+      }
+    };
+    uint64_t hd;
+    uint32_t hj;
+    head(hd, hj);
+    for (int r = 0; r < k; ++r) {
+      uint64_t bd = hd;
+      uint32_t bj = hj;
+      int bl = lane;
+      for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t od = shfl_xor64(bd, off);
+        const uint32_t oj = __shfl_xor(bj, off, 64);
+        const int ol = __shfl_xor(bl, off, 64);
+        if (lex_less(od, oj, bd, bj)) {
+          bd = od;
+          bj = oj;
+          bl = ol;
+        }
+      }
+      if (lane == 0) emit(a, qi, r, bj, __longlong_as_double((long long)bd));
+      if (lane == bl) {
+        ++pos;
+        head(hd, hj);
+      }
+    }
   }
 }
 
@@ -278,6 +352,11 @@ hipError_t launch_recheck_t(const Args& a, int64_t q_begin, int64_t q_rows, hipS
 
 hipError_t launch_tile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                        hipStream_t st) {
+  if (p.tile_kind == 1) {
+    if (p.precision == TOD_PREC_FP16) return launch_mtile_f16(p, a, q_begin, q_rows, st);
+    if (p.precision == TOD_PREC_BF16) return launch_mtile_bf16(p, a, q_begin, q_rows, st);
+    return hipErrorInvalidValue;
+  }
   switch (p.precision) {
     case TOD_PREC_FP32: return launch_tile_f32(p, a, q_begin, q_rows, st);
     case TOD_PREC_FP16: return launch_tile_f16(p, a, q_begin, q_rows, st);
@@ -299,9 +378,8 @@ hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t
 }
 
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t st) {
-  int64_t g = p.nq < 2048 ? p.nq : 2048;
-  if (g < 1) g = 1;
-  hipLaunchKernelGGL(fallback_kernel, dim3((unsigned)g), dim3(kFbThreads), 0, st, a);
+  hipLaunchKernelGGL(fallback_scan_kernel, dim3(kFbGrid), dim3(kFbThreads), 0, st, a);
+  hipLaunchKernelGGL(fallback_merge_kernel, dim3(kFbGrid), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

@@ -28,6 +28,7 @@ struct Plan {
   int32_t esize;       // bytes per quantised element (4 or 2)
   int64_t nq_pad, nr_pad; // row counts padded to 32
   int32_t waves_per_group; // waves per workgroup of the tile kernel
+  int32_t tile_kind;   // 0: LDS-list tile kernel (tile.h); 1: register-list MFMA kernel (mtile.h)
   int32_t self;        // query set == reference set (one quantised copy)
   int32_t exclude_self;
   int32_t lof;         // LOF buffers needed
@@ -35,8 +36,8 @@ struct Plan {
 
 // Workspace regions (byte offsets from the workspace base, 256-aligned).
 struct Layout {
-  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, worklist, idx32,
-      d64, lrd, total;
+  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, worklist, fbpart,
+      fbidx, idx32, d64, lrd, total;
   int32_t colpart_blocks;
 };
 
@@ -77,6 +78,8 @@ struct Args {
   double* rho_r_dummy;
   uint64_t* partial;   // per (query in block, split) sorted K' lists
   int32_t* worklist;   // global query ids that failed the certificate
+  uint2* fbpart;       // fallback chunk lists: (D^2 bits hi, lo) [kFbGrid x k]
+  uint32_t* fbidx;     // fallback chunk lists: reference ids [kFbGrid x k]
   int32_t* idx32;      // [nq x k] neighbour ids (LOF)
   double* d64;         // [nq x k] exact distances (LOF)
   double* lrd;         // [nq] LOF scratch
@@ -96,6 +99,10 @@ __device__ __forceinline__ double scale_from_maxabs(uint32_t bits) {
   return ldexp(1.0, 13 - e);
 }
 
+// Fallback scan grid and the most chunks one failing row is cut into.
+constexpr int kFbGrid = 1024;
+constexpr int kFbMaxChunks = 64;
+
 // Number of blocks of the column-mean reduction (also sizes its workspace).
 int32_t colsum_blocks(int64_t nr);
 
@@ -109,6 +116,10 @@ hipError_t launch_tile_f16(const Plan& p, const Args& a, int64_t q_begin, int64_
                            hipStream_t s);
 hipError_t launch_tile_bf16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                             hipStream_t s);
+hipError_t launch_mtile_f16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                            hipStream_t s);
+hipError_t launch_mtile_bf16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                             hipStream_t s);
 hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                           hipStream_t s);
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);

@@ -207,3 +207,24 @@ def test_large_values_and_offsets(env):
         for prec in PRECS:
             say("offset/scale", shift, scale, prec)
             check_full_lof(env, x, 9, precision=prec)
+
+
+@pytest.mark.parametrize("nq,nr,d,k", [(40, 40, 3, 7), (300, 300, 7, 9), (50, 3001, 37, 7),
+                                       (1500, 1500, 5, 12), (7, 100, 2, 99)])
+def test_forced_fallback_chunks(env, nq, nr, d, k):
+    # Every row goes through the exact fallback scan.  With fewer failing rows
+    # than the scan grid, each row's references are cut into chunks whose
+    # sorted lists are merged; with more, one chunk is the whole row.
+    _, _, oracle = env
+    rng = np.random.default_rng(31 + nq + nr)
+    xr = rng.integers(-4, 5, (nr, d)).astype(np.float32)  # many exact ties
+    self_set = nq == nr
+    xq = xr if self_set else rng.integers(-4, 5, (nq, d)).astype(np.float32)
+    say("forced fallback", nq, nr, d, k)
+    if self_set:
+        check_full_lof(env, xr, k, allow_ties=False, force_fallback=True)
+    else:
+        idx, dist, st = run_knn(env, xq, xr, k, force_fallback=True)
+        assert st["rows_fallback"] == nq
+        oidx, odist = oracle.knn(xq, xr, k)
+        compare_knn(xq, xr, np.arange(nq), idx, dist, oidx, odist, allow_ties=False)
