@@ -121,6 +121,20 @@ __device__ __forceinline__ __bf16 quantise<__bf16>(double c) {
 
 // One thread per row.  Rows in [n, n_pad) are zero-filled so that the tile
 // kernels may read whole 32-row tiles.
+// Largest value over the wave (non-negative doubles compare as their bits).
+__device__ __forceinline__ double wave_max(double v) {
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = __shfl_xor((uint32_t)b, off, 64), hi = __shfl_xor((uint32_t)(b >> 32), off, 64);
+    const double o = __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+// One thread per row.  Rows in [n, n_pad) are zero-filled so that the tile
+// kernels may read whole 32-row tiles.  The reference maxima are reduced over
+// the wave first: one atomic per wave instead of two per row.
 template <typename T>
 __global__ void __launch_bounds__(kThreads)
 quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, int dpad,
@@ -128,38 +142,42 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
                 float* __restrict__ hn, double* __restrict__ n64, double* __restrict__ rho,
                 int is_ref) {
   const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= n_pad) return;
-  T* out = xq + row * dpad;
-  if (row >= n) {
-    for (int t = 0; t < dpad; ++t) out[t] = (T)0.0f;
-    if (hn) hn[row] = 0.0f;
-    if (n64) n64[row] = 0.0;
-    if (rho) rho[row] = 0.0;
-    return;
+  double nsq = 0.0, rho_up = 0.0;
+  if (row < n_pad) {
+    T* out = xq + row * dpad;
+    if (row >= n) {
+      for (int t = 0; t < dpad; ++t) out[t] = (T)0.0f;
+      if (hn) hn[row] = 0.0f;
+      if (n64) n64[row] = 0.0;
+      if (rho) rho[row] = 0.0;
+    } else {
+      const double s = scale_from_maxabs(ctrl->maxabs_bits);
+      const float* in = x + row * d;
+      double r2 = 0.0, c2 = 0.0;
+      for (int t = 0; t < d; ++t) {
+        const double c = s * ((double)in[t] - (double)mu32[t]);
+        const T q = quantise<T>(c);
+        const double qd = (double)(float)q;
+        out[t] = q;
+        nsq += qd * qd;
+        r2 += (c - qd) * (c - qd);
+        c2 += c * c;
+      }
+      for (int t = d; t < dpad; ++t) out[t] = (T)0.0f;
+      // Round the radius up: covers the fp64 rounding of c and of the sums.
+      rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
+      if (is_ref) hn[row] = -0.5f * (float)nsq;
+      if (n64) n64[row] = nsq;
+      if (rho) rho[row] = rho_up;
+    }
   }
-  const double s = scale_from_maxabs(ctrl->maxabs_bits);
-  const float* in = x + row * d;
-  double nsq = 0.0, r2 = 0.0, c2 = 0.0;
-  for (int t = 0; t < d; ++t) {
-    const double c = s * ((double)in[t] - (double)mu32[t]);
-    const T q = quantise<T>(c);
-    const double qd = (double)(float)q;
-    out[t] = q;
-    nsq += qd * qd;
-    r2 += (c - qd) * (c - qd);
-    c2 += c * c;
-  }
-  for (int t = d; t < dpad; ++t) out[t] = (T)0.0f;
-  // Round the radius up: covers the fp64 rounding of c and of the sums.
-  const double rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
   if (is_ref) {
-    hn[row] = -0.5f * (float)nsq;
-    atomicMax((unsigned long long*)&ctrl->nmax_bits, (unsigned long long)__double_as_longlong(nsq));
-    atomicMax((unsigned long long*)&ctrl->pmax_bits,
-              (unsigned long long)__double_as_longlong(rho_up));
+    const double wn = wave_max(nsq), wp = wave_max(rho_up);
+    if ((threadIdx.x & 63) == 0) {
+      atomicMax((unsigned long long*)&ctrl->nmax_bits, (unsigned long long)__double_as_longlong(wn));
+      atomicMax((unsigned long long*)&ctrl->pmax_bits, (unsigned long long)__double_as_longlong(wp));
+    }
   }
-  if (n64) n64[row] = nsq;
-  if (rho) rho[row] = rho_up;
 }
 
 template <typename T>

@@ -97,87 +97,134 @@ __device__ __forceinline__ void emit(const Args& a, int64_t qi, int rank, uint32
   if (rank == a.k - 1 && a.score_out) a.score_out[qi] = (float)dd;
 }
 
+__device__ __forceinline__ double shfl_xor_f64(double v, int mask) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  return __longlong_as_double((long long)shfl_xor64(b, mask));
+}
+
+// Merge of the per-split lists, then the progressive exact recheck: the
+// candidates are measured exactly in key order, m at a time, until the
+// certificate holds with h = the key of the first unmeasured candidate (every
+// reference outside the first m has a key >= h) or the list is exhausted.
+// One wave per query; a candidate row is read by a group of lpc lanes (one
+// dimension each, coalesced) whose fp64 partial sums are tree-reduced.
 template <int KP, int W>
 __global__ void __launch_bounds__(W * 64)
 recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
+#pragma clang fp contract(off)
   constexpr int EL = KP >= 64 ? KP / 64 : 1;
+  __shared__ uint64_t sl[W][KP];
   __shared__ double sd2[W][KP];
-  __shared__ uint32_t sj[W][KP];
   __shared__ double stau[W];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t ql = (int64_t)blockIdx.x * W + wave;
-  if (ql >= q_rows || a.ctrl->nonfinite) return;
-  const int64_t qi = q_begin + ql;
-  // Final aggregation of the per-split candidate lists (Section 6.1).
-  const uint64_t* src = a.partial + ql * a.splits * KP;
-  uint64_t list[EL];
-#pragma unroll
-  for (int r = 0; r < EL; ++r) {
-    const int e = r * 64 + lane;
-    list[r] = e < KP ? src[e] : kEmpty;
-  }
-  for (int s = 1; s < a.splits; ++s) {
-    uint64_t other[EL];
+  if (a.ctrl->nonfinite) return;
+  // Persistent grid: each wave walks the block's queries with a grid stride
+  // and counts its certified rows locally (one atomic per wave: a counter
+  // bumped once per query serialises millions of same-address atomics).
+  uint64_t ncert = 0;
+  for (int64_t ql = (int64_t)blockIdx.x * W + wave; ql < q_rows; ql += (int64_t)gridDim.x * W) {
+    const int64_t qi = q_begin + ql;
+    // Final aggregation of the per-split candidate lists (Section 6.1).
+    const uint64_t* src = a.partial + ql * a.splits * KP;
+    uint64_t list[EL];
 #pragma unroll
     for (int r = 0; r < EL; ++r) {
       const int e = r * 64 + lane;
-      other[r] = e < KP ? src[(int64_t)s * KP + e] : kEmpty;
+      list[r] = e < KP ? src[e] : kEmpty;
     }
-    merge_lists<EL>(list, other, lane);
-  }
-  const uint64_t hent = shfl64(list[(KP - 1) >> 6], (KP - 1) & 63);
-  // Exact distances of the candidates.
-  const float* qrow = a.xq + qi * a.d;
-  double myd2[EL];
-  uint32_t myj[EL];
+    for (int s = 1; s < a.splits; ++s) {
+      uint64_t other[EL];
 #pragma unroll
-  for (int r = 0; r < EL; ++r) {
-    const int e = r * 64 + lane;
-    myd2[r] = INFINITY;
-    myj[r] = 0xffffffffu;
-    if (e < KP) {
-      if (list[r] != kEmpty) {
-        myj[r] = index_of(list[r]);
-        myd2[r] = exact_d2(qrow, a.xr + (int64_t)myj[r] * a.d, a.d);
+      for (int r = 0; r < EL; ++r) {
+        const int e = r * 64 + lane;
+        other[r] = e < KP ? src[(int64_t)s * KP + e] : kEmpty;
       }
-      sd2[wave][e] = myd2[r];
-      sj[wave][e] = myj[r];
+      merge_lists<EL>(list, other, lane);
     }
-  }
-  wave_lds_sync();
-  // Rank of each candidate under (D^2, j).
-  int rank[EL];
-#pragma unroll
-  for (int r = 0; r < EL; ++r) {
-    const int e = r * 64 + lane;
-    int c = 0;
-    if (a.no_recheck) {
-      c = e;  // debug: keep the filter's order
-    } else if (e < KP) {
-      for (int e2 = 0; e2 < KP; ++e2) {
-        const double o = sd2[wave][e2];
-        const uint32_t oj = sj[wave][e2];
-        c += (o < myd2[r] || (o == myd2[r] && oj < myj[r])) ? 1 : 0;
-      }
-    }
-    rank[r] = c;
-    if (e < KP && c == a.k - 1) stau[wave] = myd2[r];
-  }
-  wave_lds_sync();
-  const double tau2 = stau[wave];
-  bool ok = a.no_recheck ? true : certified(a, qi, hent, tau2);
-  if (a.force_fallback && !a.no_recheck) ok = false;
-  if (ok) {
 #pragma unroll
     for (int r = 0; r < EL; ++r) {
       const int e = r * 64 + lane;
-      if (e < KP && rank[r] < a.k) emit(a, qi, rank[r], myj[r], myd2[r]);
+      if (e < KP) sl[wave][e] = list[r];
     }
-    if (lane == 0) atomicAdd((unsigned long long*)&a.ctrl->certified, 1ull);
-  } else if (lane == 0) {
-    const uint32_t w = atomicAdd(&a.ctrl->worklist_count, 1u);
-    a.worklist[w] = (int32_t)qi;
+    wave_lds_sync();
+
+    const int d = a.d, k = a.k;
+    int lpc = 1;
+    while (lpc < d && lpc < 64) lpc <<= 1;
+    const int grp = lane / lpc, sub = lane & (lpc - 1), G = 64 / lpc;
+    const float* qrow = a.xq + qi * d;
+    int done = 0;
+    int m = a.no_recheck ? k : (k + 8 < KP ? k + 8 : KP);
+    bool ok = false;
+    int rank[EL];
+    while (true) {
+      // Exact D^2 of candidates [done, m): the definition's direct differences
+      // in fp64, each lane summing its dimensions, then a tree over the group.
+      for (int c0 = done; c0 < m; c0 += G) {
+        const int c = c0 + grp;
+        const uint64_t e = c < m ? sl[wave][c] : kEmpty;
+        double part = 0.0;
+        if (e != kEmpty) {
+          const float* rrow = a.xr + (int64_t)index_of(e) * d;
+          for (int t = sub; t < d; t += lpc) {
+            const double df = (double)qrow[t] - (double)rrow[t];
+            const double sq = df * df;
+            part = part + sq;
+          }
+        }
+        for (int off = lpc >> 1; off > 0; off >>= 1) part = part + shfl_xor_f64(part, off);
+        if (sub == 0 && c < m) sd2[wave][c] = e != kEmpty ? part : (double)INFINITY;
+      }
+      done = m;
+      wave_lds_sync();
+      // Rank of each measured candidate under (D^2, j); tau = rank k-1.
+#pragma unroll
+      for (int r = 0; r < EL; ++r) {
+        const int c = r * 64 + lane;
+        int cr = -1;
+        if (c < m) {
+          if (a.no_recheck) {
+            cr = c;  // debug: keep the filter's order
+          } else {
+            const double mine = sd2[wave][c];
+            const uint32_t mj = index_of(sl[wave][c]);
+            cr = 0;
+            for (int c2 = 0; c2 < m; ++c2) {
+              const double o = sd2[wave][c2];
+              cr += (o < mine || (o == mine && index_of(sl[wave][c2]) < mj)) ? 1 : 0;
+            }
+          }
+          if (cr == k - 1) stau[wave] = sd2[wave][c];
+        }
+        rank[r] = cr;
+      }
+      wave_lds_sync();
+      if (a.no_recheck) {
+        ok = true;
+        break;
+      }
+      // Every reference outside the first m candidates has a key >= h.
+      const uint64_t hent = m < KP ? sl[wave][m] : sl[wave][KP - 1];
+      ok = certified(a, qi, hent, stau[wave]);
+      if (ok || m >= KP) break;
+      m = m + 16 < KP ? m + 16 : KP;
+    }
+    if (a.force_fallback && !a.no_recheck) ok = false;
+    if (ok) {
+#pragma unroll
+      for (int r = 0; r < EL; ++r) {
+        const int c = r * 64 + lane;
+        if (c < m && rank[r] >= 0 && rank[r] < k)
+          emit(a, qi, rank[r], index_of(sl[wave][c]), sd2[wave][c]);
+      }
+      ++ncert;
+    } else if (lane == 0) {
+      const uint32_t w = atomicAdd(&a.ctrl->worklist_count, 1u);
+      a.worklist[w] = (int32_t)qi;
+    }
+    wave_lds_sync();  // the next query reuses this wave's LDS rows
   }
+  if (lane == 0 && ncert) atomicAdd((unsigned long long*)&a.ctrl->certified, (unsigned long long)ncert);
 }
 
 // ---------------------------------------------------------------------------
@@ -343,8 +390,10 @@ __global__ void __launch_bounds__(64) fallback_merge_kernel(Args a) {
 template <int KP>
 hipError_t launch_recheck_t(const Args& a, int64_t q_begin, int64_t q_rows, hipStream_t st) {
   constexpr int W = 4;
-  const dim3 grid((unsigned)((q_rows + W - 1) / W));
-  hipLaunchKernelGGL((recheck_kernel<KP, W>), grid, dim3(W * 64), 0, st, a, q_begin, q_rows);
+  int64_t g = (q_rows + W - 1) / W;
+  if (g > 4096) g = 4096;
+  hipLaunchKernelGGL((recheck_kernel<KP, W>), dim3((unsigned)g), dim3(W * 64), 0, st, a, q_begin,
+                     q_rows);
   return hipGetLastError();
 }
 
