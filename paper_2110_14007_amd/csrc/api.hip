@@ -120,6 +120,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
     p->dpad_t = dp <= 128 ? (int32_t)next_pow2(dp) : 0;
     p->dpad = p->dpad_t ? p->dpad_t : (int32_t)dp;
   }
+  p->scale_exp = 14;
   p->esize = prec == TOD_PREC_FP32 ? 4 : 2;
   p->nq_pad = round_up(nq, 32);
   p->nr_pad = round_up(nr, 32);
@@ -150,9 +151,20 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   p->split_len = len;
   p->waves_per_group = kp <= 32 ? 4 : (kp == 64 ? 2 : 1);
   // The register-list MFMA kernel covers fp16 / bf16 filters whose query
-  // operand fits in registers and whose shortlist is 16, 32 or 64 long.
-  p->tile_kind = (prec != TOD_PREC_FP32 && p->dpad_t != 0 && kp <= 64) ? 1 : 0;
-  if (p->tile_kind == 1) p->waves_per_group = 4;
+  // operand fits in registers and whose shortlist is 16, 32 or 64 long.  Rows
+  // of at most 8 elements carry the accumulator seed -N_j/2 in their padding
+  // (columns 8..11 of a 16-wide row); longer rows get it from LDS.
+  p->tile_kind = (prec != TOD_PREC_FP32 && d <= 128 && kp <= 64) ? 1 : 0;
+  if (p->tile_kind == 1) {
+    p->waves_per_group = 4;
+    if (d <= 8) {
+      p->fold = 1;
+      p->dmain = 8;
+      p->dpad = p->dpad_t = 16;
+      // fp16: |seed part| <= 8 2^(2E) / 2 / 2^15 must stay below 2^15.
+      if (prec == TOD_PREC_FP16) p->scale_exp = 14;
+    }
+  }
   return TOD_OK;
 }
 
@@ -270,6 +282,9 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.precision = p.precision;
   a.margin_scale = o.margin_scale;
   a.force_fallback = o.force_fallback ? 1 : 0;
+  a.fold = p.fold;
+  a.dmain = p.dmain;
+  a.scale_exp = p.scale_exp;
   a.no_recheck = o.no_recheck ? 1 : 0;
   a.ctrl = (tod::Ctrl*)(base + L.ctrl);
   a.mu64 = (double*)(base + L.mu64);

@@ -61,8 +61,14 @@ __device__ __forceinline__ f32x16 mfma(typename Frag<ET>::V a, typename Frag<ET>
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-constexpr int kQCap = 16;  // queue slots per lane
-constexpr int kHalf = 8;   // accumulators appended between capacity checks
+constexpr int kMerge = 16;  // queue entries one merge takes per lane
+
+// Queue slots per lane.  16-entry lists see few insertions: a 16-slot queue
+// filled half a sub-tile at a time keeps LDS small enough for three
+// workgroups per CU.  Longer lists insert often: a 24-slot queue takes a whole
+// sub-tile after at most one merge (which leaves at most 8 entries).
+template <int R>
+constexpr int queue_cap() { return R <= 8 ? 16 : 24; }
 
 // Value of v in the partner lane (lane ^ 32).
 __device__ __forceinline__ uint32_t xchg32(uint32_t v, int h) {
@@ -143,11 +149,12 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
 // (32x32 MFMA output layout: column = lane % 32).
 __device__ __forceinline__ int out_row(int r, int h) { return 8 * (r >> 2) + 4 * h + (r & 3); }
 
-// Merge every lane's queue into its pair's list (all 64 lanes take part).
+// Merge the first kMerge entries of every lane's queue (fewer where cnt is
+// smaller) into its pair's list; all 64 lanes take part.
 // list: this lane's R entries of the pair's ascending K' = 2R list.
 template <int R>
 __device__ __forceinline__ void merge_queues(uint64_t (&L)[R], const uint2* myq, int cnt, int h) {
-  constexpr int M = kQCap;
+  constexpr int M = kMerge;
   uint64_t Q[M];
 #pragma unroll
   for (int i = 0; i < M; ++i) {
@@ -203,34 +210,56 @@ __device__ __forceinline__ void merge_queues(uint64_t (&L)[R], const uint2* myq,
   clean_asc<R>(L);
 }
 
-// LDS row stride of a staged reference row.  Rows of 32 bytes are read
-// conflict-free as they are; longer rows get 16 bytes of padding so that the
-// eight rows read by one group of lanes fall in different banks.
-__host__ __device__ constexpr int row_bytes(int dpad) { return dpad == 16 ? 32 : dpad * 2 + 16; }
+// Row layouts.  Plain (FOLD = false): the row padded to DPAD (16, 32, 64 or
+// 128) and the accumulator seed -N_j/2 staged in LDS beside the rows.  Fold
+// (FOLD = true, rows of at most 8 elements, DPAD = 16): the seed is stored as
+// parts p_1..p_4 of -N_j/(2c) in columns 8..11 and the queries carry the
+// constant c there instead (built in registers), so that
+//     acc = sum_t xhat_it xhat_jt + c sum_p p_p = <xhat_i, xhat_j> - N_j/2
+// comes out of the single 16-wide MFMA step, which would otherwise multiply
+// zero padding.
+template <int DPAD, bool FOLD>
+struct Layout {
+  static constexpr int k16 = DPAD / 16;  // 16-wide k-steps
+  // LDS row stride: 32-byte rows are conflict-free as they are; longer rows
+  // get 16 bytes of padding so the eight rows of a read group hit distinct
+  // banks.
+  static constexpr int rowb = DPAD == 16 ? 32 : DPAD * 2 + 16;
+  static constexpr int cpr = DPAD / 8;  // 16-byte chunks per row
+  // Sub-tiles per stage: the stage pair, seeds and four queues stay under
+  // 80 KiB so that at least two workgroups share a CU.
+  static constexpr int ns = DPAD == 16 ? 8 : (DPAD == 32 ? 4 : (DPAD == 64 ? 2 : 1));
+  static_assert(!FOLD || DPAD == 16, "the folded seed uses the padding of 8-wide rows");
+};
 
-__host__ __device__ constexpr size_t lds_bytes(int dpad, int w, int ns) {
-  return (size_t)2 * 32 * ns * row_bytes(dpad) + (size_t)2 * 32 * ns * sizeof(float) +
-         (size_t)w * kQCap * 64 * sizeof(uint2);
+__host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int ns, int qcap) {
+  return (size_t)2 * 32 * ns * (dpad == 16 ? 32 : dpad * 2 + 16) +
+         (fold ? 0 : (size_t)2 * 32 * ns * sizeof(float)) + (size_t)w * qcap * 64 * sizeof(uint2);
 }
 
-// Two waves per SIMD: the register budget stays within 256 per lane, which
-// lets the compiler keep the MFMA accumulators in VGPRs (no AGPR copies
-// around every sub-tile).
-template <typename ET, int DPAD, int R, int W, int NS, int NG>
-__global__ void __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(2)))
+// At least two waves per SIMD for lists of up to 32 entries: the register
+// budget then stays within 256 per lane, which lets the compiler keep the
+// MFMA accumulators in VGPRs (no AGPR copies around every sub-tile).  The
+// 64-entry lists need more registers and run one wave per SIMD.
+template <typename ET, int DPAD, bool FOLD, int R, int W, int NS, int NG>
+__global__ void __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(R >= 32 ? 1 : 2)))
 mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   using V = typename Frag<ET>::V;
-  constexpr int KC = DPAD / 16;  // MFMA k-steps
-  constexpr int ROWB = row_bytes(DPAD);
+  using LY = Layout<DPAD, FOLD>;
+  constexpr int kQCap = queue_cap<R>();
+  constexpr int KC = LY::k16;
+  constexpr int ROWB = LY::rowb;
   constexpr int TR = 32 * NS;  // reference rows per stage
   constexpr int STAGE = TR * ROWB;
-  constexpr int CPR = DPAD * 2 / 16;  // 16-byte chunks per row
+  constexpr int CPR = LY::cpr;
   constexpr int CHUNKS = TR * CPR;
-  constexpr int NL = (CHUNKS + W * 64 - 1) / (W * 64);
+  constexpr int NT = W * 64;
+  constexpr int NL = (CHUNKS + NT - 1) / NT;
+  static_assert(NL <= 6, "staged chunks per thread");
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* stage = smem;
-  float* hnb = (float*)(smem + 2 * STAGE);
-  uint2* qbase = (uint2*)(smem + 2 * STAGE + 2 * TR * sizeof(float));
+  float* hnb = (float*)(smem + 2 * STAGE);  // plain layout: seeds of the staged rows
+  uint2* qbase = (uint2*)(smem + 2 * STAGE + (FOLD ? 0 : 2 * TR * sizeof(float)));
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, col = lane & 31;
@@ -247,12 +276,23 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   const int64_t r_end32 = (r_end + 31) & ~(int64_t)31;  // rows < r_end32 exist (padded copy)
   const bool selfq = a.exclude_self != 0;
 
-  // Query operand: 32 queries x DPAD, lane holds column col, k-half h.
+  // Query operand: 32 queries, lane holds column col, k-half h; in the fold
+  // layout the seed columns carry the constant c.
   V bq[KC];
   {
     const ET* qrow = (const ET*)a.xq_q + (active ? q0 + col : 0) * (int64_t)DPAD;
 #pragma unroll
     for (int c = 0; c < KC; ++c) bq[c] = *reinterpret_cast<const V*>(qrow + 16 * c + 8 * h);
+    if constexpr (FOLD) {
+      const ET cf = (ET)(float)fold_const(std::is_same<ET, _Float16>::value ? TOD_PREC_FP16
+                                                                           : TOD_PREC_BF16);
+      if (h) {
+        V v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = e < 4 ? cf : (ET)0.0f;
+        bq[0] = v;
+      }
+    }
   }
 
   uint64_t L[R];
@@ -261,58 +301,44 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   float thr = -INFINITY;  // a pair survives iff acc > thr
   int cnt = 0;            // entries in this lane's queue
 
-  // Stage staging: every thread moves NL 16-byte chunks.  Rows past the
+  // Stage staging: every thread moves up to NL 16-byte chunks.  Rows past the
   // split's padded end are clamped to its last row: they are loaded but never
-  // read back, so every load and LDS write is unconditional.
-  static_assert(CHUNKS % (W * 64) == 0, "stage chunks must divide evenly over the threads");
-  static_assert(TR / 4 <= W * 64, "one float4 of seeds per thread");
+  // read back.
   const unsigned char* xr_bytes = (const unsigned char*)a.xq_r;
-  static_assert(NL >= 1 && NL <= 4, "one to four staged chunks per thread");
-  uint4 st0 = make_uint4(0, 0, 0, 0), st1 = st0, st2 = st0, st3 = st0;
+  uint4 st[NL];
+#pragma unroll
+  for (int i = 0; i < NL; ++i) st[i] = make_uint4(0, 0, 0, 0);
+  static_assert(TR / 4 <= NT, "one float4 of seeds per thread");
   float4 sth = make_float4(0.f, 0.f, 0.f, 0.f);
-  auto chunk_src = [&](int64_t t0, int c) {
-    const int row = c / CPR, cc = c % CPR;
-    const int64_t gr = t0 + row < r_end32 ? t0 + row : r_end32 - 1;
-    return reinterpret_cast<const uint4*>(xr_bytes + gr * (int64_t)(DPAD * 2) + cc * 16);
-  };
-  auto chunk_dst = [&](unsigned char* buf, int c) {
-    return reinterpret_cast<uint4*>(buf + (c / CPR) * ROWB + (c % CPR) * 16);
-  };
-  auto fetch = [&](int64_t t0) {
-    st0 = *chunk_src(t0, tid);
-    if constexpr (NL > 1) st1 = *chunk_src(t0, tid + W * 64);
-    if constexpr (NL > 2) st2 = *chunk_src(t0, tid + 2 * W * 64);
-    if constexpr (NL > 3) st3 = *chunk_src(t0, tid + 3 * W * 64);
-    if (tid < TR / 4) {
-      const int64_t gr = t0 + 4 * tid < r_end32 ? t0 + 4 * tid : r_end32 - 4;
-      sth = *reinterpret_cast<const float4*>(a.hn_r + gr);
-    }
-  };
-  auto put = [&](int b) {
-    unsigned char* buf = stage + b * STAGE;
-    *chunk_dst(buf, tid) = st0;
-    if constexpr (NL > 1) *chunk_dst(buf, tid + W * 64) = st1;
-    if constexpr (NL > 2) *chunk_dst(buf, tid + 2 * W * 64) = st2;
-    if constexpr (NL > 3) *chunk_dst(buf, tid + 3 * W * 64) = st3;
-    if (tid < TR / 4) *reinterpret_cast<float4*>(hnb + b * TR + 4 * tid) = sth;
-  };
 
-  // Accumulator seeds -N_j/2 of sub-tile s (rows 8g + 4h + 0..3 of lane's half).
+  // A fragment of sub-tile s, 16-wide k-step c: row col, elements 16c + 8h..+7.
+  auto afrag = [&](const unsigned char* buf, int s, int c) {
+    return *reinterpret_cast<const V*>(buf + (32 * s + col) * ROWB + 32 * c + 16 * h);
+  };
+  // Accumulator seeds of sub-tile s: -N_j/2 of rows 8g + 4h + 0..3 (plain
+  // layout); zero in the fold layout, where the MFMA adds them.
   auto seed = [&](const float* hn, int s) {
     f32x16 v;
+    if constexpr (FOLD) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const float4 t = *reinterpret_cast<const float4*>(hn + 32 * s + 8 * g + 4 * h);
-      v[4 * g + 0] = t.x;
-      v[4 * g + 1] = t.y;
-      v[4 * g + 2] = t.z;
-      v[4 * g + 3] = t.w;
+      for (int r = 0; r < 16; ++r) v[r] = 0.0f;
+    } else {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 t = *reinterpret_cast<const float4*>(hn + 32 * s + 8 * g + 4 * h);
+        v[4 * g + 0] = t.x;
+        v[4 * g + 1] = t.y;
+        v[4 * g + 2] = t.z;
+        v[4 * g + 3] = t.w;
+      }
     }
     return v;
   };
-  // A fragment of sub-tile s, k-step c: row col, elements 16c + 8h .. + 7.
-  auto afrag = [&](const unsigned char* buf, int s, int c) {
-    return *reinterpret_cast<const V*>(buf + (32 * s + col) * ROWB + 32 * c + 16 * h);
+  auto subtile = [&](const unsigned char* buf, const float* hn, int s) {
+    f32x16 v = seed(hn, s);
+#pragma unroll
+    for (int c = 0; c < KC; ++c) v = mfma<ET>(afrag(buf, s, c), bq[c], v);
+    return v;
   };
   // Rows past the split and the query's own row (self exclusion) never survive.
   auto mask = [&](f32x16& v, int64_t ts) {
@@ -331,42 +357,90 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     const float e = max3f(v[12], v[13], v[14]);
     return fmaxf(max3f(a, b, c), max3f(d, e, v[15]));
   };
-  // Append this lane's survivors of a sub-tile to its queue, merging first
-  // whenever a half could overflow it.
+  // Merge the first kMerge queue entries of every lane into the lists, move
+  // the rest (at most kQCap - kMerge) to the front and tighten the threshold.
+  auto flush = [&]() {
+    merge_queues<R>(L, myq_r, cnt, h);
+#pragma unroll
+    for (int i = kMerge; i < kQCap; ++i)
+      if (i < cnt) myq[(i - kMerge) * 64] = myq_r[i * 64];
+    cnt = cnt > kMerge ? cnt - kMerge : 0;
+    const uint64_t last = L[R - 1];
+    const uint64_t t = xchg64(last, h);
+    thr = thr_of(h ? last : t);
+  };
+  // Append this lane's survivors of a sub-tile to its queue.
+  //   16-slot queue: half a sub-tile at a time, merging whenever the half
+  //   could overflow it (one merge site: the halves are a loop).
+  //   24-slot queue: room for the whole sub-tile is made first; then each
+  //   quarter costs a max, a compare and a uniform branch unless some lane's
+  //   value beats its threshold.
   auto insert = [&](const f32x16& v, int64_t ts) {
+    if constexpr (kQCap == 16) {
 #pragma unroll 1
-    for (int hf = 0; hf < 2; ++hf) {
-      float cur[kHalf];
+      for (int hf = 0; hf < 2; ++hf) {
+        float cur[8];
 #pragma unroll
-      for (int r = 0; r < kHalf; ++r) cur[r] = hf ? v[kHalf + r] : v[r];
-      float mh = cur[0];
+        for (int r = 0; r < 8; ++r) cur[r] = hf ? v[8 + r] : v[r];
+        const float mh = fmaxf(fmaxf(max3f(cur[0], cur[1], cur[2]), max3f(cur[3], cur[4], cur[5])),
+                               fmaxf(cur[6], cur[7]));
+        if (!__ballot(mh > thr)) continue;
+        if (__ballot(cnt > kQCap - 8)) flush();
 #pragma unroll
-      for (int r = 1; r < kHalf; ++r) mh = fmaxf(mh, cur[r]);
-      if (!__ballot(mh > thr)) continue;
-      if (__ballot(cnt > kQCap - kHalf)) {
-        merge_queues<R>(L, myq_r, cnt, h);
-        cnt = 0;
-        const uint64_t last = L[R - 1];
-        const uint64_t t = xchg64(last, h);
-        thr = thr_of(h ? last : t);
+        for (int r = 0; r < 8; ++r) {
+          if (cur[r] > thr) {
+            myq[cnt * 64] =
+                make_uint2(__float_as_uint(cur[r]), (uint32_t)(ts + out_row(8 * hf + r, h)));
+            ++cnt;
+          }
+        }
       }
+    } else {
+      if (__ballot(cnt > kQCap - 16)) flush();
 #pragma unroll
-      for (int r = 0; r < kHalf; ++r) {
-        if (cur[r] > thr) {
-          myq[cnt * 64] =
-              make_uint2(__float_as_uint(cur[r]), (uint32_t)(ts + out_row(kHalf * hf + r, h)));
-          ++cnt;
+      for (int q = 0; q < 4; ++q) {
+        const float mq = fmaxf(max3f(v[4 * q], v[4 * q + 1], v[4 * q + 2]), v[4 * q + 3]);
+        if (__ballot(mq > thr)) {
+#pragma unroll
+          for (int r = 4 * q; r < 4 * q + 4; ++r) {
+            if (v[r] > thr) {
+              myq[cnt * 64] = make_uint2(__float_as_uint(v[r]), (uint32_t)(ts + out_row(r, h)));
+              ++cnt;
+            }
+          }
         }
       }
     }
   };
 
-  fetch(r_begin);
-  put(0);
+#define TOD_MT_FETCH(T0)                                                                     \
+  _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
+    const int c = tid + i * NT;                                                             \
+    if (CHUNKS % NT == 0 || c < CHUNKS) {                                                   \
+      const int row = c / CPR, cc = c % CPR;                                                \
+      const int64_t gr = (T0) + row < r_end32 ? (T0) + row : r_end32 - 1;                   \
+      st[i] = *reinterpret_cast<const uint4*>(xr_bytes + gr * (int64_t)(DPAD * 2) + cc * 16); \
+    }                                                                                       \
+  }                                                                                         \
+  if (!FOLD && tid < TR / 4) {                                                              \
+    const int64_t gr = (T0) + 4 * tid < r_end32 ? (T0) + 4 * tid : r_end32 - 4;             \
+    sth = *reinterpret_cast<const float4*>(a.hn_r + gr);                                    \
+  }
+#define TOD_MT_PUT(B)                                                                        \
+  _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
+    const int c = tid + i * NT;                                                             \
+    if (CHUNKS % NT == 0 || c < CHUNKS)                                                     \
+      *reinterpret_cast<uint4*>(stage + (B) * STAGE + (c / CPR) * ROWB + (c % CPR) * 16) =    \
+          st[i];                                                                            \
+  }                                                                                         \
+  if (!FOLD && tid < TR / 4) *reinterpret_cast<float4*>(hnb + (B) * TR + 4 * tid) = sth;
+
+  TOD_MT_FETCH(r_begin)
+  TOD_MT_PUT(0)
   __syncthreads();
   int it = 0;
   for (int64_t t0 = r_begin; t0 < r_end; t0 += TR, ++it) {
-    fetch(t0 + TR);  // past the end this reloads clamped rows nobody reads
+    TOD_MT_FETCH(t0 + TR)  // past the end this reloads clamped rows nobody reads
     const int b = it & 1;
     const unsigned char* buf = stage + b * STAGE;
     const float* hn = hnb + b * TR;
@@ -376,13 +450,22 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       for (int g0 = 0; g0 < live; g0 += NG) {
         // Fast path: NG sub-tiles at once (independent MFMA chains, one
         // reduction), with no insertion code.
+        // All A fragments and seeds of the group are read before the first
+        // MFMA, so that one LDS round trip covers the group's MFMA chains.
+        V af[NG][KC];
         f32x16 acc[NG];
 #pragma unroll
-        for (int s = 0; s < NG; ++s) acc[s] = seed(hn, g0 + s);
+        for (int s = 0; s < NG; ++s) {
+#pragma unroll
+          for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
+          acc[s] = seed(hn, g0 + s);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
 #pragma unroll
         for (int c = 0; c < KC; ++c)
 #pragma unroll
-          for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(afrag(buf, g0 + s, c), bq[c], acc[s]);
+          for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(af[s][c], bq[c], acc[s]);
+        __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
         float ms[NG];
 #pragma unroll
         for (int s = 0; s < NG; ++s) {
@@ -404,20 +487,24 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
             for (int u = 1; u < NG; ++u) msel = s == u ? ms[u] : msel;
             if (!__ballot(msel > thr)) continue;
             const int64_t ts = t0 + 32 * (g0 + s);
-            f32x16 a1 = seed(hn, g0 + s);
-#pragma unroll
-            for (int c = 0; c < KC; ++c) a1 = mfma<ET>(afrag(buf, g0 + s, c), bq[c], a1);
-            mask(a1, ts);
-            insert(a1, ts);
+            if constexpr (NG == 1) {
+              insert(acc[0], ts);
+            } else {
+              f32x16 a1 = subtile(buf, hn, g0 + s);
+              mask(a1, ts);
+              insert(a1, ts);
+            }
           }
         }
       }
     }
-    put((it + 1) & 1);
+    TOD_MT_PUT((it + 1) & 1)
     __syncthreads();
   }
+#undef TOD_MT_FETCH
+#undef TOD_MT_PUT
   if (active) {
-    if (__ballot(cnt > 0)) merge_queues<R>(L, myq_r, cnt, h);
+    while (__ballot(cnt > 0)) flush();
     const int64_t ql = group * 32 + col;
     if (ql < q_rows) {
       uint64_t* dst = a.partial + (ql * a.splits + split) * (2 * R) + h * R;
@@ -430,12 +517,12 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   }
 }
 
-template <typename ET, int DPAD, int R, int W = 4, int NS = (DPAD <= 32 ? 8 : (DPAD == 64 ? 4 : 2)),
-          int NG = 2>
+template <typename ET, int DPAD, bool FOLD, int R, int W = 4, int NS = Layout<DPAD, FOLD>::ns,
+          int NG = (DPAD <= 32 ? 2 : 1)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st) {
-  const size_t lds = lds_bytes(DPAD, W, NS);
-  const auto kern = mtile_kernel<ET, DPAD, R, W, NS, NG>;
+  const size_t lds = lds_bytes(DPAD, FOLD, W, NS, queue_cap<R>());
+  const auto kern = mtile_kernel<ET, DPAD, FOLD, R, W, NS, NG>;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -447,13 +534,13 @@ hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q
   return hipGetLastError();
 }
 
-template <typename ET, int DPAD>
+template <typename ET, int DPAD, bool FOLD>
 hipError_t launch_mtile_r(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                           hipStream_t st) {
   switch (p.kprime) {
-    case 16: return launch_mtile<ET, DPAD, 8>(p, a, q_begin, q_rows, st);
-    case 32: return launch_mtile<ET, DPAD, 16>(p, a, q_begin, q_rows, st);
-    case 64: return launch_mtile<ET, DPAD, 32>(p, a, q_begin, q_rows, st);
+    case 16: return launch_mtile<ET, DPAD, FOLD, 8>(p, a, q_begin, q_rows, st);
+    case 32: return launch_mtile<ET, DPAD, FOLD, 16>(p, a, q_begin, q_rows, st);
+    case 64: return launch_mtile<ET, DPAD, FOLD, 32>(p, a, q_begin, q_rows, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -461,11 +548,13 @@ hipError_t launch_mtile_r(const Plan& p, const Args& a, int64_t q_begin, int64_t
 template <typename ET>
 hipError_t launch_mtile_any(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                             hipStream_t st) {
+  if (p.fold) return p.dpad_t == 16 ? launch_mtile_r<ET, 16, true>(p, a, q_begin, q_rows, st)
+                                    : hipErrorInvalidValue;
   switch (p.dpad_t) {
-    case 16: return launch_mtile_r<ET, 16>(p, a, q_begin, q_rows, st);
-    case 32: return launch_mtile_r<ET, 32>(p, a, q_begin, q_rows, st);
-    case 64: return launch_mtile_r<ET, 64>(p, a, q_begin, q_rows, st);
-    case 128: return launch_mtile_r<ET, 128>(p, a, q_begin, q_rows, st);
+    case 16: return launch_mtile_r<ET, 16, false>(p, a, q_begin, q_rows, st);
+    case 32: return launch_mtile_r<ET, 32, false>(p, a, q_begin, q_rows, st);
+    case 64: return launch_mtile_r<ET, 64, false>(p, a, q_begin, q_rows, st);
+    case 128: return launch_mtile_r<ET, 128, false>(p, a, q_begin, q_rows, st);
     default: return hipErrorInvalidValue;
   }
 }

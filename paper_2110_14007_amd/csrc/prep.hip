@@ -119,13 +119,12 @@ __device__ __forceinline__ __bf16 quantise<__bf16>(double c) {
   return fabsf((float)b) < 1.17549435e-38f ? (__bf16)0.0f : b;
 }
 
-// One thread per row.  Rows in [n, n_pad) are zero-filled so that the tile
-// kernels may read whole 32-row tiles.
 // Largest value over the wave (non-negative doubles compare as their bits).
 __device__ __forceinline__ double wave_max(double v) {
   for (int off = 32; off > 0; off >>= 1) {
     const uint64_t b = (uint64_t)__double_as_longlong(v);
-    const uint32_t lo = __shfl_xor((uint32_t)b, off, 64), hi = __shfl_xor((uint32_t)(b >> 32), off, 64);
+    const uint32_t lo = __shfl_xor((uint32_t)b, off, 64);
+    const uint32_t hi = __shfl_xor((uint32_t)(b >> 32), off, 64);
     const double o = __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
     v = o > v ? o : v;
   }
@@ -135,14 +134,21 @@ __device__ __forceinline__ double wave_max(double v) {
 // One thread per row.  Rows in [n, n_pad) are zero-filled so that the tile
 // kernels may read whole 32-row tiles.  The reference maxima are reduced over
 // the wave first: one atomic per wave instead of two per row.
+//
+// Fold layout (fold != 0): columns [0, d) hold xhat, [d, dmain) zeros,
+// [dmain, dmain + 4) the seed parts p_1..p_4 in the filter precision and the
+// rest zeros.  The parts split v = -N/(2c) greedily (p_1 = Q(v), p_2 =
+// Q(v - p_1), ...), every residual exact in fp64, so that c * sum p = -N/2 up
+// to err = |c sum p + N/2|, computed exactly and rounded up; the certificate
+// adds the largest err over the references.
 template <typename T>
 __global__ void __launch_bounds__(kThreads)
 quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, int dpad,
                 const float* __restrict__ mu32, Ctrl* ctrl, T* __restrict__ xq,
                 float* __restrict__ hn, double* __restrict__ n64, double* __restrict__ rho,
-                int is_ref) {
+                int is_ref, int fold, int dmain, int scale_exp, double cfold) {
   const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  double nsq = 0.0, rho_up = 0.0;
+  double nsq = 0.0, rho_up = 0.0, ferr = 0.0;
   if (row < n_pad) {
     T* out = xq + row * dpad;
     if (row >= n) {
@@ -151,7 +157,7 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
       if (n64) n64[row] = 0.0;
       if (rho) rho[row] = 0.0;
     } else {
-      const double s = scale_from_maxabs(ctrl->maxabs_bits);
+      const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
       const float* in = x + row * d;
       double r2 = 0.0, c2 = 0.0;
       for (int t = 0; t < d; ++t) {
@@ -163,7 +169,23 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
         r2 += (c - qd) * (c - qd);
         c2 += c * c;
       }
-      for (int t = d; t < dpad; ++t) out[t] = (T)0.0f;
+      if (fold) {
+        for (int t = d; t < dmain; ++t) out[t] = (T)0.0f;
+        double v = -0.5 * nsq / cfold;
+        double sum = 0.0;
+        for (int t = 0; t < 4; ++t) {
+          const T q = (T)(float)v;
+          const double qd = (double)(float)q;
+          out[dmain + t] = q;
+          sum += qd;  // parts of decreasing magnitude: the sum stays exact
+          v -= qd;    // exact: qd is v rounded to fewer bits
+        }
+        for (int t = dmain + 4; t < dpad; ++t) out[t] = (T)0.0f;
+        const double e = fabs(cfold * sum + 0.5 * nsq);
+        ferr = e * (1.0 + 0x1p-40) + 0x1p-60 * nsq;
+      } else {
+        for (int t = d; t < dpad; ++t) out[t] = (T)0.0f;
+      }
       // Round the radius up: covers the fp64 rounding of c and of the sums.
       rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
       if (is_ref) hn[row] = -0.5f * (float)nsq;
@@ -172,26 +194,30 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
     }
   }
   if (is_ref) {
-    const double wn = wave_max(nsq), wp = wave_max(rho_up);
+    const double wn = wave_max(nsq), wp = wave_max(rho_up), wf = wave_max(ferr);
     if ((threadIdx.x & 63) == 0) {
       atomicMax((unsigned long long*)&ctrl->nmax_bits, (unsigned long long)__double_as_longlong(wn));
       atomicMax((unsigned long long*)&ctrl->pmax_bits, (unsigned long long)__double_as_longlong(wp));
+      atomicMax((unsigned long long*)&ctrl->fold_max_bits,
+                (unsigned long long)__double_as_longlong(wf));
     }
   }
 }
 
 template <typename T>
 hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
+  const double cf = fold_const(p.precision);
   const int64_t blocks_r = (p.nr_pad + kThreads - 1) / kThreads;
   hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_r), dim3(kThreads), 0, st, a.xr,
                      p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r, a.hn_r,
-                     p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : (double*)nullptr, 1);
+                     p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : (double*)nullptr, 1,
+                     p.fold, p.dmain, p.scale_exp, cf);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.self) return e;
   const int64_t blocks_q = (p.nq_pad + kThreads - 1) / kThreads;
   hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_q), dim3(kThreads), 0, st, a.xq,
                      p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q, (float*)nullptr,
-                     a.n64_q, a.rho_q, 0);
+                     a.n64_q, a.rho_q, 0, p.fold, p.dmain, p.scale_exp, cf);
   return hipGetLastError();
 }
 

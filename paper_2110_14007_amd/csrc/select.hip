@@ -71,12 +71,18 @@ __device__ bool certified(const Args& a, int64_t qi, uint64_t hent, double tau2)
   const double rho_i = a.rho_q[qi];
   const double nmax = __longlong_as_double((long long)a.ctrl->nmax_bits);
   const double pmax = __longlong_as_double((long long)a.ctrl->pmax_bits);
-  const double s = scale_from_maxabs(a.ctrl->maxabs_bits);
+  const double s = scale_from_maxabs(a.ctrl->maxabs_bits, a.scale_exp);
   const double u = 0x1p-23;  // per-addition allowance (2x the fp32 unit roundoff)
-  const double t = (double)a.d + 2.0;
+  // d products, the seed (one term, or four folded parts) and one spare.
+  const double t = (double)a.d + (a.fold ? 6.0 : 2.0);
   const double gam = t * u / (1.0 - t * u);
   const double ms = (double)a.margin_scale;
-  const double err = ms * (gam * (ni + 2.0 * nmax) * (1.0 + 1e-6) + u * nmax +
+  // Seed weight in the sum of |terms|: N_j/2 for an fp32 seed; the folded
+  // parts' magnitudes sum to at most (N_j/2)(1 + 2^-7) (bf16 parts; fp16 less).
+  const double seedw = a.fold ? 2.0 + 0x1p-6 : 2.0;
+  const double fold_err =
+      a.fold ? 2.0 * __longlong_as_double((long long)a.ctrl->fold_max_bits) : 0.0;
+  const double err = ms * (gam * (ni + seedw * nmax) * (1.0 + 1e-6) + u * nmax + fold_err +
                            (double)a.d * 0x1p-120) +
                      1e-12 * (ni + fabs(h));
   const double arg = ni + h - err;

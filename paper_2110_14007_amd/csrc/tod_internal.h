@@ -29,6 +29,9 @@ struct Plan {
   int64_t nq_pad, nr_pad; // row counts padded to 32
   int32_t waves_per_group; // waves per workgroup of the tile kernel
   int32_t tile_kind;   // 0: LDS-list tile kernel (tile.h); 1: register-list MFMA kernel (mtile.h)
+  int32_t fold;        // 1: rows carry the accumulator seed as extra columns (mtile.h layout)
+  int32_t dmain;       // fold layout: columns [0, dmain) hold the row, [dmain, dmain + 4) the seed
+  int32_t scale_exp;   // E: the scaled, centred rows satisfy max |s (x - mu)| < 2^E
   int32_t self;        // query set == reference set (one quantised copy)
   int32_t exclude_self;
   int32_t lof;         // LOF buffers needed
@@ -50,7 +53,8 @@ struct Ctrl {
   uint32_t worklist_count;  // rows appended for exact recomputation
   uint32_t pad0;
   uint64_t certified;       // rows certified by the shortlist test
-  uint64_t pad[4];
+  uint64_t fold_max_bits;   // max over references of the folded seed's error, fp64 bits
+  uint64_t pad[3];
 };
 
 // Everything a kernel needs to know about the problem.
@@ -65,6 +69,7 @@ struct Args {
   int32_t precision;
   float margin_scale;
   int32_t force_fallback, no_recheck;
+  int32_t fold, dmain, scale_exp;
   // workspace views
   Ctrl* ctrl;
   double* mu64;
@@ -90,13 +95,20 @@ struct Args {
   float* lof_out;
 };
 
-// Power-of-two scale s with s * maxabs < 2^14 (exact scaling of the centred
-// rows; the fp16 range then holds every quantised value and product).
-__device__ __forceinline__ double scale_from_maxabs(uint32_t bits) {
+// Power-of-two scale s with s * maxabs < 2^E (exact scaling of the centred
+// rows; the fp16 range then holds every quantised value, product and folded
+// seed part).
+__device__ __forceinline__ double scale_from_maxabs(uint32_t bits, int scale_exp) {
   const float m = __uint_as_float(bits);
   if (!(m > 0.0f)) return 1.0;
   const int e = isinf(m) ? 128 : ilogbf(m);  // m < 2^(e+1)
-  return ldexp(1.0, 13 - e);
+  return ldexp(1.0, scale_exp - 1 - e);
+}
+
+// Constant the queries carry in the seed columns of the fold layout: the
+// seed -N_j/2 is stored as parts of -N_j/(2c) so that fp16 parts stay in range.
+__host__ __device__ constexpr double fold_const(int precision) {
+  return precision == TOD_PREC_FP16 ? 32768.0 : 1.0;
 }
 
 // Fallback scan grid and the most chunks one failing row is cut into.
