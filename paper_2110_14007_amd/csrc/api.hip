@@ -86,11 +86,12 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   p->lof = lof;
   p->self = self;
   p->exclude_self = o.exclude_self ? 1 : 0;
-  // Filter precision (provable quantization, Section 5.2 step ii).  Up to
-  // d = 128 the fp16 MFMA filter with the register-resident shortlist is the
-  // fastest exact path at every size measured; above, the bf16 MFMA filter.
+  // Filter precision (provable quantization, Section 5.2 step ii).  The fp16
+  // MFMA filter: with power-of-two scaling its 11-bit mantissa gives the
+  // certificate the smallest margin of the MFMA types, hence the shortest
+  // shortlist (bf16 needs about twice as many candidates at the same speed).
   int32_t prec = o.precision;
-  if (prec == TOD_PREC_AUTO) prec = d <= 128 ? TOD_PREC_FP16 : TOD_PREC_BF16;
+  if (prec == TOD_PREC_AUTO) prec = TOD_PREC_FP16;
   p->precision = prec;
   // Shortlist length K': a power of two >= k with room for the certificate's
   // margin.  The margin a row needs grows with the filter's rounding error:
@@ -117,7 +118,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
     p->dpad = p->dpad_t ? p->dpad_t : (int32_t)dp;
   } else {
     const int64_t dp = round_up(d, 16);
-    p->dpad_t = dp <= 128 ? (int32_t)next_pow2(dp) : 0;
+    p->dpad_t = dp <= 512 ? (int32_t)next_pow2(dp) : 0;
     p->dpad = p->dpad_t ? p->dpad_t : (int32_t)dp;
   }
   p->scale_exp = 14;
@@ -154,7 +155,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   // operand fits in registers and whose shortlist is 16, 32 or 64 long.  Rows
   // of at most 8 elements carry the accumulator seed -N_j/2 in their padding
   // (columns 8..11 of a 16-wide row); longer rows get it from LDS.
-  p->tile_kind = (prec != TOD_PREC_FP32 && d <= 128 && kp <= 64) ? 1 : 0;
+  p->tile_kind = (prec != TOD_PREC_FP32 && d <= 512 && kp <= 64) ? 1 : 0;
   if (p->tile_kind == 1) {
     p->waves_per_group = 4;
     if (d <= 8) {

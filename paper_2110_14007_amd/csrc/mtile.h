@@ -229,6 +229,9 @@ struct Layout {
   // Sub-tiles per stage: the stage pair, seeds and four queues stay under
   // 80 KiB so that at least two workgroups share a CU.
   static constexpr int ns = DPAD == 16 ? 8 : (DPAD == 32 ? 4 : (DPAD == 64 ? 2 : 1));
+  // Rows of 256 or more elements keep a 32-query operand of DPAD/2 VGPRs
+  // per lane: such kernels run one wave per SIMD.
+  static constexpr bool wide = DPAD >= 256;
   static_assert(!FOLD || DPAD == 16, "the folded seed uses the padding of 8-wide rows");
 };
 
@@ -237,12 +240,14 @@ __host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int n
          (fold ? 0 : (size_t)2 * 32 * ns * sizeof(float)) + (size_t)w * qcap * 64 * sizeof(uint2);
 }
 
-// At least two waves per SIMD for lists of up to 32 entries: the register
-// budget then stays within 256 per lane, which lets the compiler keep the
-// MFMA accumulators in VGPRs (no AGPR copies around every sub-tile).  The
-// 64-entry lists need more registers and run one wave per SIMD.
+// At least two waves per SIMD for lists of up to 32 entries and rows of up to
+// 128 elements: the register budget then stays within 256 per lane, which
+// lets the compiler keep the MFMA accumulators in VGPRs (no AGPR copies
+// around every sub-tile).  64-entry lists and wider rows need more registers
+// and run one wave per SIMD.
 template <typename ET, int DPAD, bool FOLD, int R, int W, int NS, int NG>
-__global__ void __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(R >= 32 ? 1 : 2)))
+__global__ void __launch_bounds__(W * 64)
+    __attribute__((amdgpu_waves_per_eu(R >= 32 || DPAD >= 256 ? 1 : 2)))
 mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   using V = typename Frag<ET>::V;
   using LY = Layout<DPAD, FOLD>;
@@ -255,7 +260,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   constexpr int CHUNKS = TR * CPR;
   constexpr int NT = W * 64;
   constexpr int NL = (CHUNKS + NT - 1) / NT;
-  static_assert(NL <= 6, "staged chunks per thread");
+  static_assert(NL <= 16, "staged chunks per thread");
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* stage = smem;
   float* hnb = (float*)(smem + 2 * STAGE);  // plain layout: seeds of the staged rows
@@ -555,6 +560,8 @@ hipError_t launch_mtile_any(const Plan& p, const Args& a, int64_t q_begin, int64
     case 32: return launch_mtile_r<ET, 32, false>(p, a, q_begin, q_rows, st);
     case 64: return launch_mtile_r<ET, 64, false>(p, a, q_begin, q_rows, st);
     case 128: return launch_mtile_r<ET, 128, false>(p, a, q_begin, q_rows, st);
+    case 256: return launch_mtile_r<ET, 256, false>(p, a, q_begin, q_rows, st);
+    case 512: return launch_mtile_r<ET, 512, false>(p, a, q_begin, q_rows, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -11,7 +11,7 @@ def tod():
 
 
 @pytest.mark.parametrize("name,prec,kp,blocks", [
-    ("C1", "fp16", 32, 1), ("C2", "fp16", 32, 1), ("C3", "fp16", 32, 16), ("C4", "bf16", 128, 1),
+    ("C1", "fp16", 32, 1), ("C2", "fp16", 32, 1), ("C3", "fp16", 32, 16), ("C4", "fp16", 64, 1),
     ("C5", "fp16", 16, 1)])
 def test_plan_of_each_workload(tod, name, prec, kp, blocks):
     w = workloads.WORKLOADS[name]
