@@ -92,15 +92,23 @@ def cpu_baseline(x, k, target_s):
     }
 
 
+# Sources that decide what the tile kernels execute: the kernels themselves,
+# their shared headers and the planner that picks their template arguments.
+TILE_SOURCES = ("api.hip", "tod_internal.h", "wave.h", "halfwave.h", "tile.h", "tile_f32.hip",
+                "tile_f16.hip", "tile_bf16.hip", "mtile.h", "mtile_f16.hip", "mtile_bf16.hip")
+
+
 def kernel_sources_digest():
-    """sha256 over the HIP sources; a counter record applies only to this digest."""
+    """sha256 over the tile kernels' sources; a counter record applies only to this digest."""
     import hashlib
     csrc = os.path.join(ROOT, "paper_2110_14007_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(csrc)):
+    for name in TILE_SOURCES:
         h.update(name.encode())
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(f.read())
+    with open(os.path.join(ROOT, "include", "tod.h"), "rb") as f:
+        h.update(f.read())
     return h.hexdigest()
 
 
@@ -126,7 +134,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print("bench.py measures one GPU only: --gpus %d is not supported (the path has no "
-              "multi-GPU mode in this build)" % args.gpus, file=sys.stderr)
+              "multi-GPU mode)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     if args.copy_mib:
         copy_calibration(args.copy_mib, args.steps)
