@@ -47,47 +47,43 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-// Squared distance from the original fp32 rows: fp64, direct differences,
-// sequential sum, no fused multiply-add (the definition, evaluated exactly as
-// written).
-__device__ __forceinline__ double exact_d2(const float* __restrict__ p,
-                                           const float* __restrict__ q, int d) {
-#pragma clang fp contract(off)
-  double s = 0.0;
-  for (int t = 0; t < d; ++t) {
-    const double df = (double)p[t] - (double)q[t];
-    const double sq = df * df;
-    s = s + sq;
-  }
-  return s;
-}
+// Row-independent inputs of the certificate (see file header).
+struct CertConst {
+  double nmax, pmax, s, gam, seedw, fold_err, ms, derr;
+};
 
-// Lower bound test of the certificate (see file header).  Returns true when
-// no reference outside the shortlist can be among the k nearest.
-__device__ bool certified(const Args& a, int64_t qi, uint64_t hent, double tau2) {
-  if (hent == kEmpty) return true;  // the shortlist holds every reference
-  const double h = (double)key_of(hent);
-  const double ni = a.n64_q[qi];
-  const double rho_i = a.rho_q[qi];
-  const double nmax = __longlong_as_double((long long)a.ctrl->nmax_bits);
-  const double pmax = __longlong_as_double((long long)a.ctrl->pmax_bits);
-  const double s = scale_from_maxabs(a.ctrl->maxabs_bits, a.scale_exp);
+__device__ CertConst cert_const(const Args& a) {
+  CertConst c;
+  c.nmax = __longlong_as_double((long long)a.ctrl->nmax_bits);
+  c.pmax = __longlong_as_double((long long)a.ctrl->pmax_bits);
+  c.s = scale_from_maxabs(a.ctrl->maxabs_bits, a.scale_exp);
   const double u = 0x1p-23;  // per-addition allowance (2x the fp32 unit roundoff)
   // d products, the seed (one term, or four folded parts) and one spare.
   const double t = (double)a.d + (a.fold ? 6.0 : 2.0);
-  const double gam = t * u / (1.0 - t * u);
-  const double ms = (double)a.margin_scale;
+  c.gam = t * u / (1.0 - t * u);
+  c.ms = (double)a.margin_scale;
   // Seed weight in the sum of |terms|: N_j/2 for an fp32 seed; the folded
   // parts' magnitudes sum to at most (N_j/2)(1 + 2^-7) (bf16 parts; fp16 less).
-  const double seedw = a.fold ? 2.0 + 0x1p-6 : 2.0;
-  const double fold_err =
-      a.fold ? 2.0 * __longlong_as_double((long long)a.ctrl->fold_max_bits) : 0.0;
-  const double err = ms * (gam * (ni + seedw * nmax) * (1.0 + 1e-6) + u * nmax + fold_err +
-                           (double)a.d * 0x1p-120) +
+  c.seedw = a.fold ? 2.0 + 0x1p-6 : 2.0;
+  c.fold_err = a.fold ? 2.0 * __longlong_as_double((long long)a.ctrl->fold_max_bits) : 0.0;
+  // Terms that do not depend on the row: u Nmax, the folded seed error and
+  // the subnormal allowance.
+  c.derr = u * c.nmax + c.fold_err + (double)a.d * 0x1p-120;
+  return c;
+}
+
+// Lower bound test of the certificate for a row with squared norm ni and
+// radius rho_i.  Returns true when no reference outside the shortlist can be
+// among the k nearest.
+__device__ bool certified(const CertConst& c, double ni, double rho_i, uint64_t hent,
+                          double tau2) {
+  if (hent == kEmpty) return true;  // the shortlist holds every reference
+  const double h = (double)key_of(hent);
+  const double err = c.ms * (c.gam * (ni + c.seedw * c.nmax) * (1.0 + 1e-6) + c.derr) +
                      1e-12 * (ni + fabs(h));
   const double arg = ni + h - err;
-  const double lb = (arg > 0.0 ? sqrt(arg) : 0.0) - ms * (rho_i + pmax);
-  return lb * (1.0 - 1e-9) > s * sqrt(tau2) * (1.0 + 1e-9);
+  const double lb = (arg > 0.0 ? sqrt(arg) : 0.0) - c.ms * (rho_i + c.pmax);
+  return lb * (1.0 - 1e-9) > c.s * sqrt(tau2) * (1.0 + 1e-9);
 }
 
 // Write one neighbour (rank < k) of query qi to every requested output.
@@ -108,12 +104,82 @@ __device__ __forceinline__ double shfl_xor_f64(double v, int mask) {
   return __longlong_as_double((long long)shfl_xor64(b, mask));
 }
 
+// (q - r)^2 of four consecutive elements added to part in element order.
+__device__ __forceinline__ double add_sq4(double part, float4 q, float4 r) {
+#pragma clang fp contract(off)
+  double df = (double)q.x - (double)r.x;
+  part = part + df * df;
+  df = (double)q.y - (double)r.y;
+  part = part + df * df;
+  df = (double)q.z - (double)r.z;
+  part = part + df * df;
+  df = (double)q.w - (double)r.w;
+  part = part + df * df;
+  return part;
+}
+
+__device__ __forceinline__ double add_sq1(double part, float q, float r) {
+#pragma clang fp contract(off)
+  const double df = (double)q - (double)r;
+  return part + df * df;
+}
+
+// Exact D^2 (the definition's direct differences, fp64) of the shortlist
+// entries [c0, c1), c1 - c0 <= 64, into sd2.  G = next_pow2(c1 - c0) groups of
+// lpc = 64 / G lanes take one candidate each; lane `sub` of a group sums the
+// chunks sub, sub + lpc, ... of the row in order (4 elements per chunk when
+// rows are 16-byte aligned, else 1), four chunks' loads in flight at a time,
+// and the group's partial sums are tree-reduced.
+__device__ __forceinline__ void measure(const Args& a, const float* __restrict__ qrow,
+                                        const uint64_t* sl, double* sd2, int c0, int c1,
+                                        int lane) {
+  int G = 1;
+  while (G < c1 - c0) G <<= 1;
+  const int lpc = 64 / G;
+  const int grp = lane / lpc, sub = lane & (lpc - 1);
+  const int c = c0 + grp;
+  const uint64_t e = c < c1 ? sl[c] : kEmpty;
+  const int d = a.d;
+  double part = 0.0;
+  if (e != kEmpty) {
+    const float* rrow = a.xr + (int64_t)index_of(e) * d;
+    if ((d & 3) == 0) {
+      const float4* r4 = reinterpret_cast<const float4*>(rrow);
+      const float4* q4 = reinterpret_cast<const float4*>(qrow);
+      const int nch = d >> 2;
+      int ch = sub;
+      for (; ch + 3 * lpc < nch; ch += 4 * lpc) {
+        const float4 r0 = r4[ch], r1 = r4[ch + lpc], r2 = r4[ch + 2 * lpc], r3 = r4[ch + 3 * lpc];
+        const float4 q0 = q4[ch], q1 = q4[ch + lpc], q2 = q4[ch + 2 * lpc], q3 = q4[ch + 3 * lpc];
+        part = add_sq4(part, q0, r0);
+        part = add_sq4(part, q1, r1);
+        part = add_sq4(part, q2, r2);
+        part = add_sq4(part, q3, r3);
+      }
+      for (; ch < nch; ch += lpc) part = add_sq4(part, q4[ch], r4[ch]);
+    } else {
+      int t = sub;
+      for (; t + 3 * lpc < d; t += 4 * lpc) {
+        const float r0 = rrow[t], r1 = rrow[t + lpc], r2 = rrow[t + 2 * lpc], r3 = rrow[t + 3 * lpc];
+        const float q0 = qrow[t], q1 = qrow[t + lpc], q2 = qrow[t + 2 * lpc], q3 = qrow[t + 3 * lpc];
+        part = add_sq1(part, q0, r0);
+        part = add_sq1(part, q1, r1);
+        part = add_sq1(part, q2, r2);
+        part = add_sq1(part, q3, r3);
+      }
+      for (; t < d; t += lpc) part = add_sq1(part, qrow[t], rrow[t]);
+    }
+  }
+  for (int off = lpc >> 1; off > 0; off >>= 1) part = part + shfl_xor_f64(part, off);
+  if (sub == 0 && c < c1) sd2[c] = e != kEmpty ? part : (double)INFINITY;
+}
+
 // Merge of the per-split lists, then the progressive exact recheck: the
 // candidates are measured exactly in key order, m at a time, until the
 // certificate holds with h = the key of the first unmeasured candidate (every
 // reference outside the first m has a key >= h) or the list is exhausted.
-// One wave per query; a candidate row is read by a group of lpc lanes (one
-// dimension each, coalesced) whose fp64 partial sums are tree-reduced.
+// One wave per query on a persistent grid; each measuring pass has all of its
+// candidates' loads in flight at once.
 template <int KP, int W>
 __global__ void __launch_bounds__(W * 64)
 recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
@@ -124,12 +190,14 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   __shared__ double stau[W];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (a.ctrl->nonfinite) return;
-  // Persistent grid: each wave walks the block's queries with a grid stride
-  // and counts its certified rows locally (one atomic per wave: a counter
-  // bumped once per query serialises millions of same-address atomics).
+  const CertConst cc = cert_const(a);
+  // Each wave walks the block's queries with a grid stride and counts its
+  // certified rows locally (one atomic per wave: a counter bumped once per
+  // query serialises millions of same-address atomics).
   uint64_t ncert = 0;
   for (int64_t ql = (int64_t)blockIdx.x * W + wave; ql < q_rows; ql += (int64_t)gridDim.x * W) {
     const int64_t qi = q_begin + ql;
+    const double ni = a.n64_q[qi], rho_i = a.rho_q[qi];
     // Final aggregation of the per-split candidate lists (Section 6.1).
     const uint64_t* src = a.partial + ql * a.splits * KP;
     uint64_t list[EL];
@@ -154,33 +222,15 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     }
     wave_lds_sync();
 
-    const int d = a.d, k = a.k;
-    int lpc = 1;
-    while (lpc < d && lpc < 64) lpc <<= 1;
-    const int grp = lane / lpc, sub = lane & (lpc - 1), G = 64 / lpc;
-    const float* qrow = a.xq + qi * d;
+    const int k = a.k;
+    const float* qrow = a.xq + qi * a.d;
     int done = 0;
     int m = a.no_recheck ? k : (k + 8 < KP ? k + 8 : KP);
     bool ok = false;
     int rank[EL];
     while (true) {
-      // Exact D^2 of candidates [done, m): the definition's direct differences
-      // in fp64, each lane summing its dimensions, then a tree over the group.
-      for (int c0 = done; c0 < m; c0 += G) {
-        const int c = c0 + grp;
-        const uint64_t e = c < m ? sl[wave][c] : kEmpty;
-        double part = 0.0;
-        if (e != kEmpty) {
-          const float* rrow = a.xr + (int64_t)index_of(e) * d;
-          for (int t = sub; t < d; t += lpc) {
-            const double df = (double)qrow[t] - (double)rrow[t];
-            const double sq = df * df;
-            part = part + sq;
-          }
-        }
-        for (int off = lpc >> 1; off > 0; off >>= 1) part = part + shfl_xor_f64(part, off);
-        if (sub == 0 && c < m) sd2[wave][c] = e != kEmpty ? part : (double)INFINITY;
-      }
+      for (int c0 = done; c0 < m; c0 += 64)
+        measure(a, qrow, sl[wave], sd2[wave], c0, c0 + 64 < m ? c0 + 64 : m, lane);
       done = m;
       wave_lds_sync();
       // Rank of each measured candidate under (D^2, j); tau = rank k-1.
@@ -211,7 +261,7 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       }
       // Every reference outside the first m candidates has a key >= h.
       const uint64_t hent = m < KP ? sl[wave][m] : sl[wave][KP - 1];
-      ok = certified(a, qi, hent, stau[wave]);
+      ok = certified(cc, ni, rho_i, hent, stau[wave]);
       if (ok || m >= KP) break;
       m = m + 16 < KP ? m + 16 : KP;
     }
@@ -246,6 +296,7 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 constexpr int kFbThreads = 256;
 constexpr int kFbTop = 256;    // sorted best list occupies [0, kFbTop)
 constexpr int kFbSize = 1024;  // candidates are appended in [kFbTop, kFbSize)
+constexpr int kFbSlab = 32;    // columns of the reference rows staged per pass
 
 __device__ __forceinline__ bool lex_less(uint64_t d1, uint32_t j1, uint64_t d2, uint32_t j2) {
   return d1 < d2 || (d1 == d2 && j1 < j2);
@@ -281,15 +332,18 @@ __device__ void fb_sort(uint64_t* kd, uint32_t* kj) {
 }
 
 __global__ void __launch_bounds__(kFbThreads) fallback_scan_kernel(Args a) {
+#pragma clang fp contract(off)
   __shared__ uint64_t kd[kFbSize];
   __shared__ uint32_t kj[kFbSize];
+  __shared__ float rows[kFbThreads][kFbSlab + 1];
+  __shared__ float qs[kFbSlab];
   __shared__ int bufcnt;
   if (a.ctrl->nonfinite) return;
   const uint32_t count = a.ctrl->worklist_count;
   const int P = fb_chunks(count);
   const int64_t clen = (a.nr + P - 1) / P;
   const int tid = threadIdx.x;
-  const int k = a.k;
+  const int k = a.k, d = a.d;
   for (int64_t pair = blockIdx.x; pair < (int64_t)count * P; pair += gridDim.x) {
     const int64_t w = pair / P;
     const int c = (int)(pair % P);
@@ -304,11 +358,43 @@ __global__ void __launch_bounds__(kFbThreads) fallback_scan_kernel(Args a) {
     __syncthreads();
     uint64_t thr_d = kEmpty;
     uint32_t thr_j = 0xffffffffu;
-    const float* qrow = a.xq + qi * a.d;
+    const float* qrow = a.xq + qi * d;
     for (int64_t base = j0; base < j1; base += kFbThreads) {
+      // Thread tid measures reference base + tid.  The block's rows are read
+      // kFbSlab columns at a time with coalesced loads (lane -> column) and
+      // staged in LDS; each thread then adds its row's squared differences in
+      // column order, so D^2 is the sequential sum of the definition.
+      const int nrow = j1 - base < kFbThreads ? (int)(j1 - base) : kFbThreads;
+      const int col = tid & (kFbSlab - 1), row0 = tid / kFbSlab;
+      constexpr int kRowStep = kFbThreads / kFbSlab;
+      double d2 = 0.0;
+      for (int c0 = 0; c0 < d; c0 += kFbSlab) {
+        const int wcols = d - c0 < kFbSlab ? d - c0 : kFbSlab;
+        // Uniform slab origin plus 32-bit per-lane offsets (< 2^31: at most
+        // kFbThreads rows of at most 4096 columns).  Rows past the chunk and
+        // columns past the slab are clamped to valid ones; nothing reads them.
+        const float* slab = a.xr + base * d + c0;
+        const int cc = col < wcols ? col : wcols - 1;
+        float v[kFbSlab];
+#pragma unroll
+        for (int i = 0; i < kFbSlab; ++i) {
+          const int r = row0 + i * kRowStep;
+          v[i] = slab[(r < nrow ? r : nrow - 1) * d + cc];
+        }
+        const float qv = (tid < wcols) ? qrow[c0 + tid] : 0.0f;
+        __syncthreads();  // the previous slab has been consumed
+#pragma unroll
+        for (int i = 0; i < kFbSlab; ++i) rows[row0 + i * kRowStep][col] = v[i];
+        if (tid < kFbSlab) qs[tid] = qv;
+        __syncthreads();
+#pragma unroll 8
+        for (int t = 0; t < wcols; ++t) {
+          const double df = (double)qs[t] - (double)rows[tid][t];
+          d2 = d2 + df * df;
+        }
+      }
       const int64_t j = base + tid;
-      if (j < j1 && !(a.exclude_self && j == qi)) {
-        const double d2 = exact_d2(qrow, a.xr + j * a.d, a.d);
+      if (tid < nrow && !(a.exclude_self && j == qi)) {
         const uint64_t db = (uint64_t)__double_as_longlong(d2);
         if (lex_less(db, (uint32_t)j, thr_d, thr_j)) {
           const int slot = atomicAdd(&bufcnt, 1);
