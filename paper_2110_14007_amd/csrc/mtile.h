@@ -339,12 +339,6 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     }
     return v;
   };
-  auto subtile = [&](const unsigned char* buf, const float* hn, int s) {
-    f32x16 v = seed(hn, s);
-#pragma unroll
-    for (int c = 0; c < KC; ++c) v = mfma<ET>(afrag(buf, s, c), bq[c], v);
-    return v;
-  };
   // Rows past the split and the query's own row (self exclusion) never survive.
   auto mask = [&](f32x16& v, int64_t ts) {
     const bool diag = selfq && ts == q0;
@@ -380,6 +374,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   //   24-slot queue: room for the whole sub-tile is made first; then each
   //   quarter costs a max, a compare and a uniform branch unless some lane's
   //   value beats its threshold.
+  // An append writes the next free slot unconditionally and advances the
+  // count only for a survivor (no exec-mask branch per value); the room made
+  // beforehand keeps every written slot inside the queue.
   auto insert = [&](const f32x16& v, int64_t ts) {
     if constexpr (kQCap == 16) {
 #pragma unroll 1
@@ -393,11 +390,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         if (__ballot(cnt > kQCap - 8)) flush();
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-          if (cur[r] > thr) {
-            myq[cnt * 64] =
-                make_uint2(__float_as_uint(cur[r]), (uint32_t)(ts + out_row(8 * hf + r, h)));
-            ++cnt;
-          }
+          myq[cnt * 64] =
+              make_uint2(__float_as_uint(cur[r]), (uint32_t)(ts + out_row(8 * hf + r, h)));
+          cnt += cur[r] > thr ? 1 : 0;
         }
       }
     } else {
@@ -408,10 +403,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         if (__ballot(mq > thr)) {
 #pragma unroll
           for (int r = 4 * q; r < 4 * q + 4; ++r) {
-            if (v[r] > thr) {
-              myq[cnt * 64] = make_uint2(__float_as_uint(v[r]), (uint32_t)(ts + out_row(r, h)));
-              ++cnt;
-            }
+            myq[cnt * 64] = make_uint2(__float_as_uint(v[r]), (uint32_t)(ts + out_row(r, h)));
+            cnt += v[r] > thr ? 1 : 0;
           }
         }
       }
@@ -482,8 +475,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         for (int s = 1; s < NG; ++s) m = fmaxf(m, ms[s]);
         if (__ballot(m > thr)) {
           // Slow path: sub-tile by sub-tile (one copy of the insertion and
-          // merge code), recomputing the accumulators of each sub-tile that
-          // holds a survivor.
+          // merge code).  Rows of several k-steps reuse the accumulators the
+          // fast path computed; one-step rows recompute them (one MFMA),
+          // which keeps the fast path's registers free.
           const int gl = live - g0 < NG ? live - g0 : NG;
 #pragma unroll 1
           for (int s = 0; s < gl; ++s) {
@@ -494,8 +488,15 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
             const int64_t ts = t0 + 32 * (g0 + s);
             if constexpr (NG == 1) {
               insert(acc[0], ts);
+            } else if constexpr (KC >= 2) {
+              f32x16 a1 = acc[0];
+#pragma unroll
+              for (int u = 1; u < NG; ++u)
+                if (s == u) a1 = acc[u];
+              insert(a1, ts);
             } else {
-              f32x16 a1 = subtile(buf, hn, g0 + s);
+              f32x16 a1 = seed(hn, g0 + s);
+              a1 = mfma<ET>(afrag(buf, g0 + s, 0), bq[0], a1);
               mask(a1, ts);
               insert(a1, ts);
             }
