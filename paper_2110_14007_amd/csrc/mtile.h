@@ -18,8 +18,8 @@
 // the accumulator mapped to an unsigned key that ascends as acc descends, and
 // the reference index below it.  Both lanes keep the acc of entry K'-1 as a
 // threshold; a sub-tile costs a max3 reduction and one compare per lane unless
-// some accumulator beats it.  Survivors are appended to a 16-slot LDS queue of
-// their lane.  When a queue could overflow, the whole wave merges: every lane
+// some accumulator beats it.  Survivors are appended to an LDS queue (16 or 24
+// slots) of their lane.  When a queue could overflow, the whole wave merges: every lane
 // sorts its queue, each pair merges its two queues and then the merged queue
 // with its list by bitonic stages whose cross-lane step is v_permlane32_swap.
 // No LDS round trip is needed for the lists, so LDS holds only the staged
@@ -79,9 +79,15 @@ __device__ __forceinline__ uint64_t xchg64(uint64_t v, int h) {
   return ((uint64_t)xchg32((uint32_t)(v >> 32), h) << 32) | xchg32((uint32_t)v, h);
 }
 
+// Entries are ordered by their key (the high word) alone: a 32-bit compare.
+// The order of equal keys does not matter to the filter (see the file header).
+__device__ __forceinline__ bool key_lt(uint64_t a, uint64_t b) {
+  return (uint32_t)(a >> 32) < (uint32_t)(b >> 32);
+}
+
 // Ascending compare-exchange.
 __device__ __forceinline__ void ce(uint64_t& x, uint64_t& y) {
-  const bool sw = y < x;
+  const bool sw = key_lt(y, x);
   const uint64_t lo = sw ? y : x;
   const uint64_t hi = sw ? x : y;
   x = lo;
@@ -90,7 +96,7 @@ __device__ __forceinline__ void ce(uint64_t& x, uint64_t& y) {
 
 // Keep min (h == 0) or max (h == 1) of x and the partner's value p.
 __device__ __forceinline__ uint64_t keep(uint64_t x, uint64_t p, int h) {
-  const bool take = h ? (x < p) : (p < x);
+  const bool take = h ? key_lt(x, p) : key_lt(p, x);
   return take ? p : x;
 }
 
@@ -180,7 +186,7 @@ __device__ __forceinline__ void merge_queues(uint64_t (&L)[R], const uint2* myq,
 #pragma unroll
     for (int i = 0; i < R; ++i) {
       const uint64_t o = xchg64(Q[R - 1 - i], h);
-      L[i] = o < L[i] ? o : L[i];
+      L[i] = key_lt(o, L[i]) ? o : L[i];
     }
   } else if constexpr (R < M) {
     // Q[2R-1-e] lies in lane q: for lane q itself at index 2R-1-i, for lane
@@ -189,7 +195,7 @@ __device__ __forceinline__ void merge_queues(uint64_t (&L)[R], const uint2* myq,
     for (int i = 0; i < R; ++i) {
       const uint64_t p = xchg64(Q[R - 1 - i], h);
       const uint64_t o = h ? p : Q[2 * R - 1 - i];
-      L[i] = o < L[i] ? o : L[i];
+      L[i] = key_lt(o, L[i]) ? o : L[i];
     }
   } else {
     static_assert(R == 2 * M, "list length per lane must be 8, 16 or 32");
@@ -199,7 +205,7 @@ __device__ __forceinline__ void merge_queues(uint64_t (&L)[R], const uint2* myq,
 #pragma unroll
     for (int i = 0; i < R; ++i) {
       const uint64_t o = i < M ? Q[M - 1 - i] : xchg64(Q[2 * M - 1 - i], h);
-      const uint64_t m = o < L[i] ? o : L[i];
+      const uint64_t m = key_lt(o, L[i]) ? o : L[i];
       L[i] = h ? m : L[i];
     }
   }
