@@ -259,6 +259,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   using LY = Layout<DPAD, FOLD>;
   constexpr int kQCap = queue_cap<R>();
   constexpr int KC = LY::k16;
+  constexpr bool kInterleave = NG == 1 && KC >= 16;
+  constexpr int kAhead = 4;
   constexpr int ROWB = LY::rowb;
   constexpr int TR = 32 * NS;  // reference rows per stage
   constexpr int STAGE = TR * ROWB;
@@ -360,7 +362,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     const float a = max3f(v[0], v[1], v[2]), b = max3f(v[3], v[4], v[5]);
     const float c = max3f(v[6], v[7], v[8]), d = max3f(v[9], v[10], v[11]);
     const float e = max3f(v[12], v[13], v[14]);
-    return fmaxf(max3f(a, b, c), max3f(d, e, v[15]));
+    const float f = max3f(a, b, c), g = max3f(d, e, v[15]);
+    return max3f(f, g, g);
   };
   // Merge the first kMerge queue entries of every lane into the lists, move
   // the rest (at most kQCap - kMerge) to the front and tighten the threshold.
@@ -390,8 +393,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         float cur[8];
 #pragma unroll
         for (int r = 0; r < 8; ++r) cur[r] = hf ? v[8 + r] : v[r];
-        const float mh = fmaxf(fmaxf(max3f(cur[0], cur[1], cur[2]), max3f(cur[3], cur[4], cur[5])),
-                               fmaxf(cur[6], cur[7]));
+        const float mh = max3f(max3f(cur[0], cur[1], cur[2]), max3f(cur[3], cur[4], cur[5]),
+                               max3f(cur[6], cur[7], cur[7]));
         if (!__ballot(mh > thr)) continue;
         if (__ballot(cnt > kQCap - 8)) flush();
 #pragma unroll
@@ -405,7 +408,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       if (__ballot(cnt > kQCap - 16)) flush();
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float mq = fmaxf(max3f(v[4 * q], v[4 * q + 1], v[4 * q + 2]), v[4 * q + 3]);
+        const float mq = max3f(max3f(v[4 * q], v[4 * q + 1], v[4 * q + 2]), v[4 * q + 3], v[4 * q + 3]);
         if (__ballot(mq > thr)) {
 #pragma unroll
           for (int r = 4 * q; r < 4 * q + 4; ++r) {
@@ -456,6 +459,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         // reduction), with no insertion code.
         // All A fragments and seeds of the group are read before the first
         // MFMA, so that one LDS round trip covers the group's MFMA chains.
+        // Long rows (one wave per SIMD, nothing else to overlap with) keep
+        // kAhead fragments in flight ahead of the MFMA chain instead: the
+        // LDS reads of later k-steps then run under the MFMAs of earlier ones.
         V af[NG][KC];
         f32x16 acc[NG];
 #pragma unroll
@@ -464,12 +470,22 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
           for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
           acc[s] = seed(hn, g0 + s);
         }
-        __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
 #pragma unroll
         for (int c = 0; c < KC; ++c)
 #pragma unroll
           for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(af[s][c], bq[c], acc[s]);
-        __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
+        if constexpr (kInterleave) {
+          __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
+#pragma unroll
+          for (int c = 0; c < KC - kAhead; ++c) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+        } else {
+          __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
+        }
         float ms[NG];
 #pragma unroll
         for (int s = 0; s < NG; ++s) {
@@ -478,7 +494,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         }
         float m = ms[0];
 #pragma unroll
-        for (int s = 1; s < NG; ++s) m = fmaxf(m, ms[s]);
+        for (int s = 1; s < NG; ++s) m = max3f(m, ms[s], ms[s]);
         if (__ballot(m > thr)) {
           // Slow path: sub-tile by sub-tile (one copy of the insertion and
           // merge code).  Rows of several k-steps reuse the accumulators the
