@@ -70,6 +70,14 @@ constexpr int kMerge = 16;  // queue entries one merge takes per lane
 template <int R>
 constexpr int queue_cap() { return R <= 8 ? 16 : 24; }
 
+// Workgroup barrier of the two-stage staging pipeline: this wave's LDS writes
+// are complete before it, and global loads still in flight stay in flight (a
+// release fence would wait for them).  The asm also keeps the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Value of v in the partner lane (lane ^ 32).
 __device__ __forceinline__ uint32_t xchg32(uint32_t v, int h) {
   const auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
@@ -316,13 +324,18 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 
   // Stage staging: every thread moves up to NL 16-byte chunks.  Rows past the
   // split's padded end are clamped to its last row: they are loaded but never
-  // read back.
+  // read back.  Rows of 256 or more elements (one 32-row sub-tile per stage,
+  // one wave per SIMD, registers to spare) are loaded two stages ahead into
+  // two register sets with fixed roles; shorter rows one stage ahead.
+  constexpr bool PF2 = DPAD >= 256;
   const unsigned char* xr_bytes = (const unsigned char*)a.xq_r;
-  uint4 st[NL];
+  uint4 st[NL], su[PF2 ? NL : 1];
 #pragma unroll
   for (int i = 0; i < NL; ++i) st[i] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int i = 0; i < (PF2 ? NL : 1); ++i) su[i] = make_uint4(0, 0, 0, 0);
   static_assert(TR / 4 <= NT, "one float4 of seeds per thread");
-  float4 sth = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 sth = make_float4(0.f, 0.f, 0.f, 0.f), suh = sth;
 
   // A fragment of sub-tile s, 16-wide k-step c: row col, elements 16c + 8h..+7.
   auto afrag = [&](const unsigned char* buf, int s, int c) {
@@ -367,7 +380,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   };
   // Merge the first kMerge queue entries of every lane into the lists, move
   // the rest (at most kQCap - kMerge) to the front and tighten the threshold.
-  auto flush = [&]() {
+  auto flush = [&]() __attribute__((always_inline)) {
     merge_queues<R>(L, myq_r, cnt, h);
 #pragma unroll
     for (int i = kMerge; i < kQCap; ++i)
@@ -386,7 +399,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // An append writes the next free slot unconditionally and advances the
   // count only for a survivor (no exec-mask branch per value); the room made
   // beforehand keeps every written slot inside the queue.
-  auto insert = [&](const f32x16& v, int64_t ts) {
+  auto insert = [&](const f32x16& v, int64_t ts) __attribute__((always_inline)) {
     if constexpr (kQCap == 16) {
 #pragma unroll 1
       for (int hf = 0; hf < 2; ++hf) {
@@ -420,114 +433,140 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     }
   };
 
-#define TOD_MT_FETCH(T0)                                                                     \
+#define TOD_MT_FETCH(T0, REG, REGH)                                                          \
   _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
     const int c = tid + i * NT;                                                             \
     if (CHUNKS % NT == 0 || c < CHUNKS) {                                                   \
       const int row = c / CPR, cc = c % CPR;                                                \
       const int64_t gr = (T0) + row < r_end32 ? (T0) + row : r_end32 - 1;                   \
-      st[i] = *reinterpret_cast<const uint4*>(xr_bytes + gr * (int64_t)(DPAD * 2) + cc * 16); \
+      REG[i] = *reinterpret_cast<const uint4*>(xr_bytes + gr * (int64_t)(DPAD * 2) + cc * 16); \
     }                                                                                       \
   }                                                                                         \
   if (!FOLD && tid < TR / 4) {                                                              \
     const int64_t gr = (T0) + 4 * tid < r_end32 ? (T0) + 4 * tid : r_end32 - 4;             \
-    sth = *reinterpret_cast<const float4*>(a.hn_r + gr);                                    \
+    REGH = *reinterpret_cast<const float4*>(a.hn_r + gr);                                   \
   }
-#define TOD_MT_PUT(B)                                                                        \
+#define TOD_MT_PUT(B, REG, REGH)                                                             \
   _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
     const int c = tid + i * NT;                                                             \
     if (CHUNKS % NT == 0 || c < CHUNKS)                                                     \
       *reinterpret_cast<uint4*>(stage + (B) * STAGE + (c / CPR) * ROWB + (c % CPR) * 16) =    \
-          st[i];                                                                            \
+          REG[i];                                                                           \
   }                                                                                         \
-  if (!FOLD && tid < TR / 4) *reinterpret_cast<float4*>(hnb + (B) * TR + 4 * tid) = sth;
+  if (!FOLD && tid < TR / 4) *reinterpret_cast<float4*>(hnb + (B) * TR + 4 * tid) = REGH;
 
-  TOD_MT_FETCH(r_begin)
-  TOD_MT_PUT(0)
-  __syncthreads();
-  int it = 0;
-  for (int64_t t0 = r_begin; t0 < r_end; t0 += TR, ++it) {
-    TOD_MT_FETCH(t0 + TR)  // past the end this reloads clamped rows nobody reads
-    const int b = it & 1;
-    const unsigned char* buf = stage + b * STAGE;
-    const float* hn = hnb + b * TR;
-    if (active) {
-      const int live = r_end - t0 < TR ? (int)((r_end - t0 + 31) >> 5) : NS;
-#pragma unroll 1
-      for (int g0 = 0; g0 < live; g0 += NG) {
-        // Fast path: NG sub-tiles at once (independent MFMA chains, one
-        // reduction), with no insertion code.
-        // All A fragments and seeds of the group are read before the first
-        // MFMA, so that one LDS round trip covers the group's MFMA chains.
-        // Long rows (one wave per SIMD, nothing else to overlap with) keep
-        // kAhead fragments in flight ahead of the MFMA chain instead: the
-        // LDS reads of later k-steps then run under the MFMAs of earlier ones.
-        V af[NG][KC];
-        f32x16 acc[NG];
-#pragma unroll
-        for (int s = 0; s < NG; ++s) {
-#pragma unroll
-          for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
-          acc[s] = seed(hn, g0 + s);
-        }
-#pragma unroll
-        for (int c = 0; c < KC; ++c)
-#pragma unroll
-          for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(af[s][c], bq[c], acc[s]);
-        if constexpr (kInterleave) {
-          __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
-#pragma unroll
-          for (int c = 0; c < KC - kAhead; ++c) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  // One stage: its sub-tiles from LDS buffer b.
+  auto stage_body = [&](int64_t t0, int b) __attribute__((always_inline)) {
+      const unsigned char* buf = stage + b * STAGE;
+      const float* hn = hnb + b * TR;
+      if (active) {
+        const int live = r_end - t0 < TR ? (int)((r_end - t0 + 31) >> 5) : NS;
+  #pragma unroll 1
+        for (int g0 = 0; g0 < live; g0 += NG) {
+          // Fast path: NG sub-tiles at once (independent MFMA chains, one
+          // reduction), with no insertion code.
+          // All A fragments and seeds of the group are read before the first
+          // MFMA, so that one LDS round trip covers the group's MFMA chains.
+          // Long rows (one wave per SIMD, nothing else to overlap with) keep
+          // kAhead fragments in flight ahead of the MFMA chain instead: the
+          // LDS reads of later k-steps then run under the MFMAs of earlier ones.
+          V af[NG][KC];
+          f32x16 acc[NG];
+  #pragma unroll
+          for (int s = 0; s < NG; ++s) {
+  #pragma unroll
+            for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
+            acc[s] = seed(hn, g0 + s);
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
-        } else {
-          __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
-        }
-        float ms[NG];
-#pragma unroll
-        for (int s = 0; s < NG; ++s) {
-          mask(acc[s], t0 + 32 * (g0 + s));
-          ms[s] = max16(acc[s]);  // sub-tiles past the split are fully masked
-        }
-        float m = ms[0];
-#pragma unroll
-        for (int s = 1; s < NG; ++s) m = max3f(m, ms[s], ms[s]);
-        if (__ballot(m > thr)) {
-          // Slow path: sub-tile by sub-tile (one copy of the insertion and
-          // merge code).  Rows of several k-steps reuse the accumulators the
-          // fast path computed; one-step rows recompute them (one MFMA),
-          // which keeps the fast path's registers free.
-          const int gl = live - g0 < NG ? live - g0 : NG;
-#pragma unroll 1
-          for (int s = 0; s < gl; ++s) {
-            float msel = ms[0];
-#pragma unroll
-            for (int u = 1; u < NG; ++u) msel = s == u ? ms[u] : msel;
-            if (!__ballot(msel > thr)) continue;
-            const int64_t ts = t0 + 32 * (g0 + s);
-            if constexpr (NG == 1) {
-              insert(acc[0], ts);
-            } else if constexpr (KC >= 2) {
-              f32x16 a1 = acc[0];
-#pragma unroll
-              for (int u = 1; u < NG; ++u)
-                if (s == u) a1 = acc[u];
-              insert(a1, ts);
-            } else {
-              f32x16 a1 = seed(hn, g0 + s);
-              a1 = mfma<ET>(afrag(buf, g0 + s, 0), bq[0], a1);
-              mask(a1, ts);
-              insert(a1, ts);
+  #pragma unroll
+          for (int c = 0; c < KC; ++c)
+  #pragma unroll
+            for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(af[s][c], bq[c], acc[s]);
+          if constexpr (kInterleave) {
+            __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
+  #pragma unroll
+            for (int c = 0; c < KC - kAhead; ++c) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+          } else {
+            __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
+          }
+          float ms[NG];
+  #pragma unroll
+          for (int s = 0; s < NG; ++s) {
+            mask(acc[s], t0 + 32 * (g0 + s));
+            ms[s] = max16(acc[s]);  // sub-tiles past the split are fully masked
+          }
+          float m = ms[0];
+  #pragma unroll
+          for (int s = 1; s < NG; ++s) m = max3f(m, ms[s], ms[s]);
+          if (__ballot(m > thr)) {
+            // Slow path: sub-tile by sub-tile (one copy of the insertion and
+            // merge code).  Rows of several k-steps reuse the accumulators the
+            // fast path computed; one-step rows recompute them (one MFMA),
+            // which keeps the fast path's registers free.
+            const int gl = live - g0 < NG ? live - g0 : NG;
+  #pragma unroll 1
+            for (int s = 0; s < gl; ++s) {
+              float msel = ms[0];
+  #pragma unroll
+              for (int u = 1; u < NG; ++u) msel = s == u ? ms[u] : msel;
+              if (!__ballot(msel > thr)) continue;
+              const int64_t ts = t0 + 32 * (g0 + s);
+              if constexpr (NG == 1) {
+                insert(acc[0], ts);
+              } else if constexpr (KC >= 2) {
+                f32x16 a1 = acc[0];
+  #pragma unroll
+                for (int u = 1; u < NG; ++u)
+                  if (s == u) a1 = acc[u];
+                insert(a1, ts);
+              } else {
+                f32x16 a1 = seed(hn, g0 + s);
+                a1 = mfma<ET>(afrag(buf, g0 + s, 0), bq[0], a1);
+                mask(a1, ts);
+                insert(a1, ts);
+              }
             }
           }
         }
       }
+  };
+
+  TOD_MT_FETCH(r_begin, st, sth)
+  TOD_MT_PUT(0, st, sth)
+  if constexpr (PF2) {
+    // Two stages per trip: each register set has a fixed role in straight-line
+    // code, so every wait is for the older set only, and the stage barrier
+    // (no release fence) leaves the newer set's loads in flight.
+    TOD_MT_FETCH(r_begin + TR, su, suh)
+    stage_barrier();
+    for (int64_t t0 = r_begin;;) {
+      TOD_MT_FETCH(t0 + 2 * TR, st, sth)  // past the end: clamped rows nobody reads
+      stage_body(t0, 0);
+      TOD_MT_PUT(1, su, suh)
+      stage_barrier();
+      t0 += TR;
+      if (t0 >= r_end) break;
+      TOD_MT_FETCH(t0 + 2 * TR, su, suh)
+      stage_body(t0, 1);
+      TOD_MT_PUT(0, st, sth)
+      stage_barrier();
+      t0 += TR;
+      if (t0 >= r_end) break;
     }
-    TOD_MT_PUT((it + 1) & 1)
+  } else {
     __syncthreads();
+    int it = 0;
+    for (int64_t t0 = r_begin; t0 < r_end; t0 += TR, ++it) {
+      TOD_MT_FETCH(t0 + TR, st, sth)  // past the end this reloads clamped rows nobody reads
+      stage_body(t0, it & 1);
+      TOD_MT_PUT((it + 1) & 1, st, sth)
+      __syncthreads();
+    }
   }
 #undef TOD_MT_FETCH
 #undef TOD_MT_PUT
