@@ -204,8 +204,96 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
   }
 }
 
+// Sum over the wave (butterfly: every lane ends with the same value).
+__device__ __forceinline__ double wave_sum(double v) {
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = __shfl_xor((uint32_t)b, off, 64);
+    const uint32_t hi = __shfl_xor((uint32_t)(b >> 32), off, 64);
+    v = v + __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+  }
+  return v;
+}
+
+// One wave per row for rows without the fold layout: the row is read and the
+// quantised row written with the lanes over the columns (coalesced), and the
+// three sums are reduced over the wave.  Same outputs as quantise_kernel; the
+// sums are added in another order, which the certificate's allowances for the
+// fp64 rounding of N and rho cover.  Each wave walks rows with a grid stride
+// and issues one atomic per maximum at the end.
+template <typename T>
+__global__ void __launch_bounds__(kThreads)
+quantise_rows_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, int dpad,
+                     const float* __restrict__ mu32, Ctrl* ctrl, T* __restrict__ xq,
+                     float* __restrict__ hn, double* __restrict__ n64,
+                     double* __restrict__ rho, int is_ref, int scale_exp) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
+  double wn = 0.0, wp = 0.0;  // this wave's maxima (the same in every lane)
+  for (int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6; row < n_pad;
+       row += nwaves) {
+    T* out = xq + row * dpad;
+    if (row >= n) {
+      for (int t = lane; t < dpad; t += 64) out[t] = (T)0.0f;
+      if (lane == 0) {
+        if (hn) hn[row] = 0.0f;
+        if (n64) n64[row] = 0.0;
+        if (rho) rho[row] = 0.0;
+      }
+      continue;
+    }
+    const float* in = x + row * d;
+    double nsq = 0.0, r2 = 0.0, c2 = 0.0;
+    for (int t = lane; t < dpad; t += 64) {
+      T q = (T)0.0f;
+      if (t < d) {
+        const double c = s * ((double)in[t] - (double)mu32[t]);
+        q = quantise<T>(c);
+        const double qd = (double)(float)q;
+        nsq += qd * qd;
+        r2 += (c - qd) * (c - qd);
+        c2 += c * c;
+      }
+      out[t] = q;
+    }
+    nsq = wave_sum(nsq);
+    r2 = wave_sum(r2);
+    c2 = wave_sum(c2);
+    // Round the radius up: covers the fp64 rounding of c and of the sums.
+    const double rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
+    if (lane == 0) {
+      if (is_ref) hn[row] = -0.5f * (float)nsq;
+      if (n64) n64[row] = nsq;
+      if (rho) rho[row] = rho_up;
+    }
+    wn = nsq > wn ? nsq : wn;
+    wp = rho_up > wp ? rho_up : wp;
+  }
+  if (is_ref && lane == 0) {
+    atomicMax((unsigned long long*)&ctrl->nmax_bits, (unsigned long long)__double_as_longlong(wn));
+    atomicMax((unsigned long long*)&ctrl->pmax_bits, (unsigned long long)__double_as_longlong(wp));
+  }
+}
+
 template <typename T>
 hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
+  if (!p.fold && p.d >= 64) {
+    const auto grid_rows = [](int64_t rows) {
+      int64_t g = (rows + 3) / 4;  // 4 waves per block
+      return (unsigned)(g < 1 ? 1 : (g > 4096 ? 4096 : g));
+    };
+    hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nr_pad)), dim3(kThreads), 0, st,
+                       a.xr, p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r,
+                       a.hn_r, p.self ? a.n64_q : (double*)nullptr,
+                       p.self ? a.rho_q : (double*)nullptr, 1, p.scale_exp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.self) return e;
+    hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nq_pad)), dim3(kThreads), 0, st,
+                       a.xq, p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q,
+                       (float*)nullptr, a.n64_q, a.rho_q, 0, p.scale_exp);
+    return hipGetLastError();
+  }
   const double cf = fold_const(p.precision);
   const int64_t blocks_r = (p.nr_pad + kThreads - 1) / kThreads;
   hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_r), dim3(kThreads), 0, st, a.xr,

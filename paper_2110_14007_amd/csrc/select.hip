@@ -124,20 +124,10 @@ __device__ __forceinline__ double add_sq1(double part, float q, float r) {
   return part + df * df;
 }
 
-// Exact D^2 (the definition's direct differences, fp64) of the shortlist
-// entries [c0, c1), c1 - c0 <= 64, into sd2.  G = next_pow2(c1 - c0) groups of
-// lpc = 64 / G lanes take one candidate each; lane `sub` of a group sums the
-// chunks sub, sub + lpc, ... of the row in order (4 elements per chunk when
-// rows are 16-byte aligned, else 1), four chunks' loads in flight at a time,
-// and the group's partial sums are tree-reduced.
-__device__ __forceinline__ void measure(const Args& a, const float* __restrict__ qrow,
-                                        const uint64_t* sl, double* sd2, int c0, int c1,
-                                        int lane) {
-  int G = 1;
-  while (G < c1 - c0) G <<= 1;
-  const int lpc = 64 / G;
-  const int grp = lane / lpc, sub = lane & (lpc - 1);
-  const int c = c0 + grp;
+// One pass of measure: candidate c (if below c1) by the lpc lanes of this group.
+__device__ __forceinline__ void measure_pass(const Args& a, const float* __restrict__ qrow,
+                                             const uint64_t* sl, double* sd2, int c, int c1,
+                                             int lpc, int sub) {
   const uint64_t e = c < c1 ? sl[c] : kEmpty;
   const int d = a.d;
   double part = 0.0;
@@ -172,6 +162,25 @@ __device__ __forceinline__ void measure(const Args& a, const float* __restrict__
   }
   for (int off = lpc >> 1; off > 0; off >>= 1) part = part + shfl_xor_f64(part, off);
   if (sub == 0 && c < c1) sd2[c] = e != kEmpty ? part : (double)INFINITY;
+}
+
+// Exact D^2 (the definition's direct differences, fp64) of the shortlist
+// entries [c0, c1), c1 - c0 <= 64, into sd2.  Groups of lpc lanes take one
+// candidate each: lpc = 64 / next_pow2(c1 - c0), but at least d / 64 (a power
+// of two, at most 16) so that a load instruction of a long row covers few
+// rows; the candidates then take several passes.  Lane `sub` of a group sums
+// the chunks sub, sub + lpc, ... of the row in order (4 elements per chunk
+// when rows are 16-byte aligned, else 1), four chunks' loads in flight at a
+// time, and the group's partial sums are tree-reduced.
+__device__ __forceinline__ void measure(const Args& a, const float* __restrict__ qrow,
+                                        const uint64_t* sl, double* sd2, int c0, int c1,
+                                        int lane) {
+  int G = 1;
+  while (G < c1 - c0) G <<= 1;
+  int lpc = 64 / G;
+  while (lpc < 16 && lpc * 64 < a.d) lpc <<= 1;
+  const int grp = lane / lpc, sub = lane & (lpc - 1), per = 64 / lpc;
+  for (int cb = c0; cb < c1; cb += per) measure_pass(a, qrow, sl, sd2, cb + grp, c1, lpc, sub);
 }
 
 // Merge of the per-split lists, then the progressive exact recheck: the
