@@ -75,6 +75,11 @@ typedef struct {
   float margin_scale;    /* >= 1: multiplies every error term of the certificate; 1 = default */
   int32_t force_fallback;/* debug: treat every row as uncertified (exact recomputation) */
   int32_t no_recheck;    /* debug: return the filter's shortlist order without verification */
+  int32_t reorder;       /* scan order of an X-against-X call (tod_knn with xq == xr, tod_knn_score,
+                          * tod_lof): 0 = planner, 1 = on, -1 = off.  On: the rows are grouped by a
+                          * 16-seed partition (nearest of 16 evenly spaced rows) and every query
+                          * block first scans the references of its own group, so the filter's
+                          * thresholds tighten early.  Results are identical either way. */
 } tod_options;
 
 /* Plan and per-phase timings of one call (filled when a non-NULL pointer is
@@ -90,6 +95,7 @@ typedef struct {
   int64_t rows_fallback;  /* rows recomputed exactly */
   int64_t tile_launches;  /* launches of the fused distance + selection kernel */
   float ms_prep, ms_tile, ms_recheck, ms_fallback, ms_score, ms_total;
+  int32_t reordered;      /* 1 if the scan used the grouped row order (see tod_options.reorder) */
 } tod_stats;
 
 /* Fill *opts with defaults (AUTO precision, planner-chosen sizes). */

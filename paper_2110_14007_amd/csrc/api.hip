@@ -55,6 +55,8 @@ tod_status resolve_options(const tod_options* in, tod_options* out) {
   if (out->margin_scale == 0.0f) out->margin_scale = 1.0f;
   if (!(out->margin_scale >= 1.0f) || isinf(out->margin_scale))
     return fail(TOD_ERR_INVALID_ARG, "margin_scale must be a finite value >= 1");
+  if (out->reorder < -1 || out->reorder > 1)
+    return fail(TOD_ERR_INVALID_ARG, "reorder must be -1, 0 or 1");
   return TOD_OK;
 }
 
@@ -95,7 +97,9 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   p->precision = prec;
   // Shortlist length K': a power of two >= k with room for the certificate's
   // margin.  The margin a row needs grows with the filter's rounding error:
-  // k + 4 at fp32, k + max(8, k/4) at fp16, 2k at bf16.
+  // k + 4 at fp32, k + max(8, k/4) at fp16, k + max(24, k) at bf16 (bf16's
+  // 8-bit significand leaves about one row in ten uncertified at 2k when k is
+  // small).
   int64_t kp;
   if (o.shortlist > 0) {
     kp = o.shortlist;
@@ -104,7 +108,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   } else if (prec == TOD_PREC_FP16) {
     kp = k + (k / 4 > 8 ? (k + 3) / 4 : 8);
   } else {
-    kp = 2 * (int64_t)k;
+    kp = k + (k > 24 ? k : 24);
   }
   if (kp < k) kp = k;
   kp = next_pow2(kp < 16 ? 16 : kp);
@@ -166,6 +170,11 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
       if (prec == TOD_PREC_FP16) p->scale_exp = 14;
     }
   }
+  // Grouped scan order: X against X through the register-list kernel with one
+  // reference split (each workgroup then scans the whole set from its own
+  // group on); by default from kOrderMinRows references on.
+  const bool want = o.reorder > 0 || (o.reorder == 0 && nr >= kOrderMinRows);
+  p->order = (self && p->tile_kind == 1 && p->splits == 1 && want) ? 1 : 0;
   return TOD_OK;
 }
 
@@ -193,6 +202,16 @@ Layout make_layout(const Plan& p) {
   // lists of k entries always suffice.
   L.fbpart = take(sizeof(uint2) * (size_t)tod::kFbGrid * p.k);
   L.fbidx = take(sizeof(uint32_t) * (size_t)tod::kFbGrid * p.k);
+  if (p.order) {
+    const int32_t nb = order_blocks(p.nr);
+    L.perm = take(sizeof(int32_t) * p.nr_pad);
+    L.lab = take(sizeof(int32_t) * p.nr);
+    L.cstart = take(sizeof(int32_t) * (kOrdC + 1));
+    L.bcnt = take(sizeof(int32_t) * (size_t)nb * kOrdC);
+    L.boff = take(sizeof(int32_t) * (size_t)nb * kOrdC);
+  } else {
+    L.perm = L.lab = L.cstart = L.bcnt = L.boff = 0;
+  }
   if (p.lof) {
     L.idx32 = take(sizeof(int32_t) * p.nq * p.k);
     L.d64 = take(sizeof(double) * p.nq * p.k);
@@ -300,6 +319,11 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.worklist = (int32_t*)(base + L.worklist);
   a.fbpart = (uint2*)(base + L.fbpart);
   a.fbidx = (uint32_t*)(base + L.fbidx);
+  a.perm = p.order ? (int32_t*)(base + L.perm) : nullptr;
+  a.lab = p.order ? (int32_t*)(base + L.lab) : nullptr;
+  a.cstart = p.order ? (int32_t*)(base + L.cstart) : nullptr;
+  a.bcnt = p.order ? (int32_t*)(base + L.bcnt) : nullptr;
+  a.boff = p.order ? (int32_t*)(base + L.boff) : nullptr;
   a.idx32 = lof ? (int32_t*)(base + L.idx32) : nullptr;
   a.d64 = lof ? (double*)(base + L.d64) : nullptr;
   a.lrd = lof ? (double*)(base + L.lrd) : nullptr;
@@ -353,6 +377,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     stats->rows_certified = (int64_t)host.certified;
     stats->rows_fallback = (int64_t)host.worklist_count;
     stats->tile_launches = p.blocks;
+    stats->reordered = p.order;
     stats->ms_prep = Timers::ms(e0, e_prep);
     float t = 0.0f, r = 0.0f;
     for (auto& pr : tile_ev) t += Timers::ms(pr.first, pr.second);
@@ -439,6 +464,7 @@ tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_opti
   plan->query_block = p.query_block;
   plan->blocks = p.blocks;
   plan->tile_launches = p.blocks;
+  plan->reordered = p.order;
   return TOD_OK;
 }
 

@@ -361,13 +361,16 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     return v;
   };
   // Rows past the split and the query's own row (self exclusion) never survive.
+  // The row limit is one 32-bit value per sub-tile (rows >= lim are past the
+  // split), so the rare masking code keeps no 64-bit state per row.
   auto mask = [&](f32x16& v, int64_t ts) {
     const bool diag = selfq && ts == q0;
     if (diag || ts + 32 > r_end) {
+      const int lim = ts + 32 > r_end ? (int)(r_end - ts) : 32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = out_row(r, h);
-        if (ts + row >= r_end || (diag && row == col)) v[r] = -INFINITY;
+        if (row >= lim || (diag && row == col)) v[r] = -INFINITY;
       }
     }
   };
@@ -536,34 +539,53 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       }
   };
 
-  TOD_MT_FETCH(r_begin, st, sth)
+  // Stage order.  With the grouped scan order (X against X, one split) the
+  // workgroup starts at the stage holding the first row of the group of its
+  // first query and wraps around; concurrent workgroups mostly share a group,
+  // and so the stream they read.  Otherwise the split is scanned in order.
+  const int nst = (int)((r_end - r_begin + TR - 1) / TR);
+  int st0 = 0;
+  if (a.cstart) {
+    const int p0 = (int)(q_begin + (int64_t)blockIdx.x * (W * 32));
+    int g = 0;
+#pragma unroll
+    for (int i = 1; i < kOrdC; ++i) g = a.cstart[i] <= p0 ? i : g;
+    st0 = (int)((a.cstart[g] - r_begin) / TR);
+  }
+  // First row of the i-th stage scanned (i < 2 nst + 2; stages past the last
+  // one wrap round and are loaded but never read).
+  auto t_of = [&](int i) -> int64_t {
+    int s = st0 + i;
+    s = s >= nst ? s - nst : s;
+    s = s >= nst ? s - nst : s;
+    return r_begin + (int64_t)s * TR;
+  };
+
+  TOD_MT_FETCH(t_of(0), st, sth)
   TOD_MT_PUT(0, st, sth)
   if constexpr (PF2) {
     // Two stages per trip: each register set has a fixed role in straight-line
     // code, so every wait is for the older set only, and the stage barrier
     // (no release fence) leaves the newer set's loads in flight.
-    TOD_MT_FETCH(r_begin + TR, su, suh)
+    TOD_MT_FETCH(t_of(1), su, suh)
     stage_barrier();
-    for (int64_t t0 = r_begin;;) {
-      TOD_MT_FETCH(t0 + 2 * TR, st, sth)  // past the end: clamped rows nobody reads
-      stage_body(t0, 0);
+    for (int it = 0;;) {
+      TOD_MT_FETCH(t_of(it + 2), st, sth)
+      stage_body(t_of(it), 0);
       TOD_MT_PUT(1, su, suh)
       stage_barrier();
-      t0 += TR;
-      if (t0 >= r_end) break;
-      TOD_MT_FETCH(t0 + 2 * TR, su, suh)
-      stage_body(t0, 1);
+      if (++it >= nst) break;
+      TOD_MT_FETCH(t_of(it + 2), su, suh)
+      stage_body(t_of(it), 1);
       TOD_MT_PUT(0, st, sth)
       stage_barrier();
-      t0 += TR;
-      if (t0 >= r_end) break;
+      if (++it >= nst) break;
     }
   } else {
     __syncthreads();
-    int it = 0;
-    for (int64_t t0 = r_begin; t0 < r_end; t0 += TR, ++it) {
-      TOD_MT_FETCH(t0 + TR, st, sth)  // past the end this reloads clamped rows nobody reads
-      stage_body(t0, it & 1);
+    for (int it = 0; it < nst; ++it) {
+      TOD_MT_FETCH(t_of(it + 1), st, sth)
+      stage_body(t_of(it), it & 1);
       TOD_MT_PUT((it + 1) & 1, st, sth)
       __syncthreads();
     }

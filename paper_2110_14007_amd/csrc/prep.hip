@@ -14,6 +14,8 @@
 //   hn   = -0.5 * fl32(N)                      (reference rows: accumulator seed)
 //   rho  >= ||c - xhat||                       (quantisation radius, rounded up)
 // and over the references the maxima Nmax = max N and Pmax = max rho.
+// With the grouped scan order (order.hip) the reference rows are written in
+// that order: position p holds input row perm[p].
 #include <math.h>
 
 #include "tod_internal.h"
@@ -146,7 +148,8 @@ __global__ void __launch_bounds__(kThreads)
 quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, int dpad,
                 const float* __restrict__ mu32, Ctrl* ctrl, T* __restrict__ xq,
                 float* __restrict__ hn, double* __restrict__ n64, double* __restrict__ rho,
-                int is_ref, int fold, int dmain, int scale_exp, double cfold) {
+                int is_ref, int fold, int dmain, int scale_exp, double cfold,
+                const int32_t* __restrict__ perm) {
   const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   double nsq = 0.0, rho_up = 0.0, ferr = 0.0;
   if (row < n_pad) {
@@ -158,7 +161,7 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
       if (rho) rho[row] = 0.0;
     } else {
       const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
-      const float* in = x + row * d;
+      const float* in = x + (perm ? (int64_t)perm[row] : row) * d;
       double r2 = 0.0, c2 = 0.0;
       for (int t = 0; t < d; ++t) {
         const double c = s * ((double)in[t] - (double)mu32[t]);
@@ -226,7 +229,8 @@ __global__ void __launch_bounds__(kThreads)
 quantise_rows_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, int dpad,
                      const float* __restrict__ mu32, Ctrl* ctrl, T* __restrict__ xq,
                      float* __restrict__ hn, double* __restrict__ n64,
-                     double* __restrict__ rho, int is_ref, int scale_exp) {
+                     double* __restrict__ rho, int is_ref, int scale_exp,
+                     const int32_t* __restrict__ perm) {
   const int lane = threadIdx.x & 63;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
@@ -243,7 +247,7 @@ quantise_rows_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int 
       }
       continue;
     }
-    const float* in = x + row * d;
+    const float* in = x + (perm ? (int64_t)perm[row] : row) * d;
     double nsq = 0.0, r2 = 0.0, c2 = 0.0;
     for (int t = lane; t < dpad; t += 64) {
       T q = (T)0.0f;
@@ -286,12 +290,13 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
     hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nr_pad)), dim3(kThreads), 0, st,
                        a.xr, p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r,
                        a.hn_r, p.self ? a.n64_q : (double*)nullptr,
-                       p.self ? a.rho_q : (double*)nullptr, 1, p.scale_exp);
+                       p.self ? a.rho_q : (double*)nullptr, 1, p.scale_exp, a.perm);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.self) return e;
     hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nq_pad)), dim3(kThreads), 0, st,
                        a.xq, p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q,
-                       (float*)nullptr, a.n64_q, a.rho_q, 0, p.scale_exp);
+                       (float*)nullptr, a.n64_q, a.rho_q, 0, p.scale_exp,
+                       (const int32_t*)nullptr);
     return hipGetLastError();
   }
   const double cf = fold_const(p.precision);
@@ -299,13 +304,14 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
   hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_r), dim3(kThreads), 0, st, a.xr,
                      p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r, a.hn_r,
                      p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : (double*)nullptr, 1,
-                     p.fold, p.dmain, p.scale_exp, cf);
+                     p.fold, p.dmain, p.scale_exp, cf, a.perm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.self) return e;
   const int64_t blocks_q = (p.nq_pad + kThreads - 1) / kThreads;
   hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_q), dim3(kThreads), 0, st, a.xq,
                      p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q, (float*)nullptr,
-                     a.n64_q, a.rho_q, 0, p.fold, p.dmain, p.scale_exp, cf);
+                     a.n64_q, a.rho_q, 0, p.fold, p.dmain, p.scale_exp, cf,
+                     (const int32_t*)nullptr);
   return hipGetLastError();
 }
 
@@ -338,6 +344,10 @@ hipError_t launch_prep(const Plan& p, const Args& a, hipStream_t st) {
                        p.nq, (int)p.d, a.mu32, a.ctrl);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (p.order) {
+    e = launch_order(p, a, st);
+    if (e != hipSuccess) return e;
+  }
   switch (p.precision) {
     case TOD_PREC_FP32: return launch_quantise<float>(p, a, st);
     case TOD_PREC_FP16: return launch_quantise<_Float16>(p, a, st);

@@ -205,8 +205,12 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // query serialises millions of same-address atomics).
   uint64_t ncert = 0;
   for (int64_t ql = (int64_t)blockIdx.x * W + wave; ql < q_rows; ql += (int64_t)gridDim.x * W) {
-    const int64_t qi = q_begin + ql;
-    const double ni = a.n64_q[qi], rho_i = a.rho_q[qi];
+    // With the grouped scan order the filter worked on positions: the query's
+    // input row is perm[position], and so is every candidate's (mapped below,
+    // before anything is measured, ranked or written).
+    const int64_t qpos = q_begin + ql;
+    const int64_t qi = a.perm ? (int64_t)a.perm[qpos] : qpos;
+    const double ni = a.n64_q[qpos], rho_i = a.rho_q[qpos];
     // Final aggregation of the per-split candidate lists (Section 6.1).
     const uint64_t* src = a.partial + ql * a.splits * KP;
     uint64_t list[EL];
@@ -227,7 +231,10 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 #pragma unroll
     for (int r = 0; r < EL; ++r) {
       const int e = r * 64 + lane;
-      if (e < KP) sl[wave][e] = list[r];
+      uint64_t v = list[r];
+      if (a.perm && v != kEmpty)
+        v = (v & 0xffffffff00000000ull) | (uint32_t)a.perm[index_of(v)];
+      if (e < KP) sl[wave][e] = v;
     }
     wave_lds_sync();
 

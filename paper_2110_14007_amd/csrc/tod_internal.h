@@ -35,12 +35,13 @@ struct Plan {
   int32_t self;        // query set == reference set (one quantised copy)
   int32_t exclude_self;
   int32_t lof;         // LOF buffers needed
+  int32_t order;       // 1: grouped scan order (order.hip), X against X only
 };
 
 // Workspace regions (byte offsets from the workspace base, 256-aligned).
 struct Layout {
   size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, worklist, fbpart,
-      fbidx, idx32, d64, lrd, total;
+      fbidx, idx32, d64, lrd, perm, lab, cstart, bcnt, boff, total;
   int32_t colpart_blocks;
 };
 
@@ -85,6 +86,12 @@ struct Args {
   int32_t* worklist;   // global query ids that failed the certificate
   uint2* fbpart;       // fallback chunk lists: (D^2 bits hi, lo) [kFbGrid x k]
   uint32_t* fbidx;     // fallback chunk lists: reference ids [kFbGrid x k]
+  // grouped scan order (all null when the input order is kept)
+  int32_t* perm;       // position -> input row [nr]
+  int32_t* lab;        // input row -> group [nr]
+  int32_t* cstart;     // first position of each group [kOrdC + 1]
+  int32_t* bcnt;       // rows per group in each block of kOrdRows rows
+  int32_t* boff;       // first position of each block's rows of each group
   int32_t* idx32;      // [nq x k] neighbour ids (LOF)
   double* d64;         // [nq x k] exact distances (LOF)
   double* lrd;         // [nq] LOF scratch
@@ -110,6 +117,14 @@ __device__ __forceinline__ double scale_from_maxabs(uint32_t bits, int scale_exp
 __host__ __device__ constexpr double fold_const(int precision) {
   return precision == TOD_PREC_FP16 ? 32768.0 : 1.0;
 }
+
+// Grouped scan order: groups, rows per counting block, and the smallest
+// reference set the planner groups by default.
+constexpr int kOrdC = 16;
+constexpr int kOrdRows = 4096;
+constexpr int64_t kOrderMinRows = 4096;
+int32_t order_blocks(int64_t nr);
+hipError_t launch_order(const Plan& p, const Args& a, hipStream_t s);
 
 // Fallback scan grid and the most chunks one failing row is cut into.
 constexpr int kFbGrid = 1024;

@@ -41,6 +41,7 @@ class tod_options(ctypes.Structure):
         ("margin_scale", ctypes.c_float),
         ("force_fallback", ctypes.c_int32),
         ("no_recheck", ctypes.c_int32),
+        ("reorder", ctypes.c_int32),
     ]
 
 
@@ -61,6 +62,7 @@ class tod_stats(ctypes.Structure):
         ("ms_fallback", ctypes.c_float),
         ("ms_score", ctypes.c_float),
         ("ms_total", ctypes.c_float),
+        ("reordered", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:
@@ -114,7 +116,7 @@ def last_error() -> str:
 
 
 def options(precision="auto", exclude_self=False, shortlist=0, query_block=0, ref_splits=0,
-            margin_scale=1.0, force_fallback=False, no_recheck=False) -> tod_options:
+            margin_scale=1.0, force_fallback=False, no_recheck=False, reorder=0) -> tod_options:
     o = tod_options()
     _lib.tod_default_options(ctypes.byref(o))
     o.precision = PRECISIONS[precision] if isinstance(precision, str) else int(precision)
@@ -125,6 +127,7 @@ def options(precision="auto", exclude_self=False, shortlist=0, query_block=0, re
     o.margin_scale = float(margin_scale)
     o.force_fallback = int(bool(force_fallback))
     o.no_recheck = int(bool(no_recheck))
+    o.reorder = int(reorder)
     return o
 
 
@@ -150,7 +153,8 @@ def tod_plan(nq: int, nr: int, d: int, k: int, opts=None) -> dict:
                          ctypes.byref(opts) if opts is not None else None, ctypes.byref(s)),
            "tod_plan")
     return {"precision": PRECISION_NAMES[s.precision], "kprime": s.kprime,
-            "ref_splits": s.ref_splits, "query_block": s.query_block, "blocks": s.blocks}
+            "ref_splits": s.ref_splits, "query_block": s.query_block, "blocks": s.blocks,
+            "reordered": bool(s.reordered)}
 
 
 # ---------------------------------------------------------------------------

@@ -228,3 +228,50 @@ def test_forced_fallback_chunks(env, nq, nr, d, k):
         assert st["rows_fallback"] == nq
         oidx, odist = oracle.knn(xq, xr, k)
         compare_knn(xq, xr, np.arange(nq), idx, dist, oidx, odist, allow_ties=False)
+
+
+# Grouped scan order (tod_options.reorder): the rows are partitioned and laid
+# out group by group, each workgroup starts its scan at its own group, and the
+# recheck maps positions back to input rows.  One reference split is forced:
+# the order applies only then.
+@pytest.mark.parametrize("case", ["line", "lattice", "ints", "dups", "C1", "tiny"])
+def test_reorder_matches_oracle(env, case):
+    rng = np.random.default_rng(41)
+    if case == "line":
+        x, k, ties = workloads.line(10, 4), 3, False
+    elif case == "lattice":
+        x, k, ties = workloads.lattice(9, 2), 5, False
+    elif case == "ints":
+        x, k, ties = rng.integers(-3, 4, (2500, 3)).astype(np.float32), 11, False
+    elif case == "dups":
+        base = rng.standard_normal((300, 6)).astype(np.float32)
+        x, k, ties = np.concatenate([base, base[::3], base[::7]]), 6, False
+    elif case == "C1":
+        x, k, ties = workloads.generate("C1")[0], 10, True
+    else:
+        x, k, ties = rng.standard_normal((70, 5)).astype(np.float32), 9, True
+    say("reorder", case, x.shape, k)
+    st, _ = check_full_lof(env, x, k, allow_ties=ties, precision="fp16", reorder=1, ref_splits=1)
+    assert st["reordered"]
+
+
+@pytest.mark.parametrize("prec", ["fp16", "bf16"])
+def test_reorder_invariance(env, prec):
+    x, _ = workloads.generate("C2", n=6000)
+    on = run_lof(env, x, 20, precision=prec, reorder=1, ref_splits=1)
+    off = run_lof(env, x, 20, precision=prec, reorder=-1, ref_splits=1)
+    say("reorder invariance", prec, on[4], off[4])
+    assert on[4]["reordered"] and not off[4]["reordered"]
+    for u, v in zip(on[:4], off[:4]):
+        np.testing.assert_array_equal(u, v)
+
+
+def test_reorder_default(env):
+    # The planner groups X-against-X scans of 4096+ references with one split.
+    big, _ = workloads.generate("C2", n=5000)
+    small, _ = workloads.generate("C2", n=3000)
+    assert run_lof(env, big, 20, precision="fp16", ref_splits=1)[4]["reordered"]
+    assert not run_lof(env, small, 20, precision="fp16", ref_splits=1)[4]["reordered"]
+    xq = big[:500].copy()
+    _, _, st = run_knn(env, xq, big, 5, precision="fp16", ref_splits=1)
+    assert not st["reordered"]  # separate query set: input order

@@ -51,3 +51,11 @@ def test_workspace_grows_with_problem(tod):
     assert c > 0
     assert tod.tod_workspace_size(10, 10, 4, 11) == 0  # k > nr
     assert tod.tod_workspace_size(10, 12, 4, 5, lof=True) == 0  # LOF needs nq == nr
+
+
+@pytest.mark.parametrize("k,expect", [(5, 32), (10, 64), (20, 64), (50, 128), (200, 256)])
+def test_bf16_shortlist_rule(tod, k, expect):
+    # bf16 keeps k + max(24, k) candidates: at 2k about one row in ten of the
+    # 4,000,000-point d = 8 workload (k = 5) fails the certificate.
+    p = tod.tod_plan(5000, 5000, 16, k, tod.options(precision="bf16"))
+    assert p["kprime"] == expect
