@@ -95,7 +95,8 @@ def cpu_baseline(x, k, target_s):
 # Sources that decide what the tile kernels execute: the kernels themselves,
 # their shared headers and the planner that picks their template arguments.
 TILE_SOURCES = ("api.hip", "tod_internal.h", "wave.h", "halfwave.h", "tile.h", "tile_f32.hip",
-                "tile_f16.hip", "tile_bf16.hip", "mtile.h", "mtile_f16.hip", "mtile_bf16.hip")
+                "tile_f16.hip", "tile_bf16.hip", "mtile.h", "mtile_f16.hip", "mtile_bf16.hip",
+                "order.hip")
 
 
 def kernel_sources_digest():

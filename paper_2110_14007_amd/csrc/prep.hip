@@ -59,12 +59,26 @@ colsum_partial_kernel(const float* __restrict__ x, int64_t n, int d, int64_t row
   }
 }
 
-__global__ void colsum_final_kernel(const double* __restrict__ part, int nb, int d, int64_t n,
-                                    double* __restrict__ mu64, float* __restrict__ mu32) {
-  for (int c = threadIdx.x; c < d; c += blockDim.x) {
-    double t = 0.0;
-    for (int b = 0; b < nb; ++b) t += part[(int64_t)b * d + c];
-    const double m = t / (double)n;
+// One block per group of columns: kThreads / cpb threads per column sum
+// fixed, strided subsets of the partial sums, then a fixed-order tree
+// (deterministic).
+__global__ void __launch_bounds__(kThreads)
+colsum_final_kernel(const double* __restrict__ part, int nb, int d, int64_t n,
+                    double* __restrict__ mu64, float* __restrict__ mu32) {
+  __shared__ double red[kThreads];
+  const int cpb = d < kThreads ? d : kThreads;  // columns per block
+  const int tpc = kThreads / cpb;               // threads per column
+  const int tid = threadIdx.x, cl = tid % cpb, sub = tid / cpb;
+  const int c = blockIdx.x * cpb + cl;
+  double t = 0.0;
+  if (sub < tpc && c < d)
+    for (int b = sub; b < nb; b += tpc) t += part[(int64_t)b * d + c];
+  red[tid] = t;
+  __syncthreads();
+  if (sub == 0 && c < d) {
+    double s = 0.0;
+    for (int i = 0; i < tpc; ++i) s += red[i * cpb + cl];
+    const double m = s / (double)n;
     mu64[c] = m;
     mu32[c] = (float)m;
   }
@@ -79,12 +93,19 @@ maxabs_kernel(const float* __restrict__ x, int64_t rows, int d, const float* __r
   bool bad = false;
   const int64_t total = rows * d;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+  // The column index is tracked incrementally (no division per element).
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cstep = (int)(stride % d);
+  int col = (int)(i0 % d);
+  for (int64_t i = i0; i < total; i += stride) {
     const float v = x[i];
+    const int cc = col;
+    col += cstep;
+    col = col >= d ? col - d : col;
     if (!isfinite(v)) {
       bad = true;
     } else {
-      const double diff = fabs((double)v - (double)mu32[i % d]);
+      const double diff = fabs((double)v - (double)mu32[cc]);
       float f = (float)diff;
       if ((double)f < diff) f = nextafterf(f, INFINITY);
       m = fmaxf(m, f);
@@ -331,8 +352,9 @@ hipError_t launch_prep(const Plan& p, const Args& a, hipStream_t st) {
   const int64_t rpb = (p.nr + nb - 1) / nb;
   hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(kThreads), 0, st, a.xr, p.nr,
                      (int)p.d, rpb, a.colpart);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3(1), dim3(kThreads), 0, st, a.colpart, nb,
-                     (int)p.d, p.nr, a.mu64, a.mu32);
+  const int cpb = p.d < kThreads ? (int)p.d : kThreads;
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)((p.d + cpb - 1) / cpb)),
+                     dim3(kThreads), 0, st, a.colpart, nb, (int)p.d, p.nr, a.mu64, a.mu32);
   const auto grid_for = [](int64_t total) {
     int64_t g = (total + kThreads * 4 - 1) / (kThreads * 4);
     return (unsigned)(g < 1 ? 1 : (g > 4096 ? 4096 : g));

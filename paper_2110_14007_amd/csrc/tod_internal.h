@@ -121,7 +121,7 @@ __host__ __device__ constexpr double fold_const(int precision) {
 // Grouped scan order: groups, rows per counting block, and the smallest
 // reference set the planner groups by default.
 constexpr int kOrdC = 16;
-constexpr int kOrdRows = 4096;
+constexpr int kOrdRows = 1024;
 constexpr int64_t kOrderMinRows = 4096;
 int32_t order_blocks(int64_t nr);
 hipError_t launch_order(const Plan& p, const Args& a, hipStream_t s);
