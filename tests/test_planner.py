@@ -59,3 +59,20 @@ def test_bf16_shortlist_rule(tod, k, expect):
     # 4,000,000-point d = 8 workload (k = 5) fails the certificate.
     p = tod.tod_plan(5000, 5000, 16, k, tod.options(precision="bf16"))
     assert p["kprime"] == expect
+
+
+def test_reorder_rule(tod):
+    # X against X (tod_plan reads exclude_self as "the sets are one") through the
+    # register-list kernel with one split and 4096+ references: grouped order.
+    self_opts = dict(precision="fp16", exclude_self=True)
+    assert tod.tod_plan(100000, 100000, 32, 20, tod.options(**self_opts))["reordered"]
+    assert not tod.tod_plan(100000, 100000, 32, 20,
+                            tod.options(reorder=-1, **self_opts))["reordered"]
+    assert not tod.tod_plan(3000, 3000, 32, 20, tod.options(ref_splits=1, **self_opts))["reordered"]
+    assert tod.tod_plan(3000, 3000, 32, 20,
+                        tod.options(ref_splits=1, reorder=1, **self_opts))["reordered"]
+    assert not tod.tod_plan(100000, 100000, 32, 20, tod.options(precision="fp16"))["reordered"]
+    assert not tod.tod_plan(100000, 100000, 32, 20,
+                            tod.options(precision="fp32", exclude_self=True))["reordered"]
+    with pytest.raises(tod.TodError):
+        tod.tod_plan(100, 100, 4, 3, tod.options(reorder=2))
