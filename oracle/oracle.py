@@ -11,6 +11,8 @@ Functions:
   lof(idx, dist)                          -> (lof, lrd, kdist), fp64 [n]
   lof_rows(x, k, rows)                    -> (lof, lrd, kdist) for the listed rows
   knn_score(dist)                         -> distance to the k-th neighbour
+  nwr(xq, xr, phi, exclude_self, rows=None) -> (row_ptr int64 [m+1], idx int64, dist fp64):
+                                             neighbours within range, CSR, ascending index
 """
 from __future__ import annotations
 
@@ -54,6 +56,9 @@ def _load():
     lib.oracle_lof.restype = ctypes.c_int
     lib.oracle_lof_rows.argtypes = [vp, i64, i64, i32, vp, i64, i32, vp, vp, vp]
     lib.oracle_lof_rows.restype = ctypes.c_int
+    lib.oracle_nwr.argtypes = [vp, i64, vp, i64, i64, ctypes.c_double, i32, vp, i64, i32, vp, vp,
+                               vp, vp]
+    lib.oracle_nwr.restype = ctypes.c_int
     lib.oracle_default_threads.argtypes = []
     lib.oracle_default_threads.restype = ctypes.c_int
     _lib = lib
@@ -129,3 +134,37 @@ def lof_rows(x, k: int, rows, threads: int = 0):
     if rc != 0:
         raise ValueError("oracle_lof_rows failed (rc=%d)" % rc)
     return out[0], out[1], out[2]
+
+
+def nwr(xq, xr, phi: float, exclude_self: bool = False, rows=None, threads: int = 0):
+    """Neighbours within range phi (a radius) of each query row, as CSR.
+
+    A pair is in range iff its fp64 squared distance is <= phi * phi; each
+    row lists its references in increasing index.
+    """
+    xq, xr = _f32(xq), _f32(xr)
+    if xq.shape[1] != xr.shape[1]:
+        raise ValueError("dimension mismatch")
+    lib = _load()
+    if rows is not None:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        m = rows.shape[0]
+    else:
+        m = xq.shape[0]
+    rp = _ptr(rows) if rows is not None else None
+    counts = np.empty(m, dtype=np.int64)
+    rc = lib.oracle_nwr(_ptr(xq), xq.shape[0], _ptr(xr), xr.shape[0], xq.shape[1], float(phi),
+                        int(bool(exclude_self)), rp, m, int(threads), _ptr(counts), None, None, None)
+    if rc != 0:
+        raise ValueError("oracle_nwr rejected its arguments (rc=%d)" % rc)
+    row_ptr = np.zeros(m + 1, dtype=np.int64)
+    np.cumsum(counts, out=row_ptr[1:])
+    nnz = int(row_ptr[-1])
+    idx = np.empty(max(nnz, 1), dtype=np.int64)
+    dist = np.empty(max(nnz, 1), dtype=np.float64)
+    rc = lib.oracle_nwr(_ptr(xq), xq.shape[0], _ptr(xr), xr.shape[0], xq.shape[1], float(phi),
+                        int(bool(exclude_self)), rp, m, int(threads), None, _ptr(row_ptr),
+                        _ptr(idx), _ptr(dist))
+    if rc != 0:
+        raise ValueError("oracle_nwr fill failed (rc=%d)" % rc)
+    return row_ptr, idx[:nnz], dist[:nnz]

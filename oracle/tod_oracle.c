@@ -383,3 +383,66 @@ done:
   free(ldist);
   return status;
 }
+
+/* -------------------------------------------------------------------------- */
+/* Neighbours within range.                                                    */
+/* -------------------------------------------------------------------------- */
+
+/*
+ * NWR (Section 5.3): for a query row i, every reference row j whose distance
+ * is at most the threshold phi.  phi is a radius; a pair is in range iff the
+ * squared distance D2 (the same sequential fp64 direct-difference sum as the
+ * kNN above) satisfies D2 <= phi * phi, both sides in fp64.  References are
+ * listed in increasing j.
+ */
+typedef struct {
+  const float* xq;
+  const float* xr;
+  int64_t nr, d;
+  double phi2;
+  int32_t exclude_self;
+  const int64_t* rows;
+  int64_t* counts;       /* count pass: pairs per row */
+  const int64_t* start;  /* fill pass: first output slot per row, or NULL */
+  int64_t* idx_out;
+  double* dist_out;
+} nwr_ctx;
+
+static void nwr_rows(void* p, int64_t begin, int64_t end) {
+  nwr_ctx* c = (nwr_ctx*)p;
+  for (int64_t r = begin; r < end; ++r) {
+    const int64_t qi = c->rows ? c->rows[r] : r;
+    const float* q = c->xq + qi * c->d;
+    int64_t m = 0;
+    for (int64_t j = 0; j < c->nr; ++j) {
+      if (c->exclude_self && j == qi) continue;
+      double d2 = sq_dist(q, c->xr + j * c->d, c->d);
+      if (!(d2 <= c->phi2)) continue;
+      if (c->start) {
+        c->idx_out[c->start[r] + m] = j;
+        c->dist_out[c->start[r] + m] = sqrt(d2);
+      }
+      ++m;
+    }
+    if (!c->start) c->counts[r] = m;
+  }
+}
+
+/*
+ * Count pass: counts_out[nrows] = pairs in range per query row.
+ * Fill pass (start != NULL): row r's pairs go to idx_out / dist_out from
+ * start[r] on (Euclidean distances, fp64).
+ */
+int oracle_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d, double phi,
+               int32_t exclude_self, const int64_t* rows, int64_t nrows, int32_t nthreads,
+               int64_t* counts_out, const int64_t* start, int64_t* idx_out, double* dist_out) {
+  if (!xq || !xr || nq <= 0 || nr <= 0 || d <= 0 || !(phi >= 0.0)) return ORACLE_EINVAL;
+  if (start ? (!idx_out || !dist_out) : !counts_out) return ORACLE_EINVAL;
+  int64_t count = rows ? nrows : nq;
+  if (rows)
+    for (int64_t r = 0; r < nrows; ++r)
+      if (rows[r] < 0 || rows[r] >= nq) return ORACLE_EINVAL;
+  nwr_ctx c = {xq, xr, nr, d, phi * phi, exclude_self, rows, counts_out, start, idx_out, dist_out};
+  parallel_for(count, nthreads, nwr_rows, &c);
+  return ORACLE_OK;
+}

@@ -263,3 +263,110 @@ def test_workload_shapes_small():
         assert y.shape == (3000,) and 0 < y.sum() < 3000
         x2, _ = workloads.generate(name, n=3000)
         np.testing.assert_array_equal(x, x2)
+
+
+# ---------------------------------------------------------------------------
+# Neighbours within range (NWR, Section 5.3): phi is a radius, a pair is in
+# range iff its squared distance is <= phi^2.
+# ---------------------------------------------------------------------------
+
+def _nwr_lists(row_ptr, idx):
+    return [idx[row_ptr[i]:row_ptr[i + 1]].tolist() for i in range(len(row_ptr) - 1)]
+
+
+@pytest.mark.parametrize("phi,offsets", [
+    (1.0, [(0, 0), (1, 0), (-1, 0), (0, 1), (0, -1)]),           # boundary pairs (D = 1) count
+    (1.25, [(0, 0), (1, 0), (-1, 0), (0, 1), (0, -1)]),          # between 1 and sqrt 2
+    (math.sqrt(2.0), [(a, b) for a in (-1, 0, 1) for b in (-1, 0, 1)]),  # fl(sqrt2)^2 > 2
+    (1.5, [(a, b) for a in (-1, 0, 1) for b in (-1, 0, 1)]),
+    (2.0, [(a, b) for a in (-2, -1, 0, 1, 2) for b in (-2, -1, 0, 1, 2) if a * a + b * b <= 4]),
+    (0.999, [(0, 0)]),
+])
+@pytest.mark.parametrize("excl", [False, True])
+def test_nwr_lattice_closed_forms(oracle_mod, phi, offsets, excl):
+    side = 9
+    x = workloads.lattice(side, 2)
+    rp, idx, dist = oracle_mod.nwr(x, x, phi, exclude_self=excl)
+    coords = x.astype(int)
+    pos = {tuple(c): i for i, c in enumerate(coords.tolist())}
+    for i, (r, c) in enumerate(coords.tolist()):
+        want = sorted(pos[(r + a, c + b)] for a, b in offsets
+                      if (r + a, c + b) in pos and not (excl and a == 0 and b == 0))
+        got = idx[rp[i]:rp[i + 1]].tolist()
+        assert got == want, (i, got, want)
+        np.testing.assert_array_equal(
+            dist[rp[i]:rp[i + 1]],
+            [math.sqrt((coords[j][0] - r) ** 2 + (coords[j][1] - c) ** 2) for j in want])
+
+
+@pytest.mark.parametrize("d", [1, 4])
+def test_nwr_line_windows(oracle_mod, d):
+    x = workloads.line(10, d)
+    rp, idx, _ = oracle_mod.nwr(x, x, 2.0, exclude_self=True)
+    assert _nwr_lists(rp, idx) == [[j for j in range(max(0, i - 2), min(10, i + 3)) if j != i]
+                                   for i in range(10)]
+
+
+def _exact_nwr(xq, xr, phi2, exclude_self):
+    fq = [[Fraction(float(v)) for v in row] for row in xq]
+    fr = [[Fraction(float(v)) for v in row] for row in xr]
+    out = []
+    for i, q in enumerate(fq):
+        out.append([j for j, r in enumerate(fr) if not (exclude_self and i == j)
+                    and sum((a - b) * (a - b) for a, b in zip(q, r)) <= phi2])
+    return out
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_nwr_exact_rational_bruteforce(oracle_mod, case):
+    x, _ = _tiny_cases()[case]
+    fx = [[Fraction(float(v)) for v in row] for row in x]
+    d2 = sorted({sum((a - b) * (a - b) for a, b in zip(p, q)) for p in fx for q in fx})
+    # A radius strictly inside a gap between two exact squared distances, far
+    # from both relative to fp64 rounding, so that the fp64 decision is exact.
+    gaps = [(b - a, a, b) for a, b in zip(d2, d2[1:]) if b - a > Fraction(1, 10 ** 6) * b]
+    _, lo, hi = gaps[len(gaps) // 2]
+    mid = (lo + hi) / 2
+    phi = math.sqrt(float(mid))
+    for excl in (False, True):
+        rp, idx, _ = oracle_mod.nwr(x, x, phi, exclude_self=excl)
+        assert _nwr_lists(rp, idx) == _exact_nwr(x, x, mid, excl)
+
+
+def test_nwr_contains_knn(oracle_mod):
+    x, _ = workloads.generate("C1")
+    k = 10
+    kidx, kdist = oracle_mod.knn_self(x, k)
+    r = kdist[:, -1]
+    rows = np.arange(0, len(x), 7)
+    for i in rows:
+        rp, idx, _ = oracle_mod.nwr(x, x, float(r[i]) * (1 + 1e-9), exclude_self=True, rows=[i])
+        got = set(idx.tolist())
+        assert set(kidx[i].tolist()) <= got and len(got) >= k
+        if kdist[i, -2] < r[i] * (1 - 1e-9):
+            rp, idx, _ = oracle_mod.nwr(x, x, float(r[i]) * (1 - 1e-9), exclude_self=True,
+                                        rows=[i])
+            assert len(idx) == k - 1
+
+
+def test_nwr_invariances(oracle_mod):
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((300, 6)).astype(np.float32)
+    rp, idx, dist = oracle_mod.nwr(x, x, 2.0)
+    perm = rng.permutation(len(x))
+    rp2, idx2, dist2 = oracle_mod.nwr(x[perm], x[perm], 2.0)
+    inv = np.argsort(perm)
+    for i in range(len(x)):
+        a = sorted(perm[idx2[rp2[inv[i]]:rp2[inv[i] + 1]]].tolist())
+        assert a == idx[rp[i]:rp[i + 1]].tolist()
+    rp3, idx3, dist3 = oracle_mod.nwr(x * 8, x * 8, 16.0)  # power-of-two scaling is exact
+    np.testing.assert_array_equal(rp3, rp)
+    np.testing.assert_array_equal(idx3, idx)
+    np.testing.assert_array_equal(dist3, dist * 8)
+
+
+def test_nwr_rejects_bad_arguments(oracle_mod):
+    x = np.zeros((4, 2), np.float32)
+    for phi in (-1.0, float("nan")):
+        with pytest.raises(ValueError):
+            oracle_mod.nwr(x, x, phi)
