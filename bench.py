@@ -3,6 +3,9 @@
 One step = one tod_lof call on the whole workload: prep, fused distance tiles
 with top-K' selection, certificate + exact recheck, fallback, kNN-OD score
 and LOF for every point.  Inputs are resident in HBM before timing starts.
+For a neighbours-within-range workload (--workload N1) one step is one
+tod_nwr call: prep, the range tile's count and fill passes, exact
+verification of the uncertain pairs and the CSR output with distances.
 
 Prints ONE JSON line (see the design doc for the field definitions).
 """
@@ -96,7 +99,7 @@ def cpu_baseline(x, k, target_s):
 # their shared headers and the planner that picks their template arguments.
 TILE_SOURCES = ("api.hip", "tod_internal.h", "wave.h", "halfwave.h", "tile.h", "tile_f32.hip",
                 "tile_f16.hip", "tile_bf16.hip", "mtile.h", "mtile_f16.hip", "mtile_bf16.hip",
-                "order.hip")
+                "order.hip", "rtile.h", "rtile_f16.hip", "rtile_bf16.hip")
 
 
 def kernel_sources_digest():
@@ -131,6 +134,104 @@ def recorded_traffic(workload, kernel):
     return traffic
 
 
+def cpu_baseline_nwr(x, phi, target_s):
+    """The oracle's neighbours within range on a bounded sample of query rows."""
+    import numpy as np
+
+    from oracle import oracle
+    n = x.shape[0]
+    order = np.random.default_rng(2024).permutation(n).astype(np.int64)
+    rows_done, t_total, batch = 0, 0.0, 64
+    while t_total < target_s and rows_done < n:
+        m = min(batch, n - rows_done)
+        rows = np.sort(order[rows_done:rows_done + m])
+        t0 = time.perf_counter()
+        oracle.nwr(x, x, phi, exclude_self=True, rows=rows)
+        t_total += time.perf_counter() - t0
+        rows_done += m
+        if t_total < target_s / 4:
+            batch *= 2
+    return {
+        "value": rows_done / t_total,
+        "unit": "points/s",
+        "cores": oracle.default_threads(),
+        "kind": "oracle",
+        "sample": "exact fp64 neighbours within range (phi=%g) of %d distinct seeded-random "
+                  "query rows against all %d reference rows, %.1f s of oracle time"
+                  % (phi, rows_done, n, t_total),
+    }
+
+
+def bench_nwr(args, w):
+    """One step = one tod_nwr call (X against itself, self excluded, with distances)."""
+    import numpy as np
+    import torch
+
+    from paper_2110_14007_amd import tod, workloads
+
+    x_host, _ = workloads.generate(w.name)
+    n, d = x_host.shape
+    phi = float(w.extra["phi"])
+    x = torch.from_numpy(x_host).to("cuda:0")
+    opts = tod.options(precision=args.precision, exclude_self=True)
+    ws = tod.Workspace()
+    rp, idx, _ = tod.tod_nwr(x, x, phi, opts, workspace=ws)  # sizes the outputs
+    cap = int(idx.numel())
+    for _ in range(max(args.warmup - 1, 0)):
+        tod.tod_nwr(x, x, phi, opts, workspace=ws, capacity=cap)
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        st = tod.new_stats()
+        tod.tod_nwr(x, x, phi, opts, workspace=ws, capacity=cap, stats=st)
+        stats.append(st.as_dict())
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    def avg(key):
+        return float(np.mean([s[key] for s in stats]))
+
+    prec = stats[0]["precision"]
+    launches = stats[0]["tile_launches"]
+    # the count pass and the fill passes each evaluate every pair once
+    flops = 2.0 * 2.0 * d * float(n) * float(n)
+    tile_ms = avg("ms_tile") / launches
+    achieved = flops / launches / (tile_ms * 1e-3) / 1e12
+    kname = "range_tile<%s,d=%d>" % (prec, d)
+    line = {
+        "metric": METRIC,
+        "value": round(n / (ms_step * 1e-3), 1),
+        "unit": "points/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "%s+f64" % prec.replace("fp", "f"),
+        "data": "synthetic",
+        "config": {"workload": "%s: %s" % (w.name, w.description), "n": n, "d": d, "phi": phi,
+                   "filter_precision": prec, "ref_splits": stats[0]["ref_splits"],
+                   "batches": stats[0]["blocks"], "parallelism": "single GPU"},
+        "pairs_per_s": float(n) * float(n) / (ms_step * 1e-3),
+        "pairs_in_range": stats[0]["pairs_in_range"],
+        "pairs_candidate": stats[0]["pairs_candidate"],
+        "pairs_uncertain": stats[0]["pairs_uncertain"],
+        "phase_ms": {key: round(avg(key), 4) for key in ("ms_prep", "ms_tile", "ms_recheck",
+                                                         "ms_total")},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_MFMA_F16,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_F16, 4),
+                     "traffic": recorded_traffic(w.name, kname), "kernel": kname,
+                     "launch_ms": round(tile_ms, 4)},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_nwr(x_host, phi, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -146,6 +247,9 @@ def main():
     from paper_2110_14007_amd import tod, workloads
 
     w = workloads.WORKLOADS[args.workload]
+    if w.name.startswith("N"):
+        bench_nwr(args, w)
+        return
     x_host, _ = workloads.generate(args.workload)
     n, d, k = x_host.shape[0], x_host.shape[1], w.k
     dev = torch.device("cuda:0")

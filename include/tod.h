@@ -53,7 +53,9 @@ typedef enum {
   TOD_ERR_WORKSPACE = 3,   /* workspace smaller than tod_workspace_size() or misaligned */
   TOD_ERR_UNSUPPORTED = 4, /* k > 256, d > 4096, or more than 2^31 - 1 rows */
   TOD_ERR_HIP = 5,         /* a HIP launch or runtime call failed; see tod_last_error() */
-  TOD_ERR_INTERNAL = 6
+  TOD_ERR_INTERNAL = 6,
+  TOD_ERR_CAPACITY = 7     /* tod_nwr: more pairs in range than the output capacity (the row
+                            * offsets and the total are still written) */
 } tod_status;
 
 /* Precision of the shortlist filter (the exact recheck always works from the
@@ -96,6 +98,9 @@ typedef struct {
   int64_t tile_launches;  /* launches of the fused distance + selection kernel */
   float ms_prep, ms_tile, ms_recheck, ms_fallback, ms_score, ms_total;
   int32_t reordered;      /* 1 if the scan used the grouped row order (see tod_options.reorder) */
+  int64_t pairs_candidate; /* tod_nwr: pairs the filter could not rule out of range */
+  int64_t pairs_uncertain; /* tod_nwr: candidates the filter could not rule in either (recomputed) */
+  int64_t pairs_in_range;  /* tod_nwr: pairs within the threshold */
 } tod_stats;
 
 /* Fill *opts with defaults (AUTO precision, planner-chosen sizes). */
@@ -150,6 +155,45 @@ tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_op
  */
 tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,
                     tod_stats* plan);
+
+/*
+ * Neighbours within range (NWR, Section 5.3: the case study of provable
+ * quantization).  For every query row i, the reference rows j whose
+ * Euclidean distance is at most phi.  The decision is exact: a pair is in
+ * range iff its squared distance, summed in fp64 over the columns in order
+ * from the fp32 rows ((double)x - (double)y, squared, added), is at most
+ * phi * phi rounded to fp64.  The filter evaluates every pair in fp16 / bf16
+ * (MFMA, fp32 accumulation); pairs it can place on neither side of phi with
+ * certainty (Eq. (nwr-check)'s test |D - phi| > Err, with this library's
+ * error bound) are recomputed exactly, the others are decided by the filter.
+ *   row_ptr_out[nq + 1] int64 (device): CSR offsets, row i's pairs occupy
+ *                       [row_ptr_out[i], row_ptr_out[i + 1]).  Always written.
+ *   idx_out[capacity]   int64 (device), nullable: reference ids, ascending
+ *                       within a row.  NULL = count only.
+ *   dist_out[capacity]  fp32 (device), nullable: their Euclidean distances
+ *                       (fp64 rounded to fp32).
+ *   total_out           HOST pointer, nullable: the number of pairs in range.
+ * opts: precision AUTO (= FP16) or FP16 / BF16 (FP32 is TOD_ERR_UNSUPPORTED:
+ * the range filter is an MFMA tile), exclude_self (drops j == i; requires
+ * xq == xr and nq == nr), ref_splits, margin_scale, force_fallback (no pair
+ * is ruled in by the filter: every candidate is recomputed).  shortlist,
+ * query_block, no_recheck and reorder do not apply.
+ * Workspace: a fixed part plus room for candidate pairs (8 bytes each);
+ * tod_nwr_workspace_size() gives the fixed part plus room for 64 candidates
+ * per query row and 2^20 more.  Any extra bytes are used as candidate room.
+ * Query rows are processed in as many batches (of multiples of 32 rows) as
+ * that room needs: automatic batching sized to memory (Section 6).
+ * TOD_ERR_WORKSPACE if 32 consecutive query rows have more candidates than
+ * the room holds (tod_last_error() names the bytes needed).
+ * TOD_ERR_CAPACITY if idx_out is given and the total exceeds capacity; then
+ * row_ptr_out and *total_out are valid and idx_out / dist_out unspecified.
+ * Requires phi finite and >= 0, d <= 512.
+ */
+size_t tod_nwr_workspace_size(int64_t nq, int64_t nr, int64_t d, const tod_options* opts);
+tod_status tod_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                   double phi, const tod_options* opts, void* workspace, size_t ws_bytes,
+                   void* stream, int64_t* row_ptr_out, int64_t capacity, int64_t* idx_out,
+                   float* dist_out, int64_t* total_out, tod_stats* stats);
 
 /* Static string naming a status code. */
 const char* tod_status_string(tod_status status);

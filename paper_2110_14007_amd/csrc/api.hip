@@ -223,6 +223,91 @@ Layout make_layout(const Plan& p) {
   return L;
 }
 
+// Neighbours within range: the fp16 / bf16 MFMA range tile (rtile.h) over
+// rows padded to a power of two of at least 16 elements, reference splits by
+// the kNN rule, no query blocks of its own (the batches follow from the
+// candidate counts and the workspace, see tod_nwr).
+tod_status make_plan_nwr(int64_t nq, int64_t nr, int64_t d, int32_t self, const tod_options& o,
+                         Plan* p, const char** why) {
+  *why = "";
+  memset(p, 0, sizeof(*p));
+  p->nq = nq;
+  p->nr = nr;
+  p->d = d;
+  p->self = self;
+  p->exclude_self = o.exclude_self ? 1 : 0;
+  int32_t prec = o.precision == TOD_PREC_AUTO ? TOD_PREC_FP16 : o.precision;
+  if (prec == TOD_PREC_FP32) {
+    *why = "tod_nwr filters in fp16 or bf16 (MFMA); fp32 is not offered";
+    return TOD_ERR_UNSUPPORTED;
+  }
+  if (d > 512) {
+    *why = "tod_nwr supports rows of at most 512 elements";
+    return TOD_ERR_UNSUPPORTED;
+  }
+  p->precision = prec;
+  p->dpad = p->dpad_t = (int32_t)next_pow2(round_up(d, 16));
+  p->esize = 2;
+  p->scale_exp = 14;
+  p->nq_pad = round_up(nq, 32);
+  p->nr_pad = round_up(nr, 32);
+  p->query_block = p->nq_pad;
+  p->blocks = 1;
+  const int64_t waves = p->nq_pad / 32;
+  int64_t s;
+  if (o.ref_splits > 0) {
+    s = o.ref_splits;
+  } else {
+    s = (2048 + waves - 1) / waves;
+    const int64_t cap = nr / 2048 > 1 ? nr / 2048 : 1;
+    if (s > cap) s = cap;
+    if (s > 16) s = 16;
+  }
+  if (s < 1) s = 1;
+  const int64_t len = round_up((nr + s - 1) / s, 32);
+  p->splits = (int32_t)((nr + len - 1) / len);
+  p->split_len = len;
+  p->waves_per_group = 4;
+  p->tile_kind = 2;
+  return TOD_OK;
+}
+
+NwrLayout make_layout_nwr(const Plan& p) {
+  NwrLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  L.colpart_blocks = colsum_blocks(p.nr);
+  L.groups = p.nq_pad / 32;
+  const int64_t nc = p.nq * p.splits;
+  L.ctrl = take(sizeof(Ctrl));
+  L.mu64 = take(sizeof(double) * p.d);
+  L.mu32 = take(sizeof(float) * p.d);
+  L.colpart = take(sizeof(double) * p.d * L.colpart_blocks);
+  L.xq_r = take((size_t)p.nr_pad * p.dpad * p.esize);
+  L.xq_q = p.self ? L.xq_r : take((size_t)p.nq_pad * p.dpad * p.esize);
+  L.hn_r = take(sizeof(float) * p.nr_pad);
+  L.n64_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
+  L.rho_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
+  L.ccount = take(sizeof(int32_t) * p.nq_pad * p.splits);
+  L.coff = take(sizeof(int64_t) * (nc + 1));
+  const int64_t parts = scan_parts(nc > p.nq ? nc : p.nq);
+  L.part = take(sizeof(int64_t) * parts);
+  L.goff = take(sizeof(int64_t) * (L.groups + 1));
+  L.incnt = take(sizeof(int32_t) * p.nq);
+  L.cand = off;
+  return L;
+}
+
+int64_t nwr_candidate_room(const NwrLayout& L, size_t ws_bytes) {
+  if (ws_bytes < L.cand + 512) return 0;
+  // ids (4 B) and distances (4 B), each region 256-aligned
+  return (int64_t)((ws_bytes - L.cand - 512) / 8);
+}
+
 }  // namespace tod
 
 namespace {
@@ -378,6 +463,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     stats->rows_fallback = (int64_t)host.worklist_count;
     stats->tile_launches = p.blocks;
     stats->reordered = p.order;
+    stats->pairs_candidate = stats->pairs_uncertain = stats->pairs_in_range = 0;
     stats->ms_prep = Timers::ms(e0, e_prep);
     float t = 0.0f, r = 0.0f;
     for (auto& pr : tile_ev) t += Timers::ms(pr.first, pr.second);
@@ -389,6 +475,176 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     stats->ms_total = Timers::ms(e0, e_end);
   }
   if (host.nonfinite) return fail(TOD_ERR_NONFINITE, "input contains NaN or Inf");
+  return TOD_OK;
+}
+
+tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                   double phi, const tod_options* opts_in, void* ws, size_t ws_bytes,
+                   void* stream, int64_t* row_ptr_out, int64_t capacity, int64_t* idx_out,
+                   float* dist_out, int64_t* total_out, tod_stats* stats) {
+  g_last_error.clear();
+  tod_options o;
+  tod_status st = resolve_options(opts_in, &o);
+  if (st != TOD_OK) return st;
+  if (stats && stats->struct_size != sizeof(tod_stats))
+    return fail(TOD_ERR_INVALID_ARG, "tod_stats.struct_size does not match this library");
+  if (!xq || !xr) return fail(TOD_ERR_INVALID_ARG, "null input pointer");
+  if (!row_ptr_out) return fail(TOD_ERR_INVALID_ARG, "null row_ptr output");
+  if (!ws) return fail(TOD_ERR_INVALID_ARG, "null workspace");
+  if (!(phi >= 0.0) || isinf(phi)) return fail(TOD_ERR_INVALID_ARG, "phi must be finite and >= 0");
+  if (idx_out && capacity < 0) return fail(TOD_ERR_INVALID_ARG, "capacity must be >= 0");
+  if (dist_out && !idx_out) return fail(TOD_ERR_INVALID_ARG, "dist_out needs idx_out");
+  if (nq <= 0 || nr <= 0) return fail(TOD_ERR_INVALID_ARG, "row counts must be positive");
+  if (d <= 0) return fail(TOD_ERR_INVALID_ARG, "d must be positive");
+  if (nq > kMaxRows || nr > kMaxRows) return fail(TOD_ERR_UNSUPPORTED, "more than 2^31 - 1 rows");
+  const int32_t self = (xq == xr && nq == nr) ? 1 : 0;
+  if (o.exclude_self && !self)
+    return fail(TOD_ERR_INVALID_ARG, "exclude_self requires the query set to be the reference set");
+  if (((uintptr_t)xq | (uintptr_t)xr) & 15)
+    return fail(TOD_ERR_INVALID_ARG, "input pointers must be 16-byte aligned");
+  if ((uintptr_t)ws & 255) return fail(TOD_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  Plan p;
+  const char* why = "";
+  st = tod::make_plan_nwr(nq, nr, d, self, o, &p, &why);
+  if (st != TOD_OK) return fail(st, why);
+  const tod::NwrLayout L = tod::make_layout_nwr(p);
+  const int64_t room = tod::nwr_candidate_room(L, ws_bytes);
+  if (room < 1)
+    return fail(TOD_ERR_WORKSPACE, "workspace too small: need more than " +
+                                       std::to_string(L.cand + 512) + " bytes, got " +
+                                       std::to_string(ws_bytes));
+  char* base = (char*)ws;
+  Args a;
+  memset(&a, 0, sizeof(a));
+  a.xq = xq;
+  a.xr = xr;
+  a.nq = nq;
+  a.nr = nr;
+  a.d = (int32_t)d;
+  a.dpad = p.dpad;
+  a.splits = p.splits;
+  a.split_len = p.split_len;
+  a.exclude_self = p.exclude_self;
+  a.precision = p.precision;
+  a.margin_scale = o.margin_scale;
+  a.force_fallback = o.force_fallback ? 1 : 0;
+  a.scale_exp = p.scale_exp;
+  a.ctrl = (tod::Ctrl*)(base + L.ctrl);
+  a.mu64 = (double*)(base + L.mu64);
+  a.mu32 = (float*)(base + L.mu32);
+  a.colpart = (double*)(base + L.colpart);
+  a.xq_r = base + L.xq_r;
+  a.xq_q = base + L.xq_q;
+  a.hn_r = (float*)(base + L.hn_r);
+  a.n64_q = (double*)(base + L.n64_q);
+  a.rho_q = (double*)(base + L.rho_q);
+  a.phi = phi;
+  a.ccount = (int32_t*)(base + L.ccount);
+  a.coff = (int64_t*)(base + L.coff);
+  a.incnt = (int32_t*)(base + L.incnt);
+  a.cand = (uint32_t*)(base + L.cand);
+  a.cand_d = (float*)(base + L.cand + ((size_t)room * 4 + 255) / 256 * 256);
+  a.ccap = room;
+  a.row_ptr = row_ptr_out;
+  a.idx_out = idx_out;
+  a.dist_out = dist_out;
+  a.out_cap = idx_out ? capacity : 0;
+  int64_t* part = (int64_t*)(base + L.part);
+  int64_t* goff = (int64_t*)(base + L.goff);
+  const auto tile = p.precision == TOD_PREC_FP16 ? tod::launch_range_tile_f16
+                                                 : tod::launch_range_tile_bf16;
+
+  hipStream_t s = (hipStream_t)stream;
+  Timers tm;
+  tm.on = stats != nullptr;
+  hipEvent_t e0 = tm.mark(s);
+  hipError_t he = tod::launch_prep(p, a, s);
+  if (he != hipSuccess) return hip_fail(he, "prep launch");
+  hipEvent_t e_prep = tm.mark(s);
+  he = tile(p, a, 0, nq, false, s);
+  if (he != hipSuccess) return hip_fail(he, "range tile launch (count)");
+  hipEvent_t e_count = tm.mark(s);
+  he = tod::launch_scan(a.ccount, nq * p.splits, a.coff, nullptr, part, s);
+  if (he == hipSuccess) he = tod::launch_group_offsets(a, L.groups, goff, s);
+  if (he != hipSuccess) return hip_fail(he, "candidate offsets launch");
+  hipEvent_t e_scan = tm.mark(s);
+  // Candidate offsets at 32-row group boundaries decide the batches.
+  std::vector<int64_t> g(L.groups + 1);
+  tod::Ctrl host;
+  he = hipMemcpyAsync(g.data(), goff, sizeof(int64_t) * g.size(), hipMemcpyDeviceToHost, s);
+  if (he == hipSuccess) he = hipMemcpyAsync(&host, a.ctrl, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
+  if (he != hipSuccess) return hip_fail(he, "candidate count readback");
+  if (host.nonfinite) return fail(TOD_ERR_NONFINITE, "input contains NaN or Inf");
+  std::vector<std::pair<int64_t, int64_t>> batches;  // [group begin, group end)
+  for (int64_t g0 = 0; g0 < L.groups;) {
+    int64_t g1 = g0 + 1;
+    if (g[g1] - g[g0] > room) {
+      const size_t need = L.cand + 512 + (size_t)(g[g1] - g[g0]) * 8;
+      return fail(TOD_ERR_WORKSPACE,
+                  "workspace too small: 32 query rows have " + std::to_string(g[g1] - g[g0]) +
+                      " candidate pairs; need at least " + std::to_string(need) + " bytes");
+    }
+    while (g1 < L.groups && g[g1 + 1] - g[g0] <= room) ++g1;
+    batches.emplace_back(g0, g1);
+    g0 = g1;
+  }
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> tile_ev, rc_ev;
+  int64_t largest = 0;
+  for (const auto& bt : batches) {
+    const int64_t b0 = 32 * bt.first;
+    const int64_t b1 = 32 * bt.second < nq ? 32 * bt.second : nq;
+    const int64_t rows = b1 - b0;
+    largest = rows > largest ? rows : largest;
+    a.cbase = g[bt.first];
+    hipEvent_t ts = tm.mark(s);
+    he = tile(p, a, b0, rows, true, s);
+    if (he != hipSuccess) return hip_fail(he, "range tile launch (fill)");
+    hipEvent_t te = tm.mark(s);
+    he = tod::launch_range_verify(a, b0, rows, dist_out ? 1 : 0, s);
+    if (he == hipSuccess)
+      he = tod::launch_scan(a.incnt + b0, rows, row_ptr_out + b0, b0 ? row_ptr_out + b0 : nullptr,
+                            part, s);
+    if (he == hipSuccess && idx_out) he = tod::launch_range_emit(a, b0, rows, s);
+    if (he != hipSuccess) return hip_fail(he, "range verify / emit launch");
+    hipEvent_t re = tm.mark(s);
+    tile_ev.emplace_back(ts, te);
+    rc_ev.emplace_back(te, re);
+  }
+  hipEvent_t e_end = tm.mark(s);
+  int64_t total = 0;
+  he = hipMemcpyAsync(&total, row_ptr_out + nq, sizeof(total), hipMemcpyDeviceToHost, s);
+  if (he == hipSuccess) he = hipMemcpyAsync(&host, a.ctrl, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
+  if (he != hipSuccess) return hip_fail(he, "status readback");
+  if (total_out) *total_out = total;
+  if (stats) {
+    stats->precision = p.precision;
+    stats->kprime = 0;
+    stats->ref_splits = p.splits;
+    stats->query_block = largest;
+    stats->blocks = (int64_t)batches.size();
+    stats->rows_certified = 0;
+    stats->rows_fallback = 0;
+    stats->tile_launches = 1 + (int64_t)batches.size();
+    stats->reordered = 0;
+    stats->ms_prep = Timers::ms(e0, e_prep);
+    float t = Timers::ms(e_prep, e_count), r = Timers::ms(e_count, e_scan);
+    for (auto& pr : tile_ev) t += Timers::ms(pr.first, pr.second);
+    for (auto& pr : rc_ev) r += Timers::ms(pr.first, pr.second);
+    stats->ms_tile = t;
+    stats->ms_recheck = r;
+    stats->ms_fallback = 0.0f;
+    stats->ms_score = 0.0f;
+    stats->ms_total = Timers::ms(e0, e_end);
+    stats->pairs_candidate = g[L.groups];
+    stats->pairs_uncertain = (int64_t)host.uncertain;
+    stats->pairs_in_range = total;
+  }
+  if (host.internal) return fail(TOD_ERR_INTERNAL, "range tile passes disagree");
+  if (idx_out && total > capacity)
+    return fail(TOD_ERR_CAPACITY, "pairs in range: " + std::to_string(total) + ", capacity " +
+                                      std::to_string(capacity));
   return TOD_OK;
 }
 
@@ -444,6 +700,27 @@ tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_op
              knn_score_out, lof_out, stats);
 }
 
+size_t tod_nwr_workspace_size(int64_t nq, int64_t nr, int64_t d, const tod_options* opts) {
+  tod_options o;
+  if (resolve_options(opts, &o) != TOD_OK) return 0;
+  if (nq <= 0 || nr <= 0 || d <= 0 || nq > kMaxRows || nr > kMaxRows) return 0;
+  Plan p;
+  const char* why;
+  // Sized for separate query and reference sets (enough for any call).
+  if (tod::make_plan_nwr(nq, nr, d, 0, o, &p, &why) != TOD_OK) return 0;
+  const tod::NwrLayout L = tod::make_layout_nwr(p);
+  const size_t room = (size_t)64 * p.nq_pad + ((size_t)1 << 20);
+  return L.cand + 512 + room * 8;
+}
+
+tod_status tod_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                   double phi, const tod_options* opts, void* workspace, size_t ws_bytes,
+                   void* stream, int64_t* row_ptr_out, int64_t capacity, int64_t* idx_out,
+                   float* dist_out, int64_t* total_out, tod_stats* stats) {
+  return run_nwr(xq, nq, xr, nr, d, phi, opts, workspace, ws_bytes, stream, row_ptr_out,
+                 capacity, idx_out, dist_out, total_out, stats);
+}
+
 tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,
                     tod_stats* plan) {
   g_last_error.clear();
@@ -477,6 +754,7 @@ const char* tod_status_string(tod_status s) {
     case TOD_ERR_UNSUPPORTED: return "TOD_ERR_UNSUPPORTED";
     case TOD_ERR_HIP: return "TOD_ERR_HIP";
     case TOD_ERR_INTERNAL: return "TOD_ERR_INTERNAL";
+    case TOD_ERR_CAPACITY: return "TOD_ERR_CAPACITY";
   }
   return "TOD_ERR_UNKNOWN";
 }

@@ -1,0 +1,227 @@
+// Neighbours within range (Section 5.3): exact verification of the filter's
+// uncertain pairs (Section 5.2 step iii, "recalculate only where the
+// verification fails") and assembly of the CSR output.
+//
+// After the fill pass (rtile.h) the candidate buffer holds, for each query
+// row of the batch, its candidates in increasing reference index; bit 31
+// marks the ones the filter could not rule in.
+//   verify  one wave per row: the uncertain candidates (and every candidate
+//           when distances are requested) get the exact squared distance,
+//           computed as in the definition: fp64, columns in order,
+//           ((double)x - (double)y)^2 added one at a time with no fused
+//           multiply-add, so the in-range decision D2 <= phi^2 is the same
+//           bit for bit as a plain fp64 evaluation.  Kept candidates get
+//           their distance (or 0), dropped ones -1; the row's count is stored.
+//   scan    row offsets = exclusive prefix sums of the counts (continuing
+//           from the previous batch's last offset).
+//   emit    one wave per row: kept candidates are compacted in order (ballot
+//           ranks) into idx_out / dist_out at the row's offset, within the
+//           caller's capacity.
+#include <math.h>
+
+#include "tod_internal.h"
+
+namespace tod {
+
+namespace {
+
+constexpr int kScanT = 256;
+constexpr int kScanPer = 16;
+constexpr int kScanChunk = kScanT * kScanPer;
+
+// Exact squared distance of two fp32 rows, as the definition states it.
+__device__ __forceinline__ double exact_d2(const float* __restrict__ q,
+                                           const float* __restrict__ r, int d) {
+#pragma clang fp contract(off)
+  double s = 0.0;
+  if ((d & 3) == 0) {
+    for (int t = 0; t < d; t += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(q + t);
+      const float4 y = *reinterpret_cast<const float4*>(r + t);
+      double e = (double)x.x - (double)y.x;
+      s = s + e * e;
+      e = (double)x.y - (double)y.y;
+      s = s + e * e;
+      e = (double)x.z - (double)y.z;
+      s = s + e * e;
+      e = (double)x.w - (double)y.w;
+      s = s + e * e;
+    }
+  } else {
+    for (int t = 0; t < d; ++t) {
+      const double e = (double)q[t] - (double)r[t];
+      s = s + e * e;
+    }
+  }
+  return s;
+}
+
+__global__ void __launch_bounds__(256)
+range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = b0 + (int64_t)blockIdx.x * 4 + wave;
+  if (row >= b0 + rows) return;  // uniform per wave
+  const int64_t beg = a.coff[row * a.splits] - a.cbase;
+  const int64_t end = a.coff[(row + 1) * a.splits] - a.cbase;
+  const float* qrow = a.xq + row * (int64_t)a.d;
+  const double phi2 = a.phi * a.phi;
+  int kept = 0, unc = 0;
+  for (int64_t p0 = beg; p0 < end; p0 += 64) {
+    const int64_t p = p0 + lane;
+    const bool live = p < end;
+    const uint32_t c = live ? a.cand[p] : 0u;
+    const bool u = live && (c >> 31);
+    const bool need = live && (u || want_dist);
+    double d2 = 0.0;
+    if (need) d2 = exact_d2(qrow, a.xr + (int64_t)(c & 0x7fffffffu) * a.d, a.d);
+    const bool keep = live && (!u || d2 <= phi2);
+    if (live) a.cand_d[p] = keep ? (need ? (float)sqrt(d2) : 0.0f) : -1.0f;
+    kept += __popcll(__ballot(keep));
+    unc += __popcll(__ballot(u));
+  }
+  if (lane == 0) {
+    a.incnt[row] = kept;
+    if (unc) atomicAdd((unsigned long long*)&a.ctrl->uncertain, (unsigned long long)unc);
+  }
+}
+
+__global__ void __launch_bounds__(256)
+range_emit_kernel(Args a, int64_t b0, int64_t rows) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = b0 + (int64_t)blockIdx.x * 4 + wave;
+  if (row >= b0 + rows) return;  // uniform per wave
+  const int64_t beg = a.coff[row * a.splits] - a.cbase;
+  const int64_t end = a.coff[(row + 1) * a.splits] - a.cbase;
+  int64_t out = a.row_ptr[row];
+  const uint64_t below = (1ull << lane) - 1ull;
+  for (int64_t p0 = beg; p0 < end; p0 += 64) {
+    const int64_t p = p0 + lane;
+    const bool live = p < end;
+    const float dd = live ? a.cand_d[p] : -1.0f;
+    const bool keep = dd >= 0.0f;
+    const uint64_t m = __ballot(keep);
+    const int64_t pos = out + __popcll(m & below);
+    if (keep && pos < a.out_cap) {
+      a.idx_out[pos] = (int64_t)(a.cand[p] & 0x7fffffffu);
+      if (a.dist_out) a.dist_out[pos] = dd;
+    }
+    out += __popcll(m);
+  }
+}
+
+// Block sums of kScanChunk-element chunks.
+__global__ void __launch_bounds__(kScanT)
+scan_sum_kernel(const int32_t* __restrict__ in, int64_t n, int64_t* __restrict__ part) {
+  __shared__ int64_t red[kScanT / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk;
+  int64_t s = 0;
+  for (int i = threadIdx.x; i < kScanChunk; i += kScanT) {
+    const int64_t k = base + i;
+    if (k < n) s += in[k];
+  }
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t t = 0;
+    for (int w = 0; w < kScanT / 64; ++w) t += red[w];
+    part[blockIdx.x] = t;
+  }
+}
+
+// Exclusive scan of the np block sums in place (one workgroup), plus *base.
+__global__ void __launch_bounds__(kScanT)
+scan_top_kernel(int64_t* __restrict__ part, int64_t np, const int64_t* __restrict__ base) {
+  __shared__ int64_t sh[kScanT];
+  int64_t carry = base ? *base : 0;
+  for (int64_t c0 = 0; c0 < np; c0 += kScanT) {
+    const int64_t k = c0 + threadIdx.x;
+    const int64_t v = k < np ? part[k] : 0;
+    sh[threadIdx.x] = v;
+    __syncthreads();
+    for (int o = 1; o < kScanT; o <<= 1) {
+      const int64_t t = threadIdx.x >= o ? sh[threadIdx.x - o] : 0;
+      __syncthreads();
+      sh[threadIdx.x] += t;
+      __syncthreads();
+    }
+    if (k < np) part[k] = carry + sh[threadIdx.x] - v;
+    carry += sh[kScanT - 1];
+    __syncthreads();
+  }
+}
+
+// out[i] = part[block] + prefix of the block's chunk up to i; out[n] = total.
+__global__ void __launch_bounds__(kScanT)
+scan_final_kernel(const int32_t* __restrict__ in, int64_t n, const int64_t* __restrict__ part,
+                  int64_t* __restrict__ out) {
+  __shared__ int64_t sh[kScanT];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanPer;
+  int32_t v[kScanPer];
+  int64_t s = 0;
+#pragma unroll
+  for (int i = 0; i < kScanPer; ++i) {
+    v[i] = base + i < n ? in[base + i] : 0;
+    s += v[i];
+  }
+  sh[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 1; o < kScanT; o <<= 1) {
+    const int64_t t = threadIdx.x >= o ? sh[threadIdx.x - o] : 0;
+    __syncthreads();
+    sh[threadIdx.x] += t;
+    __syncthreads();
+  }
+  int64_t acc = part[blockIdx.x] + sh[threadIdx.x] - s;
+#pragma unroll
+  for (int i = 0; i < kScanPer; ++i) {
+    if (base + i < n) out[base + i] = acc;
+    acc += v[i];
+    if (base + i == n - 1) out[n] = acc;
+  }
+}
+
+__global__ void group_offsets_kernel(const int64_t* __restrict__ coff, int64_t nq, int32_t splits,
+                                     int64_t groups, int64_t* __restrict__ goff) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g > groups) return;
+  const int64_t row = 32 * g < nq ? 32 * g : nq;
+  goff[g] = coff[row * splits];
+}
+
+unsigned blocks_for_rows(int64_t rows) { return (unsigned)((rows + 3) / 4); }
+
+}  // namespace
+
+int64_t scan_parts(int64_t n) { return (n + kScanChunk - 1) / kScanChunk; }
+
+hipError_t launch_scan(const int32_t* in, int64_t n, int64_t* out, const int64_t* base,
+                       int64_t* part, hipStream_t s) {
+  const int64_t np = scan_parts(n);
+  hipLaunchKernelGGL(scan_sum_kernel, dim3((unsigned)np), dim3(kScanT), 0, s, in, n, part);
+  hipLaunchKernelGGL(scan_top_kernel, dim3(1), dim3(kScanT), 0, s, part, np, base);
+  hipLaunchKernelGGL(scan_final_kernel, dim3((unsigned)np), dim3(kScanT), 0, s, in, n,
+                     (const int64_t*)part, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_offsets(const Args& a, int64_t groups, int64_t* goff, hipStream_t s) {
+  hipLaunchKernelGGL(group_offsets_kernel, dim3((unsigned)((groups + 1 + 255) / 256)), dim3(256),
+                     0, s, (const int64_t*)a.coff, a.nq, a.splits, groups, goff);
+  return hipGetLastError();
+}
+
+hipError_t launch_range_verify(const Args& a, int64_t b0, int64_t rows, int32_t want_dist,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(range_verify_kernel, dim3(blocks_for_rows(rows)), dim3(256), 0, s, a, b0,
+                     rows, want_dist);
+  return hipGetLastError();
+}
+
+hipError_t launch_range_emit(const Args& a, int64_t b0, int64_t rows, hipStream_t s) {
+  hipLaunchKernelGGL(range_emit_kernel, dim3(blocks_for_rows(rows)), dim3(256), 0, s, a, b0,
+                     rows);
+  return hipGetLastError();
+}
+
+}  // namespace tod

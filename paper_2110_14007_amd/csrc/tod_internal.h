@@ -52,10 +52,11 @@ struct Ctrl {
   uint64_t nmax_bits;       // max ||xhat_j||^2 over references, fp64 bits
   uint64_t pmax_bits;       // max rho_j over references, fp64 bits
   uint32_t worklist_count;  // rows appended for exact recomputation
-  uint32_t pad0;
+  uint32_t internal;        // set when a kernel finds an inconsistency it cannot recover from
   uint64_t certified;       // rows certified by the shortlist test
   uint64_t fold_max_bits;   // max over references of the folded seed's error, fp64 bits
-  uint64_t pad[3];
+  uint64_t uncertain;       // NWR: candidate pairs recomputed exactly
+  uint64_t pad[2];
 };
 
 // Everything a kernel needs to know about the problem.
@@ -100,6 +101,17 @@ struct Args {
   float* dist_out;
   float* score_out;
   float* lof_out;
+  // neighbours within range (rtile.h, nwr.hip)
+  double phi;          // the range threshold (a distance)
+  int32_t* ccount;     // count pass: candidates per (query, split) [nq_pad x S]
+  int64_t* coff;       // their exclusive prefix sums [nq x S + 1]
+  int64_t cbase;       // candidate offset of the first row of the current query batch
+  uint32_t* cand;      // candidate reference ids of the batch; bit 31: not ruled in by the filter
+  float* cand_d;       // after verification: distance if kept (0 if not measured), -1 if not
+  int64_t ccap;        // candidate room
+  int32_t* incnt;      // pairs in range per query row [nq]
+  int64_t* row_ptr;    // CSR offsets [nq + 1] (the caller's output)
+  int64_t out_cap;     // entries idx_out / dist_out can hold
 };
 
 // Power-of-two scale s with s * maxabs < 2^E (exact scaling of the centred
@@ -152,9 +164,39 @@ hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t s);
 
+// Neighbours within range: fused MFMA tile with the range test (count pass:
+// candidates per (query, split); fill pass: their ids, in increasing j per
+// row), exact verification, CSR assembly.
+hipError_t launch_range_tile_f16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                                 bool fill, hipStream_t s);
+hipError_t launch_range_tile_bf16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
+                                  bool fill, hipStream_t s);
+// Exclusive prefix sums of n int32 values into out[0..n] (out[n] = total),
+// plus *base when base is not null.  part holds scan_parts(n) int64.
+int64_t scan_parts(int64_t n);
+hipError_t launch_scan(const int32_t* in, int64_t n, int64_t* out, const int64_t* base,
+                       int64_t* part, hipStream_t s);
+// goff[g] = coff[min(32 g, nq) * S] for g = 0..groups.
+hipError_t launch_group_offsets(const Args& a, int64_t groups, int64_t* goff, hipStream_t s);
+hipError_t launch_range_verify(const Args& a, int64_t b0, int64_t rows, int32_t want_dist,
+                               hipStream_t s);
+hipError_t launch_range_emit(const Args& a, int64_t b0, int64_t rows, hipStream_t s);
+
 // Planner and layout (host only, no HIP calls).
 tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, int32_t self,
                      const tod_options& o, Plan* plan, const char** why);
 Layout make_layout(const Plan& p);
+tod_status make_plan_nwr(int64_t nq, int64_t nr, int64_t d, int32_t self, const tod_options& o,
+                         Plan* plan, const char** why);
+// NWR workspace regions; cand is the first byte of the candidate room.
+struct NwrLayout {
+  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, ccount, coff, part, goff,
+      incnt, cand;
+  int64_t groups;  // 32-row query groups
+  int32_t colpart_blocks;
+};
+NwrLayout make_layout_nwr(const Plan& p);
+// Candidate pairs a workspace of ws_bytes holds (0 if it is smaller than the fixed part).
+int64_t nwr_candidate_room(const NwrLayout& L, size_t ws_bytes);
 
 }  // namespace tod

@@ -21,13 +21,15 @@ TOD_ERR_WORKSPACE = 3
 TOD_ERR_UNSUPPORTED = 4
 TOD_ERR_HIP = 5
 TOD_ERR_INTERNAL = 6
+TOD_ERR_CAPACITY = 7
 
 PREC_AUTO, PREC_FP32, PREC_FP16, PREC_BF16 = 0, 1, 2, 3
 PRECISIONS = {"auto": PREC_AUTO, "fp32": PREC_FP32, "fp16": PREC_FP16, "bf16": PREC_BF16}
 PRECISION_NAMES = {v: k for k, v in PRECISIONS.items()}
 
 SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
-           "tod_plan", "tod_status_string", "tod_last_error")
+           "tod_nwr_workspace_size", "tod_nwr", "tod_plan", "tod_status_string",
+           "tod_last_error")
 
 
 class tod_options(ctypes.Structure):
@@ -63,6 +65,9 @@ class tod_stats(ctypes.Structure):
         ("ms_score", ctypes.c_float),
         ("ms_total", ctypes.c_float),
         ("reordered", ctypes.c_int32),
+        ("pairs_candidate", ctypes.c_int64),
+        ("pairs_uncertain", ctypes.c_int64),
+        ("pairs_in_range", ctypes.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -95,6 +100,11 @@ def _load():
     lib.tod_knn_score.restype = ctypes.c_int
     lib.tod_lof.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, vp, st_p]
     lib.tod_lof.restype = ctypes.c_int
+    lib.tod_nwr_workspace_size.argtypes = [i64, i64, i64, opt_p]
+    lib.tod_nwr_workspace_size.restype = sz
+    lib.tod_nwr.argtypes = [vp, i64, vp, i64, i64, ctypes.c_double, opt_p, vp, sz, vp, vp, i64, vp,
+                            vp, ctypes.POINTER(i64), st_p]
+    lib.tod_nwr.restype = ctypes.c_int
     lib.tod_plan.argtypes = [i64, i64, i64, i32, opt_p, st_p]
     lib.tod_plan.restype = ctypes.c_int
     lib.tod_status_string.argtypes = [ctypes.c_int]
@@ -190,10 +200,16 @@ class Workspace:
 
 
 def _ws(workspace, nbytes, device):
+    """(buffer, pointer, size) of a workspace of at least nbytes.
+
+    The caller must hold the returned buffer until the library call returns:
+    a temporary workspace would otherwise go back to torch's caching
+    allocator, which may hand the same memory to the next output tensor.
+    """
     if workspace is None:
         workspace = Workspace()
     buf = workspace.get(nbytes, device)
-    return ctypes.c_void_p(buf.data_ptr()), ctypes.c_size_t(buf.numel())
+    return buf, ctypes.c_void_p(buf.data_ptr()), ctypes.c_size_t(buf.numel())
 
 
 def _stream(stream):
@@ -218,7 +234,7 @@ def tod_knn(xq, xr, k: int, opts=None, workspace=None, stream=None, stats=None):
     idx = torch.empty((nq, k), dtype=torch.int64, device=xq.device)
     dist = torch.empty((nq, k), dtype=torch.float32, device=xq.device)
     need = tod_workspace_size(nq, nr, d, k, False, opts)
-    wsp, wsn = _ws(workspace, need, xq.device)
+    wsbuf, wsp, wsn = _ws(workspace, need, xq.device)
     st = _lib.tod_knn(_p(xq), nq, _p(xr), nr, d, int(k),
                       ctypes.byref(opts) if opts is not None else None, wsp, wsn,
                       _stream(stream), _p(idx), _p(dist),
@@ -239,7 +255,7 @@ def tod_knn_score(x, k: int, opts=None, workspace=None, stream=None, stats=None,
         idx = torch.empty((n, k), dtype=torch.int64, device=x.device)
         dist = torch.empty((n, k), dtype=torch.float32, device=x.device)
     need = tod_workspace_size(n, n, d, k, False, opts)
-    wsp, wsn = _ws(workspace, need, x.device)
+    wsbuf, wsp, wsn = _ws(workspace, need, x.device)
     st = _lib.tod_knn_score(_p(x), n, d, int(k), ctypes.byref(opts) if opts is not None else None,
                             wsp, wsn, _stream(stream), _p(score), _p(idx), _p(dist),
                             ctypes.byref(stats) if stats is not None else None)
@@ -263,12 +279,62 @@ def tod_lof(x, k: int, opts=None, workspace=None, stream=None, stats=None,
         idx = torch.empty((n, k), dtype=torch.int64, device=x.device)
         dist = torch.empty((n, k), dtype=torch.float32, device=x.device)
     need = tod_workspace_size(n, n, d, k, True, opts)
-    wsp, wsn = _ws(workspace, need, x.device)
+    wsbuf, wsp, wsn = _ws(workspace, need, x.device)
     st = _lib.tod_lof(_p(x), n, d, int(k), ctypes.byref(opts) if opts is not None else None,
                       wsp, wsn, _stream(stream), _p(lof), _p(score), _p(idx), _p(dist),
                       ctypes.byref(stats) if stats is not None else None)
     _check(st, "tod_lof")
     return (lof, score, idx, dist) if return_lists else (lof, score)
+
+
+def tod_nwr_workspace_size(nq: int, nr: int, d: int, opts=None) -> int:
+    return int(_lib.tod_nwr_workspace_size(int(nq), int(nr), int(d),
+                                           ctypes.byref(opts) if opts is not None else None))
+
+
+def tod_nwr(xq, xr, phi: float, opts=None, workspace=None, stream=None, stats=None,
+            capacity=None, with_dist: bool = True, count_only: bool = False,
+            workspace_bytes=None):
+    """Neighbours within range phi -> (row_ptr int64 [nq+1], idx int64 [total], dist fp32 [total]).
+
+    With count_only, only row_ptr is computed (idx and dist are None).  The
+    outputs are allocated with ``capacity`` entries (default 64 per query
+    row); if the pairs in range do not fit, they are reallocated to the
+    total the library reports and the call is made once more.
+    ``workspace_bytes`` overrides the workspace size (candidate room).
+    """
+    torch = _torch()
+    _dev_matrix(xq, "xq")
+    _dev_matrix(xr, "xr")
+    nq, d = xq.shape
+    nr = xr.shape[0]
+    if xr.shape[1] != d:
+        raise ValueError("xq and xr must have the same number of columns")
+    need = int(workspace_bytes) if workspace_bytes is not None else \
+        tod_nwr_workspace_size(nq, nr, d, opts)
+    wsbuf, wsp, wsn = _ws(workspace, need, xq.device)
+    row_ptr = torch.empty((nq + 1,), dtype=torch.int64, device=xq.device)
+    total = ctypes.c_int64(0)
+    optp = ctypes.byref(opts) if opts is not None else None
+    stp = ctypes.byref(stats) if stats is not None else None
+    if count_only:
+        st = _lib.tod_nwr(_p(xq), nq, _p(xr), nr, d, float(phi), optp, wsp, wsn, _stream(stream),
+                          _p(row_ptr), 0, None, None, ctypes.byref(total), stp)
+        _check(st, "tod_nwr")
+        return row_ptr, None, None
+    cap = 64 * nq if capacity is None else int(capacity)
+    for _ in range(2):
+        idx = torch.empty((max(cap, 1),), dtype=torch.int64, device=xq.device)
+        dist = torch.empty((max(cap, 1),), dtype=torch.float32, device=xq.device) \
+            if with_dist else None
+        st = _lib.tod_nwr(_p(xq), nq, _p(xr), nr, d, float(phi), optp, wsp, wsn, _stream(stream),
+                          _p(row_ptr), cap, _p(idx), _p(dist), ctypes.byref(total), stp)
+        if st != TOD_ERR_CAPACITY:
+            break
+        cap = int(total.value)
+    _check(st, "tod_nwr")
+    n = int(total.value)
+    return row_ptr, idx[:n], (dist[:n] if dist is not None else None)
 
 
 def raw_library():

@@ -22,6 +22,15 @@ the same generator.  Labels: 1 = outlier.
                              (32 x 512), + 0.1*N(0, I) noise; 1,000 outliers N(0, I_512)
                                                                               (kNN, bf16 filter)
   C5  n=4,000,000 d=8  k=5   3,996,000 U[0,1]^8 + 4,000 U[1.5, 3]^8           (kNN)
+  N1  n=30,000   d=200 phi=18  10 unit-variance Gaussian clusters (means 5*N(0,I),
+                             2,970 points each) + 300 outliers 10*N(0, I);
+                             phi = 0.9 sqrt(2d), 90 % of the typical distance
+                             between two points of one cluster             (neighbours within range)
+
+N1 stands in for the paper's 30,000-sample synthetic set of its NWR runtime
+breakdown (Table 5); the paper states neither its dimension nor its
+threshold, so d follows the paper's other synthetic sets (200 features) and
+phi is set relative to the cluster scale.
 """
 from __future__ import annotations
 
@@ -57,6 +66,9 @@ WORKLOADS = {
                    "full-rank outliers, bf16 filter"),
     "C5": Workload("C5", 4_000_000, 8, 5, 5, "fp32", False, 0,
                    "kNN-OD, n=4000000 d=8 k=5: U[0,1]^8 + 0.1% U[1.5,3]^8 outliers"),
+    "N1": Workload("N1", 30_000, 200, 0, 6, "fp16", False, 0,
+                   "NWR, n=30000 d=200 phi=18: 10-cluster Gaussian mixture + 1% N(0,100I) "
+                   "outliers, fp16 filter", {"phi": 18.0}),
 }
 
 
@@ -93,7 +105,7 @@ def generate(name: str, n: int | None = None):
         lo, hi = inl.min(axis=0), inl.max(axis=0)
         pad = 0.1 * (hi - lo)
         out = rng.uniform(lo - pad, hi + pad, (n_out, d))
-    elif name == "C3":
+    elif name in ("C3", "N1"):
         n_out = max(1, n // 100)
         n_in = n - n_out
         means = 5.0 * rng.standard_normal((10, d))
@@ -121,7 +133,7 @@ def sample_rows(name: str, n: int | None = None, count: int = 2048) -> np.ndarra
     """Seeded query-row sample used to check large workloads row by row."""
     w = WORKLOADS[name]
     n = w.n if n is None else int(n)
-    rng = np.random.default_rng(1000 + int(name[1:]))
+    rng = np.random.default_rng((1000 if name[0] == "C" else 2000) + int(name[1:]))
     return np.sort(rng.choice(n, size=min(count, n), replace=False)).astype(np.int64)
 
 

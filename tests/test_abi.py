@@ -117,3 +117,48 @@ def test_score_and_lof_entry_points_validate(tod):
                        None) == 1
     assert lib.tod_lof(FAKE, 100, 8, 5, None, FAKE, 100, None, FAKE, None, None, None,
                        None) == tod.TOD_ERR_WORKSPACE
+
+
+def _nwr(tod, nq=100, nr=100, d=8, phi=1.0, opts=None, ws=FAKE, ws_bytes=1 << 30, xq=FAKE,
+         xr=FAKE, row_ptr=FAKE, cap=10, idx=FAKE, dist=FAKE):
+    lib = tod.raw_library()
+    total = ctypes.c_int64(-1)
+    st = lib.tod_nwr(xq, nq, xr, nr, d, phi, ctypes.byref(opts) if opts else None, ws, ws_bytes,
+                     None, row_ptr, cap, idx, dist, ctypes.byref(total), None)
+    assert total.value == -1  # untouched on an argument error
+    return st
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(nq=0), 1), (dict(nr=-1), 1), (dict(d=0), 1), (dict(phi=-1.0), 1),
+    (dict(phi=float("nan")), 1), (dict(phi=float("inf")), 1), (dict(cap=-1), 1),
+    (dict(idx=None), 1),  # dist without idx
+    (dict(row_ptr=None), 1), (dict(xr=None), 1), (dict(ws=None), 1),
+    (dict(d=513), 4), (dict(nq=1 << 31), 4),
+    (dict(ws=ctypes.c_void_p(0x100010)), 3), (dict(ws_bytes=4096), 3),
+    (dict(xq=ctypes.c_void_p(0x100004)), 1),
+])
+def test_nwr_invalid_arguments_rejected(tod, kw, status):
+    assert _nwr(tod, **kw) == status
+    assert tod.last_error() != ""
+
+
+def test_nwr_options(tod):
+    assert _nwr(tod, opts=tod.options(precision="fp32")) == tod.TOD_ERR_UNSUPPORTED
+    assert _nwr(tod, opts=tod.options(exclude_self=True), xr=ctypes.c_void_p(0x200000)) == \
+        tod.TOD_ERR_INVALID_ARG
+    o = tod.options()
+    o.margin_scale = 0.5
+    assert _nwr(tod, opts=o) == tod.TOD_ERR_INVALID_ARG
+
+
+def test_nwr_workspace_size(tod):
+    small = tod.tod_nwr_workspace_size(1000, 1000, 16)
+    big = tod.tod_nwr_workspace_size(100000, 1000, 16)
+    assert 0 < small < big
+    # room for 64 candidates per padded query row and 2^20 more, 8 bytes each
+    assert big - small >= (100000 - 1024) * 64 * 8
+    assert tod.tod_nwr_workspace_size(1000, 1000, 600) == 0
+    assert tod.tod_nwr_workspace_size(0, 1000, 16) == 0
+    assert tod.tod_nwr_workspace_size(10, 10, 16, tod.options(precision="fp32")) == 0
+    assert tod.status_string(tod.TOD_ERR_CAPACITY) == "TOD_ERR_CAPACITY"
