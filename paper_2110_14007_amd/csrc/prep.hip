@@ -25,6 +25,7 @@ namespace tod {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kFinalCols = 32;  // columns per block of the column-mean final sum
 
 __global__ void init_ctrl_kernel(Ctrl* ctrl) {
   uint32_t* w = reinterpret_cast<uint32_t*>(ctrl);
@@ -66,8 +67,8 @@ __global__ void __launch_bounds__(kThreads)
 colsum_final_kernel(const double* __restrict__ part, int nb, int d, int64_t n,
                     double* __restrict__ mu64, float* __restrict__ mu32) {
   __shared__ double red[kThreads];
-  const int cpb = d < kThreads ? d : kThreads;  // columns per block
-  const int tpc = kThreads / cpb;               // threads per column
+  const int cpb = d < kFinalCols ? d : kFinalCols;  // columns per block
+  const int tpc = kThreads / cpb;                   // threads per column
   const int tid = threadIdx.x, cl = tid % cpb, sub = tid / cpb;
   const int c = blockIdx.x * cpb + cl;
   double t = 0.0;
@@ -154,6 +155,22 @@ __device__ __forceinline__ double wave_max(double v) {
   return v;
 }
 
+// Largest value over the workgroup of kThreads threads, for every thread
+// (every lane of a wave may hold its own value).  All threads must call it.
+__device__ __forceinline__ double block_max(double v, double* red) {
+  v = wave_max(v);
+  __syncthreads();  // red may still be in use by a previous call
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double m = red[0];
+  for (int w = 1; w < kThreads / 64; ++w) m = red[w] > m ? red[w] : m;
+  return m;
+}
+
+__device__ __forceinline__ void atomic_max_nonneg(uint64_t* addr, double v) {
+  atomicMax((unsigned long long*)addr, (unsigned long long)__double_as_longlong(v));
+}
+
 // One thread per row.  Rows in [n, n_pad) are zero-filled so that the tile
 // kernels may read whole 32-row tiles.  The reference maxima are reduced over
 // the wave first: one atomic per wave instead of two per row.
@@ -217,13 +234,14 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
       if (rho) rho[row] = rho_up;
     }
   }
-  if (is_ref) {
-    const double wn = wave_max(nsq), wp = wave_max(rho_up), wf = wave_max(ferr);
-    if ((threadIdx.x & 63) == 0) {
-      atomicMax((unsigned long long*)&ctrl->nmax_bits, (unsigned long long)__double_as_longlong(wn));
-      atomicMax((unsigned long long*)&ctrl->pmax_bits, (unsigned long long)__double_as_longlong(wp));
-      atomicMax((unsigned long long*)&ctrl->fold_max_bits,
-                (unsigned long long)__double_as_longlong(wf));
+  if (is_ref) {  // uniform: one atomic per maximum per workgroup
+    __shared__ double red[kThreads / 64];
+    const double bn = block_max(nsq, red), bp = block_max(rho_up, red);
+    const double bf = block_max(ferr, red);
+    if (threadIdx.x == 0) {
+      atomic_max_nonneg(&ctrl->nmax_bits, bn);
+      atomic_max_nonneg(&ctrl->pmax_bits, bp);
+      atomic_max_nonneg(&ctrl->fold_max_bits, bf);
     }
   }
 }
@@ -295,18 +313,23 @@ quantise_rows_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int 
     wn = nsq > wn ? nsq : wn;
     wp = rho_up > wp ? rho_up : wp;
   }
-  if (is_ref && lane == 0) {
-    atomicMax((unsigned long long*)&ctrl->nmax_bits, (unsigned long long)__double_as_longlong(wn));
-    atomicMax((unsigned long long*)&ctrl->pmax_bits, (unsigned long long)__double_as_longlong(wp));
+  if (is_ref) {  // uniform: one atomic per maximum per workgroup
+    __shared__ double red[kThreads / 64];
+    const double bn = block_max(wn, red), bp = block_max(wp, red);
+    if (threadIdx.x == 0) {
+      atomic_max_nonneg(&ctrl->nmax_bits, bn);
+      atomic_max_nonneg(&ctrl->pmax_bits, bp);
+    }
   }
 }
 
 template <typename T>
 hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
   if (!p.fold && p.d >= 64) {
+    // 4 waves per block; at most 1024 blocks (one atomic per maximum each).
     const auto grid_rows = [](int64_t rows) {
-      int64_t g = (rows + 3) / 4;  // 4 waves per block
-      return (unsigned)(g < 1 ? 1 : (g > 4096 ? 4096 : g));
+      int64_t g = (rows + 3) / 4;
+      return (unsigned)(g < 1 ? 1 : (g > 1024 ? 1024 : g));
     };
     hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nr_pad)), dim3(kThreads), 0, st,
                        a.xr, p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r,
@@ -338,9 +361,11 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
 
 }  // namespace
 
+// About 1024 blocks of consecutive rows for the column partial sums (enough
+// to fill the GPU when n is small and d large, few enough partials per
+// column for the final sum).
 int32_t colsum_blocks(int64_t nr) {
-  int64_t rpb = nr / 1024 + 1;
-  if (rpb < 512) rpb = 512;
+  const int64_t rpb = (nr + 1023) / 1024;
   return (int32_t)((nr + rpb - 1) / rpb);
 }
 
@@ -352,12 +377,14 @@ hipError_t launch_prep(const Plan& p, const Args& a, hipStream_t st) {
   const int64_t rpb = (p.nr + nb - 1) / nb;
   hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(kThreads), 0, st, a.xr, p.nr,
                      (int)p.d, rpb, a.colpart);
-  const int cpb = p.d < kThreads ? (int)p.d : kThreads;
+  const int cpb = p.d < kFinalCols ? (int)p.d : kFinalCols;
   hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)((p.d + cpb - 1) / cpb)),
                      dim3(kThreads), 0, st, a.colpart, nb, (int)p.d, p.nr, a.mu64, a.mu32);
+  // At most 1024 blocks: each ends with one atomic on the same word, and
+  // same-address atomics serialise.
   const auto grid_for = [](int64_t total) {
     int64_t g = (total + kThreads * 4 - 1) / (kThreads * 4);
-    return (unsigned)(g < 1 ? 1 : (g > 4096 ? 4096 : g));
+    return (unsigned)(g < 1 ? 1 : (g > 1024 ? 1024 : g));
   };
   hipLaunchKernelGGL(maxabs_kernel, dim3(grid_for(p.nr * p.d)), dim3(kThreads), 0, st, a.xr,
                      p.nr, (int)p.d, a.mu32, a.ctrl);

@@ -139,33 +139,36 @@ range_tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     }
   }
 
+  // Staging: every thread moves up to NL 16-byte chunks of a stage (rows past
+  // the split's padded end are clamped to its last row: loaded, never read).
+  // The staging registers start zeroed: left undefined, the compiler keeps
+  // them as a stack object in scratch memory.
   const unsigned char* xr_bytes = (const unsigned char*)a.xq_r;
   uint4 st[NL];
+#pragma unroll
+  for (int i = 0; i < NL; ++i) st[i] = make_uint4(0, 0, 0, 0);
   float4 sth = make_float4(0.f, 0.f, 0.f, 0.f);
-  auto fetch = [&](int64_t t0) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int c = tid + i * NT;
-      if (CHUNKS % NT == 0 || c < CHUNKS) {
-        const int row = c / CPR, cc = c % CPR;
-        const int64_t gr = t0 + row < r_end32 ? t0 + row : r_end32 - 1;
-        st[i] = *reinterpret_cast<const uint4*>(xr_bytes + gr * (int64_t)(DPAD * 2) + cc * 16);
-      }
-    }
-    if (tid < TR / 4) {
-      const int64_t gr = t0 + 4 * tid < r_end32 ? t0 + 4 * tid : r_end32 - 4;
-      sth = *reinterpret_cast<const float4*>(a.hn_r + gr);
-    }
-  };
-  auto put = [&](int b) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int c = tid + i * NT;
-      if (CHUNKS % NT == 0 || c < CHUNKS)
-        *reinterpret_cast<uint4*>(stage + b * STAGE + (c / CPR) * ROWB + (c % CPR) * 16) = st[i];
-    }
-    if (tid < TR / 4) *reinterpret_cast<float4*>(hnb + b * TR + 4 * tid) = sth;
-  };
+#define TOD_RT_FETCH(T0)                                                                     \
+  _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
+    const int c = tid + i * NT;                                                             \
+    if (CHUNKS % NT == 0 || c < CHUNKS) {                                                   \
+      const int row = c / CPR, cc = c % CPR;                                                \
+      const int64_t gr = (T0) + row < r_end32 ? (T0) + row : r_end32 - 1;                   \
+      st[i] = *reinterpret_cast<const uint4*>(xr_bytes + gr * (int64_t)(DPAD * 2) + cc * 16); \
+    }                                                                                       \
+  }                                                                                         \
+  if (tid < TR / 4) {                                                                       \
+    const int64_t gr = (T0) + 4 * tid < r_end32 ? (T0) + 4 * tid : r_end32 - 4;             \
+    sth = *reinterpret_cast<const float4*>(a.hn_r + gr);                                    \
+  }
+#define TOD_RT_PUT(B)                                                                        \
+  _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
+    const int c = tid + i * NT;                                                             \
+    if (CHUNKS % NT == 0 || c < CHUNKS)                                                     \
+      *reinterpret_cast<uint4*>(stage + (B) * STAGE + (c / CPR) * ROWB + (c % CPR) * 16) =    \
+          st[i];                                                                            \
+  }                                                                                         \
+  if (tid < TR / 4) *reinterpret_cast<float4*>(hnb + (B) * TR + 4 * tid) = sth;
 
   auto body = [&](int64_t t0, int b) __attribute__((always_inline)) {
     if (!active) return;
@@ -241,15 +244,17 @@ range_tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 
   const int nst = (int)((r_end - r_begin + TR - 1) / TR);
   auto t_of = [&](int i) -> int64_t { return r_begin + (int64_t)(i < nst ? i : 0) * TR; };
-  fetch(t_of(0));
-  put(0);
+  TOD_RT_FETCH(t_of(0))
+  TOD_RT_PUT(0)
   __syncthreads();
   for (int it = 0; it < nst; ++it) {
-    fetch(t_of(it + 1));  // the stage after the last is a reload of the first, never read
+    TOD_RT_FETCH(t_of(it + 1))  // the stage after the last is a reload of the first, never read
     body(t_of(it), it & 1);
-    put((it + 1) & 1);
+    TOD_RT_PUT((it + 1) & 1)
     __syncthreads();
   }
+#undef TOD_RT_FETCH
+#undef TOD_RT_PUT
   if constexpr (!FILL) {
     const int tot = run + (int)mt::xchg32((uint32_t)run, h);
     if (qvalid && h == 0) a.ccount[q * a.splits + split] = tot;
