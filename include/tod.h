@@ -99,7 +99,7 @@ typedef struct {
   float ms_prep, ms_tile, ms_recheck, ms_fallback, ms_score, ms_total;
   int32_t reordered;      /* 1 if the scan used the grouped row order (see tod_options.reorder) */
   int64_t pairs_candidate; /* tod_nwr: pairs the filter could not rule out of range */
-  int64_t pairs_uncertain; /* tod_nwr: candidates the filter could not rule in either (recomputed) */
+  int64_t pairs_uncertain; /* tod_nwr: candidates whose range test needed the exact distance */
   int64_t pairs_in_range;  /* tod_nwr: pairs within the threshold */
 } tod_stats;
 

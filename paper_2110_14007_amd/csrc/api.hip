@@ -292,6 +292,7 @@ NwrLayout make_layout_nwr(const Plan& p) {
   L.hn_r = take(sizeof(float) * p.nr_pad);
   L.n64_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
   L.rho_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
+  L.rho_r = p.self ? L.rho_q : take(sizeof(double) * p.nr_pad);
   L.ccount = take(sizeof(int32_t) * p.nq_pad * p.splits);
   L.coff = take(sizeof(int64_t) * (nc + 1));
   const int64_t parts = scan_parts(nc > p.nq ? nc : p.nq);
@@ -538,6 +539,7 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
   a.hn_r = (float*)(base + L.hn_r);
   a.n64_q = (double*)(base + L.n64_q);
   a.rho_q = (double*)(base + L.rho_q);
+  a.rho_r = (double*)(base + L.rho_r);
   a.phi = phi;
   a.ccount = (int32_t*)(base + L.ccount);
   a.coff = (int64_t*)(base + L.coff);

@@ -5,9 +5,11 @@
 // After the fill pass (rtile.h) the candidate buffer holds, for each query
 // row of the batch, its candidates in increasing reference index; bit 31
 // marks the ones the filter could not rule in.
-//   verify  one wave per row: the uncertain candidates (and every candidate
-//           when distances are requested) get the exact squared distance,
-//           computed as in the definition: fp64, columns in order,
+//   verify  one wave per row.  An uncertain candidate first gets the
+//           tile's test again with its own reference norm and radius in
+//           place of the maxima (pair_test); the ones still undecided (and
+//           every kept candidate when distances are requested) get the exact
+//           squared distance, computed as in the definition: fp64, columns in order,
 //           ((double)x - (double)y)^2 added one at a time with no fused
 //           multiply-add, so the in-range decision D2 <= phi^2 is the same
 //           bit for bit as a plain fp64 evaluation.  Kept candidates get
@@ -56,6 +58,29 @@ __device__ __forceinline__ double exact_d2(const float* __restrict__ q,
   return s;
 }
 
+// Range test of one pair with the pair's own reference norm and radius
+// (the tile's per-row thresholds use the reference maxima): +1 in range for
+// certain, -1 out of range for certain, 0 undecided.  acc is the pair's fp32
+// accumulator from the fill pass, t = -2 acc its key; the bounds are the
+// tile's (rtile.h) with N_j <= -2 hn_r[j] (1 + 2^-22) and rho_j in place of
+// Nmax and Pmax.
+__device__ __forceinline__ int pair_test(const Args& a, double s, double gam, double ni,
+                                         double rho_i, uint32_t j, float acc) {
+  const double ms = (double)a.margin_scale;
+  const double u = 0x1p-23;
+  const double nj = -2.0 * (double)a.hn_r[j] * (1.0 + 0x1p-22);
+  const double e = ms * (gam * (ni + 2.0 * nj) * (1.0 + 1e-6) + u * nj + (double)a.d * 0x1p-120);
+  const double r = ms * (rho_i + a.rho_r[j]);
+  const double t = -2.0 * (double)acc;
+  const double slack = 1e-12 * (ni + fabs(t) + e);
+  const double ps = s * a.phi;
+  const double hi = ni + t + e + slack;
+  if (hi >= 0.0 && sqrt(hi) + r < ps * (1.0 - 4e-9)) return 1;
+  const double lo = ni + t - e - slack;
+  if (lo > 0.0 && sqrt(lo) - r > ps * (1.0 + 4e-9)) return -1;
+  return 0;
+}
+
 __global__ void __launch_bounds__(256)
 range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -65,16 +90,25 @@ range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
   const int64_t end = a.coff[(row + 1) * a.splits] - a.cbase;
   const float* qrow = a.xq + row * (int64_t)a.d;
   const double phi2 = a.phi * a.phi;
+  const double s = scale_from_maxabs(a.ctrl->maxabs_bits, a.scale_exp);
+  const double tt = (double)a.d + 2.0;
+  const double gam = tt * 0x1p-23 / (1.0 - tt * 0x1p-23);
+  const double ni = a.n64_q[row], rho_i = a.rho_q[row];
   int kept = 0, unc = 0;
   for (int64_t p0 = beg; p0 < end; p0 += 64) {
     const int64_t p = p0 + lane;
     const bool live = p < end;
     const uint32_t c = live ? a.cand[p] : 0u;
-    const bool u = live && (c >> 31);
-    const bool need = live && (u || want_dist);
+    const uint32_t j = c & 0x7fffffffu;
+    // Uncertain for the tile: first the per-pair test (not under
+    // force_fallback, which recomputes every candidate).
+    int pt = 0;
+    if (live && (c >> 31) && !a.force_fallback) pt = pair_test(a, s, gam, ni, rho_i, j, a.cand_d[p]);
+    const bool u = live && (c >> 31) && pt == 0;
+    const bool need = live && (u || (want_dist && pt >= 0));
     double d2 = 0.0;
-    if (need) d2 = exact_d2(qrow, a.xr + (int64_t)(c & 0x7fffffffu) * a.d, a.d);
-    const bool keep = live && (!u || d2 <= phi2);
+    if (need) d2 = exact_d2(qrow, a.xr + (int64_t)j * a.d, a.d);
+    const bool keep = live && pt >= 0 && (!u || d2 <= phi2);
     if (live) a.cand_d[p] = keep ? (need ? (float)sqrt(d2) : 0.0f) : -1.0f;
     kept += __popcll(__ballot(keep));
     unc += __popcll(__ballot(u));

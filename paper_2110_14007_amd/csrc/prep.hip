@@ -25,7 +25,7 @@ namespace tod {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kFinalCols = 32;  // columns per block of the column-mean final sum
+constexpr int kFinalCols = 8;  // columns per block of the column-mean final sum
 
 __global__ void init_ctrl_kernel(Ctrl* ctrl) {
   uint32_t* w = reinterpret_cast<uint32_t*>(ctrl);
@@ -334,7 +334,7 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
     hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nr_pad)), dim3(kThreads), 0, st,
                        a.xr, p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r,
                        a.hn_r, p.self ? a.n64_q : (double*)nullptr,
-                       p.self ? a.rho_q : (double*)nullptr, 1, p.scale_exp, a.perm);
+                       p.self ? a.rho_q : a.rho_r, 1, p.scale_exp, a.perm);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.self) return e;
     hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nq_pad)), dim3(kThreads), 0, st,
@@ -347,7 +347,7 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
   const int64_t blocks_r = (p.nr_pad + kThreads - 1) / kThreads;
   hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_r), dim3(kThreads), 0, st, a.xr,
                      p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r, a.hn_r,
-                     p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : (double*)nullptr, 1,
+                     p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : a.rho_r, 1,
                      p.fold, p.dmain, p.scale_exp, cf, a.perm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.self) return e;

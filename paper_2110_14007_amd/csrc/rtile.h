@@ -130,11 +130,13 @@ range_tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // pair written so far (the same in both lanes).
   int run = 0;
   uint32_t* dst = nullptr;
+  float* fdst = nullptr;  // the candidates' accumulators (for the per-pair test)
   int64_t room = 0;
   if constexpr (FILL) {
     if (qvalid) {
       const int64_t o = a.coff[q * a.splits + split];
       dst = a.cand + (o - a.cbase);
+      fdst = a.cand_d + (o - a.cbase);
       room = a.coff[q * a.splits + split + 1] - o;
     }
   }
@@ -226,16 +228,22 @@ range_tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 #pragma unroll
         for (int g = 0; g < 4; ++g)
           rows |= (((m_lo >> (4 * g)) & 15u) << (8 * g)) | (((m_hi >> (4 * g)) & 15u) << (8 * g + 4));
+        // One trip per candidate of this lane (usually one or two).
+        auto accv = [&](int r) {
+          float v = acc[0];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if ((cm >> r) & 1u) {
-            const int row = mt::out_row(r, h);
-            const int pos = run + __builtin_popcount(rows & ((1u << row) - 1u));
-            if (pos < room)
-              dst[pos] = (uint32_t)(ts + row) | (((um >> r) & 1u) << 31);
-            else
-              atomicOr(&a.ctrl->internal, 1u);  // the passes disagree: report, never overrun
-          }
+          for (int e = 1; e < 16; ++e) v = r == e ? acc[e] : v;
+          return v;
+        };
+        for (uint32_t m = cm; m; m &= m - 1u) {
+          const int r = __builtin_ctz(m);
+          const int row = mt::out_row(r, h);
+          const int pos = run + __builtin_popcount(rows & ((1u << row) - 1u));
+          if (pos < room) {
+            dst[pos] = (uint32_t)(ts + row) | (((um >> r) & 1u) << 31);
+            fdst[pos] = accv(r);
+          } else
+            atomicOr(&a.ctrl->internal, 1u);  // the passes disagree: report, never overrun
         }
         run += __builtin_popcount(rows);
       }

@@ -82,7 +82,7 @@ struct Args {
   float* hn_r;      // -0.5 * fl32(||xhat_j||^2) per reference [nr_pad]
   double* n64_q;    // ||xhat_i||^2 per query (fp64) [nq_pad]
   double* rho_q;    // quantisation radius per query, rounded up [nq_pad]
-  double* rho_r_dummy;
+  double* rho_r;    // quantisation radius per reference when the sets differ (NWR), else null
   uint64_t* partial;   // per (query in block, split) sorted K' lists
   int32_t* worklist;   // global query ids that failed the certificate
   uint2* fbpart;       // fallback chunk lists: (D^2 bits hi, lo) [kFbGrid x k]
@@ -107,7 +107,8 @@ struct Args {
   int64_t* coff;       // their exclusive prefix sums [nq x S + 1]
   int64_t cbase;       // candidate offset of the first row of the current query batch
   uint32_t* cand;      // candidate reference ids of the batch; bit 31: not ruled in by the filter
-  float* cand_d;       // after verification: distance if kept (0 if not measured), -1 if not
+  float* cand_d;       // fill pass: the candidate's accumulator; after verification: its
+                       // distance if kept (0 if not measured), -1 if not
   int64_t ccap;        // candidate room
   int32_t* incnt;      // pairs in range per query row [nq]
   int64_t* row_ptr;    // CSR offsets [nq + 1] (the caller's output)
@@ -190,8 +191,8 @@ tod_status make_plan_nwr(int64_t nq, int64_t nr, int64_t d, int32_t self, const 
                          Plan* plan, const char** why);
 // NWR workspace regions; cand is the first byte of the candidate room.
 struct NwrLayout {
-  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, ccount, coff, part, goff,
-      incnt, cand;
+  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, rho_r, ccount, coff, part,
+      goff, incnt, cand;
   int64_t groups;  // 32-row query groups
   int32_t colpart_blocks;
 };
