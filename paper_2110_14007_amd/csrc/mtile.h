@@ -78,6 +78,32 @@ __device__ __forceinline__ void stage_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// LDS byte address of a pointer into the workgroup's shared memory.
+__device__ __forceinline__ uint32_t lds_off(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// Direct staging: each active lane moves 16 bytes from global memory to LDS
+// address lds + 16 * lane (global_load_lds_dwordx4; lds must be wave-uniform).
+// Issued from asm so that the compiler, which cannot tell the LDS buffers
+// apart, does not wait for every staging load before each LDS read; the
+// caller orders them with dl_barrier().  M0 is set right before the load.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g),
+               "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Barrier of the direct-staging pipeline: this wave's staging loads except
+// the newest N are complete (so is every LDS access), then all waves meet.
+template <int N>
+__device__ __forceinline__ void dl_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
 // Value of v in the partner lane (lane ^ 32).
 __device__ __forceinline__ uint32_t xchg32(uint32_t v, int h) {
   const auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
@@ -249,9 +275,16 @@ struct Layout {
   static_assert(!FOLD || DPAD == 16, "the folded seed uses the padding of 8-wide rows");
 };
 
+// Stage buffers: rows of 512 elements are staged directly into LDS two
+// stages ahead (three buffers); other rows through registers (two buffers).
+__host__ __device__ constexpr int stage_buffers(int dpad, bool fold) {
+  return dpad >= 512 && !fold ? 3 : 2;
+}
+
 __host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int ns, int qcap) {
-  return (size_t)2 * 32 * ns * (dpad == 16 ? 32 : dpad * 2 + 16) +
-         (fold ? 0 : (size_t)2 * 32 * ns * sizeof(float)) + (size_t)w * qcap * 64 * sizeof(uint2);
+  return (size_t)stage_buffers(dpad, fold) * 32 * ns * (dpad == 16 ? 32 : dpad * 2 + 16) +
+         (fold ? 0 : (size_t)stage_buffers(dpad, fold) * 32 * ns * sizeof(float)) +
+         (size_t)w * qcap * 64 * sizeof(uint2);
 }
 
 // At least two waves per SIMD for lists of up to 32 entries and rows of up to
@@ -277,10 +310,12 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   constexpr int NT = W * 64;
   constexpr int NL = (CHUNKS + NT - 1) / NT;
   static_assert(NL <= 16, "staged chunks per thread");
+  constexpr bool DL = stage_buffers(DPAD, FOLD) == 3;  // direct staging, two stages ahead
+  constexpr int NBUF = stage_buffers(DPAD, FOLD);
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* stage = smem;
-  float* hnb = (float*)(smem + 2 * STAGE);  // plain layout: seeds of the staged rows
-  uint2* qbase = (uint2*)(smem + 2 * STAGE + (FOLD ? 0 : 2 * TR * sizeof(float)));
+  float* hnb = (float*)(smem + NBUF * STAGE);  // plain layout: seeds of the staged rows
+  uint2* qbase = (uint2*)(smem + NBUF * STAGE + (FOLD ? 0 : NBUF * TR * sizeof(float)));
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, col = lane & 31;
@@ -327,11 +362,11 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // read back.  Rows of 256 or more elements (one 32-row sub-tile per stage,
   // one wave per SIMD, registers to spare) are loaded two stages ahead into
   // two register sets with fixed roles; shorter rows one stage ahead.
-  constexpr bool PF2 = DPAD >= 256;
+  constexpr bool PF2 = DPAD >= 256 && !DL;
   const unsigned char* xr_bytes = (const unsigned char*)a.xq_r;
-  uint4 st[NL], su[PF2 ? NL : 1];
+  uint4 st[DL ? 1 : NL], su[PF2 ? NL : 1];
 #pragma unroll
-  for (int i = 0; i < NL; ++i) st[i] = make_uint4(0, 0, 0, 0);
+  for (int i = 0; i < (DL ? 1 : NL); ++i) st[i] = make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int i = 0; i < (PF2 ? NL : 1); ++i) su[i] = make_uint4(0, 0, 0, 0);
   static_assert(TR / 4 <= NT, "one float4 of seeds per thread");
@@ -561,6 +596,38 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     return r_begin + (int64_t)s * TR;
   };
 
+  if constexpr (DL) {
+    // Rows of 512 elements: each wave moves 8 whole rows (one 1 KiB row per
+    // instruction) and 8 seeds of every stage straight into LDS, two stages
+    // ahead, 9 loads per wave per stage.  The compiler-visible wait first
+    // retires the query operand's loads, so that the compiler, which does
+    // not see the staging loads, has no load of its own left to wait for.
+    static_assert(TR == 8 * W && W == 4, "direct staging: 8 rows and 8 seeds per wave");
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    const uint32_t lbase = lds_off(smem);
+    auto dl_issue = [&](int64_t t0, int b) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < TR / W; ++i) {
+        const int r = wave + W * i;
+        const int64_t gr = t0 + r < r_end32 ? t0 + r : r_end32 - 1;
+        dma16(xr_bytes + gr * (int64_t)(DPAD * 2) + lane * 16, lbase + b * STAGE + r * ROWB);
+      }
+      if (lane < 2)  // rows t0 .. t0 + 31 all exist (t0 is a multiple of 32 below r_end)
+        dma16((const unsigned char*)(a.hn_r + t0 + 8 * wave) + lane * 16,
+              lbase + NBUF * STAGE + (b * TR + 8 * wave) * (int)sizeof(float));
+    };
+    dl_issue(t_of(0), 0);
+    dl_issue(t_of(1), 1);
+    dl_barrier<TR / W + 1>();
+    for (int it = 0; it < nst; ++it) {
+      // Buffer (it + 2) % 3 was last read in trip it - 1, before its barrier.
+      dl_issue(t_of(it + 2), (it + 2) % 3);
+      stage_body(t_of(it), it % 3);
+      dl_barrier<TR / W + 1>();
+    }
+    // No staging write may outlive the workgroup's LDS allocation.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else {
   TOD_MT_FETCH(t_of(0), st, sth)
   TOD_MT_PUT(0, st, sth)
   if constexpr (PF2) {
@@ -589,6 +656,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       TOD_MT_PUT((it + 1) & 1, st, sth)
       __syncthreads();
     }
+  }
   }
 #undef TOD_MT_FETCH
 #undef TOD_MT_PUT

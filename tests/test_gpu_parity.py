@@ -124,6 +124,32 @@ def test_cross_sets(env, prec):
     compare_knn(xq, xr, np.arange(len(xq)), idx, dist, oidx, odist)
 
 
+@pytest.mark.parametrize("prec", ["fp16", "bf16"])
+@pytest.mark.parametrize("n,d,k", [(1000, 300, 5), (2500, 512, 20), (1777, 512, 50),
+                                   (700, 257, 12)])
+def test_wide_rows(env, prec, n, d, k):
+    """Rows of 257..512 elements (the directly staged and the register-staged
+    wide kernels, lists of 16, 32 and 64), ragged row counts, every row."""
+    x, _ = workloads.generate("C4", n=n)
+    x = np.ascontiguousarray(x[:, :d])
+    say("wide rows", prec, n, d, k)
+    st, n_exc = check_full_lof(env, x, k, precision=prec)
+    say("stats", st, "excused", n_exc)
+
+
+@pytest.mark.parametrize("prec", ["fp16", "bf16"])
+def test_wide_rows_cross_and_splits(env, prec):
+    _, _, oracle = env
+    rng = np.random.default_rng(23)
+    xr = rng.standard_normal((4001, 512)).astype(np.float32)
+    xq = rng.standard_normal((333, 512)).astype(np.float32)
+    for kw in (dict(), dict(ref_splits=3), dict(query_block=96)):
+        say("wide cross", prec, kw)
+        idx, dist, st = run_knn(env, xq, xr, 9, precision=prec, **kw)
+        oidx, odist = oracle.knn(xq, xr, 9)
+        compare_knn(xq, xr, np.arange(len(xq)), idx, dist, oidx, odist)
+
+
 @pytest.mark.parametrize("prec", PRECS)
 def test_C2_reduced_full(env, prec):
     x, _ = workloads.generate("C2", n=20000)
