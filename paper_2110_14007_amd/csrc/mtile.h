@@ -339,6 +339,15 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     const ET* qrow = (const ET*)a.xq_q + (active ? q0 + col : 0) * (int64_t)DPAD;
 #pragma unroll
     for (int c = 0; c < KC; ++c) bq[c] = *reinterpret_cast<const V*>(qrow + 16 * c + 8 * h);
+    if constexpr (LY::wide) {
+      // One wave per SIMD: the operand lives in AGPRs, which the MFMA reads
+      // as its B operand directly.  Left to itself the compiler keeps it in
+      // VGPRs, spills it to AGPRs under the lists' register pressure and
+      // copies it back before every MFMA (about 110 copies per sub-tile at
+      // rows of 512 elements).
+#pragma unroll
+      for (int c = 0; c < KC; ++c) asm volatile("" : "+a"(bq[c]));
+    }
     if constexpr (FOLD) {
       const ET cf = (ET)(float)fold_const(std::is_same<ET, _Float16>::value ? TOD_PREC_FP16
                                                                            : TOD_PREC_BF16);
