@@ -67,6 +67,16 @@ typedef enum {
   TOD_PREC_BF16 = 3  /* bf16 MFMA distance tile, fp32 accumulate */
 } tod_precision;
 
+/* Outlier score from the k exact neighbour distances of a point (the kNN
+ * detector of Table 1: the distance to the k-th neighbour, or an aggregate of
+ * the k distances such as Angiulli and Pizzuti's weight, their sum). */
+typedef enum {
+  TOD_SCORE_KTH = 0,    /* distance to the k-th nearest neighbour (default) */
+  TOD_SCORE_MEAN = 1,   /* mean of the k distances */
+  TOD_SCORE_MEDIAN = 2, /* median of the k distances (mean of the two middle ones for even k) */
+  TOD_SCORE_SUM = 3     /* sum of the k distances */
+} tod_score;
+
 typedef struct {
   uint32_t struct_size;  /* must be sizeof(tod_options) */
   int32_t precision;     /* tod_precision; AUTO picks by d */
@@ -82,6 +92,8 @@ typedef struct {
                           * 16-seed partition (nearest of 16 evenly spaced rows) and every query
                           * block first scans the references of its own group, so the filter's
                           * thresholds tighten early.  Results are identical either way. */
+  int32_t score;         /* tod_score: the kNN outlier score of tod_knn_score, tod_knn_decision
+                          * and tod_lof's knn_score_out */
 } tod_options;
 
 /* Plan and per-phase timings of one call (filled when a non-NULL pointer is
@@ -107,10 +119,13 @@ typedef struct {
 void tod_default_options(tod_options* opts);
 
 /*
- * Workspace bytes needed by tod_knn (lof = 0) or tod_lof (lof = 1) for these
- * sizes and options.  Returns 0 if the arguments are invalid or unsupported.
+ * Workspace bytes needed for these sizes and options by
+ *   mode 0: tod_knn, tod_knn_score, tod_knn_decision (any query and reference sets);
+ *   mode 1: tod_lof (X against itself, nq == nr);
+ *   mode 2: tod_knn_classify.
+ * Returns 0 if the arguments are invalid or unsupported.
  */
-size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof,
+size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t mode,
                           const tod_options* opts);
 
 /*
@@ -127,8 +142,10 @@ tod_status tod_knn(const float* xq, int64_t nq, const float* xr, int64_t nr, int
                    void* stream, int64_t* idx_out, float* dist_out, tod_stats* stats);
 
 /*
- * kNN-OD scores of X against itself (each point's own row excluded):
- *   score_out[n] = distance to the k-th nearest neighbour (Table 1, kNN).
+ * kNN-OD scores of X against itself (each point's own row excluded), the
+ * detector's fit (Appendix D's fit / decision_scores_):
+ *   score_out[n] = opts->score of the k neighbour distances (default: the
+ *                  distance to the k-th nearest neighbour, Table 1's kNN).
  * idx_out[n x k] and dist_out[n x k] are optional (NULL to skip).
  */
 tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
@@ -146,6 +163,35 @@ tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
 tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
                    void* workspace, size_t ws_bytes, void* stream, float* lof_out,
                    float* knn_score_out, int64_t* idx_out, float* dist_out, tod_stats* stats);
+
+/*
+ * kNN-OD scores of new points xq[nq x d] against the fitted set xr[nr x d]
+ * (Appendix D's decision_function, the inductive setting): the same score as
+ * tod_knn_score, from the k nearest rows of xr, nothing excluded (a row of xr
+ * passed again as a query is its own neighbour at distance 0).
+ *   score_out[nq] fp32; idx_out, dist_out optional as in tod_knn.
+ * opts->exclude_self must be 0.
+ */
+tod_status tod_knn_decision(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                            int32_t k, const tod_options* opts, void* workspace, size_t ws_bytes,
+                            void* stream, float* score_out, int64_t* idx_out, float* dist_out,
+                            tod_stats* stats);
+
+/*
+ * kNN classifier (Appendix B's kNN_CLF: cdist, topk, then a majority vote):
+ * the predicted class of every row of xq is the most frequent label among
+ * its k nearest rows of xr, ties going to the smallest label.
+ *   labels_r[nr]  int32 (device), classes 0 .. n_classes - 1
+ *   pred_out[nq]  int32 (device)
+ * Requires 1 <= n_classes <= 65536 and opts->exclude_self == 0 (unless
+ * xq == xr: then each point votes without itself).  A label outside
+ * [0, n_classes) makes the call fail with TOD_ERR_INVALID_ARG (after the
+ * kernels ran; pred_out is then unspecified).  Workspace: mode 2.
+ */
+tod_status tod_knn_classify(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                            int32_t k, const int32_t* labels_r, int32_t n_classes,
+                            const tod_options* opts, void* workspace, size_t ws_bytes,
+                            void* stream, int32_t* pred_out, tod_stats* stats);
 
 /*
  * Host-only planner (Section 6 automatic batching): fills *plan with the

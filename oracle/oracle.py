@@ -10,7 +10,9 @@ Functions:
   knn_self(x, k, rows=None)               -> kNN of X against itself, self excluded
   lof(idx, dist)                          -> (lof, lrd, kdist), fp64 [n]
   lof_rows(x, k, rows)                    -> (lof, lrd, kdist) for the listed rows
-  knn_score(dist)                         -> distance to the k-th neighbour
+  knn_score(dist, method="kth")           -> kNN outlier score from the k neighbour distances:
+                                             k-th (default), mean, median or sum
+  knn_vote(idx, labels, n_classes)        -> kNN classifier: majority label, ties to the smallest
   nwr(xq, xr, phi, exclude_self, rows=None) -> (row_ptr int64 [m+1], idx int64, dist fp64):
                                              neighbours within range, CSR, ascending index
 """
@@ -106,9 +108,32 @@ def knn_self(x, k: int, rows=None, threads: int = 0):
     return knn(x, x, k, exclude_self=True, rows=rows, threads=threads)
 
 
-def knn_score(dist) -> np.ndarray:
-    """kNN outlier score: distance to the k-th nearest neighbour."""
-    return np.asarray(dist)[:, -1].copy()
+def knn_score(dist, method: str = "kth") -> np.ndarray:
+    """kNN outlier score of each row from its k neighbour distances (sorted
+    ascending, fp64): the distance to the k-th nearest neighbour (Table 1's
+    kNN detector), or the mean, the median (mean of the two middle distances
+    for even k) or the sum of the k distances (the weight of Angiulli and
+    Pizzuti's detector, which the paper cites for kNN)."""
+    d = np.asarray(dist, dtype=np.float64)
+    if method in ("kth", "largest"):
+        return d[:, -1].copy()
+    if method == "mean":
+        return d.sum(axis=1) / d.shape[1]
+    if method == "median":
+        return np.median(d, axis=1)
+    if method == "sum":
+        return d.sum(axis=1)
+    raise ValueError("unknown score method %r" % method)
+
+
+def knn_vote(idx, labels, n_classes: int) -> np.ndarray:
+    """kNN classifier (Appendix B): for each row, the most frequent label among
+    its k neighbours; ties go to the smallest label."""
+    idx = np.asarray(idx, dtype=np.int64)
+    lab = np.asarray(labels, dtype=np.int64)[idx]  # [m, k]
+    counts = np.zeros((lab.shape[0], int(n_classes)), dtype=np.int64)
+    np.add.at(counts, (np.repeat(np.arange(lab.shape[0]), lab.shape[1]), lab.ravel()), 1)
+    return counts.argmax(axis=1).astype(np.int32)  # argmax returns the first (smallest) maximum
 
 
 def lof(idx, dist):

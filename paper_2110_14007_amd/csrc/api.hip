@@ -57,6 +57,8 @@ tod_status resolve_options(const tod_options* in, tod_options* out) {
     return fail(TOD_ERR_INVALID_ARG, "margin_scale must be a finite value >= 1");
   if (out->reorder < -1 || out->reorder > 1)
     return fail(TOD_ERR_INVALID_ARG, "reorder must be -1, 0 or 1");
+  if (out->score < TOD_SCORE_KTH || out->score > TOD_SCORE_SUM)
+    return fail(TOD_ERR_INVALID_ARG, "unknown score");
   return TOD_OK;
 }
 
@@ -86,6 +88,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   p->d = d;
   p->k = k;
   p->lof = lof;
+  p->lists = (lof || o.score != TOD_SCORE_KTH) ? 1 : 0;
   p->self = self;
   p->exclude_self = o.exclude_self ? 1 : 0;
   // Filter precision (provable quantization, Section 5.2 step ii).  The fp16
@@ -212,13 +215,13 @@ Layout make_layout(const Plan& p) {
   } else {
     L.perm = L.lab = L.cstart = L.bcnt = L.boff = 0;
   }
-  if (p.lof) {
+  if (p.lists) {
     L.idx32 = take(sizeof(int32_t) * p.nq * p.k);
     L.d64 = take(sizeof(double) * p.nq * p.k);
-    L.lrd = take(sizeof(double) * p.nq);
   } else {
-    L.idx32 = L.d64 = L.lrd = 0;
+    L.idx32 = L.d64 = 0;
   }
+  L.lrd = p.lof ? take(sizeof(double) * p.nq) : 0;
   L.total = off;
   return L;
 }
@@ -342,11 +345,14 @@ tod_status hip_fail(hipError_t e, const char* where) {
   return fail(TOD_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
 }
 
+// mode: 0 kNN lists / scores, 1 LOF, 2 classifier.
 tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d, int32_t k,
-               const tod_options* opts_in, int32_t force_excl, int32_t lof, void* ws,
+               const tod_options* opts_in, int32_t force_excl, int32_t mode, void* ws,
                size_t ws_bytes, void* stream, int64_t* idx_out, float* dist_out,
-               float* score_out, float* lof_out, tod_stats* stats) {
+               float* score_out, float* lof_out, const int32_t* labels_r, int32_t n_classes,
+               int32_t* pred_out, tod_stats* stats) {
   g_last_error.clear();
+  const int32_t lof = mode == 1 ? 1 : 0;
   tod_options o;
   tod_status st = resolve_options(opts_in, &o);
   if (st != TOD_OK) return st;
@@ -367,6 +373,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   const char* why = "";
   st = tod::make_plan(nq, nr, d, k, lof, self, o, &p, &why);
   if (st != TOD_OK) return fail(st, why);
+  if (mode == 2) p.lists = 1;
   const Layout L = tod::make_layout(p);
   if (ws_bytes < L.total)
     return fail(TOD_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) +
@@ -410,9 +417,13 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.cstart = p.order ? (int32_t*)(base + L.cstart) : nullptr;
   a.bcnt = p.order ? (int32_t*)(base + L.bcnt) : nullptr;
   a.boff = p.order ? (int32_t*)(base + L.boff) : nullptr;
-  a.idx32 = lof ? (int32_t*)(base + L.idx32) : nullptr;
-  a.d64 = lof ? (double*)(base + L.d64) : nullptr;
+  a.idx32 = p.lists ? (int32_t*)(base + L.idx32) : nullptr;
+  a.d64 = p.lists ? (double*)(base + L.d64) : nullptr;
   a.lrd = lof ? (double*)(base + L.lrd) : nullptr;
+  a.score = o.score;
+  a.labels_r = labels_r;
+  a.n_classes = n_classes;
+  a.pred_out = pred_out;
   a.idx_out = idx_out;
   a.dist_out = dist_out;
   a.score_out = score_out;
@@ -448,6 +459,14 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     he = tod::launch_lof(p, a, s);
     if (he != hipSuccess) return hip_fail(he, "lof launch");
   }
+  if (score_out && o.score != TOD_SCORE_KTH) {
+    he = tod::launch_score(p, a, s);
+    if (he != hipSuccess) return hip_fail(he, "score launch");
+  }
+  if (mode == 2) {
+    he = tod::launch_vote(p, a, s);
+    if (he != hipSuccess) return hip_fail(he, "vote launch");
+  }
   hipEvent_t e_end = tm.mark(s);
   tod::Ctrl host;
   he = hipMemcpyAsync(&host, a.ctrl, sizeof(host), hipMemcpyDeviceToHost, s);
@@ -476,6 +495,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     stats->ms_total = Timers::ms(e0, e_end);
   }
   if (host.nonfinite) return fail(TOD_ERR_NONFINITE, "input contains NaN or Inf");
+  if (host.bad_label) return fail(TOD_ERR_INVALID_ARG, "a reference label is outside [0, n_classes)");
   return TOD_OK;
 }
 
@@ -662,18 +682,21 @@ void tod_default_options(tod_options* o) {
   o->margin_scale = 1.0f;
 }
 
-size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof,
+size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t mode,
                           const tod_options* opts) {
   tod_options o;
   if (resolve_options(opts, &o) != TOD_OK) return 0;
+  if (mode < 0 || mode > 2) return 0;
+  const int32_t lof = mode == 1 ? 1 : 0;
   if (lof) o.exclude_self = 1;
   if (check_sizes(nq, nr, d, k, o.exclude_self) != TOD_OK) return 0;
   if (lof && nq != nr) return 0;
   Plan p;
   const char* why;
-  // lof = 0 sizes for separate query and reference sets (enough for any
-  // tod_knn / tod_knn_score call); lof = 1 for X against itself.
-  if (tod::make_plan(nq, nr, d, k, lof ? 1 : 0, lof ? 1 : 0, o, &p, &why) != TOD_OK) return 0;
+  // Modes 0 and 2 size for separate query and reference sets (enough for any
+  // call of those entry points); mode 1 for X against itself.
+  if (tod::make_plan(nq, nr, d, k, lof, lof, o, &p, &why) != TOD_OK) return 0;
+  if (mode == 2) p.lists = 1;
   return tod::make_layout(p).total;
 }
 
@@ -682,7 +705,7 @@ tod_status tod_knn(const float* xq, int64_t nq, const float* xr, int64_t nr, int
                    void* stream, int64_t* idx_out, float* dist_out, tod_stats* stats) {
   if (!idx_out || !dist_out) return fail(TOD_ERR_INVALID_ARG, "null output pointer");
   return run(xq, nq, xr, nr, d, k, opts, 0, 0, workspace, ws_bytes, stream, idx_out, dist_out,
-             nullptr, nullptr, stats);
+             nullptr, nullptr, nullptr, 0, nullptr, stats);
 }
 
 tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
@@ -691,7 +714,7 @@ tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
                          tod_stats* stats) {
   if (!score_out) return fail(TOD_ERR_INVALID_ARG, "null score output");
   return run(x, n, x, n, d, k, opts, 1, 0, workspace, ws_bytes, stream, idx_out, dist_out,
-             score_out, nullptr, stats);
+             score_out, nullptr, nullptr, 0, nullptr, stats);
 }
 
 tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
@@ -699,7 +722,31 @@ tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_op
                    float* knn_score_out, int64_t* idx_out, float* dist_out, tod_stats* stats) {
   if (!lof_out) return fail(TOD_ERR_INVALID_ARG, "null LOF output");
   return run(x, n, x, n, d, k, opts, 1, 1, workspace, ws_bytes, stream, idx_out, dist_out,
-             knn_score_out, lof_out, stats);
+             knn_score_out, lof_out, nullptr, 0, nullptr, stats);
+}
+
+tod_status tod_knn_decision(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                            int32_t k, const tod_options* opts, void* workspace, size_t ws_bytes,
+                            void* stream, float* score_out, int64_t* idx_out, float* dist_out,
+                            tod_stats* stats) {
+  g_last_error.clear();
+  if (!score_out) return fail(TOD_ERR_INVALID_ARG, "null score output");
+  if (opts && opts->struct_size == sizeof(tod_options) && opts->exclude_self)
+    return fail(TOD_ERR_INVALID_ARG, "tod_knn_decision scores new points: exclude_self must be 0");
+  return run(xq, nq, xr, nr, d, k, opts, 0, 0, workspace, ws_bytes, stream, idx_out, dist_out,
+             score_out, nullptr, nullptr, 0, nullptr, stats);
+}
+
+tod_status tod_knn_classify(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                            int32_t k, const int32_t* labels_r, int32_t n_classes,
+                            const tod_options* opts, void* workspace, size_t ws_bytes,
+                            void* stream, int32_t* pred_out, tod_stats* stats) {
+  g_last_error.clear();
+  if (!labels_r || !pred_out) return fail(TOD_ERR_INVALID_ARG, "null labels or prediction output");
+  if (n_classes < 1 || n_classes > 65536)
+    return fail(TOD_ERR_INVALID_ARG, "n_classes must be in [1, 65536]");
+  return run(xq, nq, xr, nr, d, k, opts, 0, 2, workspace, ws_bytes, stream, nullptr, nullptr,
+             nullptr, nullptr, labels_r, n_classes, pred_out, stats);
 }
 
 size_t tod_nwr_workspace_size(int64_t nq, int64_t nr, int64_t d, const tod_options* opts) {

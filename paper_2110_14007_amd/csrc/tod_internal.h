@@ -35,6 +35,8 @@ struct Plan {
   int32_t self;        // query set == reference set (one quantised copy)
   int32_t exclude_self;
   int32_t lof;         // LOF buffers needed
+  int32_t lists;       // int32 / fp64 neighbour lists kept in the workspace (LOF, score
+                       // aggregates, classifier)
   int32_t order;       // 1: grouped scan order (order.hip), X against X only
 };
 
@@ -56,7 +58,9 @@ struct Ctrl {
   uint64_t certified;       // rows certified by the shortlist test
   uint64_t fold_max_bits;   // max over references of the folded seed's error, fp64 bits
   uint64_t uncertain;       // NWR: candidate pairs recomputed exactly
-  uint64_t pad[2];
+  uint32_t bad_label;       // classifier: a reference label outside [0, n_classes)
+  uint32_t pad0;
+  uint64_t pad1;
 };
 
 // Everything a kernel needs to know about the problem.
@@ -101,6 +105,10 @@ struct Args {
   float* dist_out;
   float* score_out;
   float* lof_out;
+  int32_t score;            // tod_score of score_out
+  int32_t n_classes;        // classifier
+  const int32_t* labels_r;  // classifier: reference labels [nr]
+  int32_t* pred_out;        // classifier: predicted classes [nq]
   // neighbours within range (rtile.h, nwr.hip)
   double phi;          // the range threshold (a distance)
   int32_t* ccount;     // count pass: candidates per (query, split) [nq_pad x S]
@@ -164,6 +172,10 @@ hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t
                           hipStream_t s);
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t s);
+// kNN score aggregates (mean, median, sum) and the classifier's majority vote
+// from the exact lists.
+hipError_t launch_score(const Plan& p, const Args& a, hipStream_t s);
+hipError_t launch_vote(const Plan& p, const Args& a, hipStream_t s);
 
 // Neighbours within range: fused MFMA tile with the range test (count pass:
 // candidates per (query, split); fill pass: their ids, in increasing j per

@@ -26,10 +26,11 @@ TOD_ERR_CAPACITY = 7
 PREC_AUTO, PREC_FP32, PREC_FP16, PREC_BF16 = 0, 1, 2, 3
 PRECISIONS = {"auto": PREC_AUTO, "fp32": PREC_FP32, "fp16": PREC_FP16, "bf16": PREC_BF16}
 PRECISION_NAMES = {v: k for k, v in PRECISIONS.items()}
+SCORES = {"kth": 0, "largest": 0, "mean": 1, "median": 2, "sum": 3}
 
 SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
-           "tod_nwr_workspace_size", "tod_nwr", "tod_plan", "tod_status_string",
-           "tod_last_error")
+           "tod_knn_decision", "tod_knn_classify", "tod_nwr_workspace_size", "tod_nwr", "tod_plan",
+           "tod_status_string", "tod_last_error")
 
 
 class tod_options(ctypes.Structure):
@@ -44,6 +45,7 @@ class tod_options(ctypes.Structure):
         ("force_fallback", ctypes.c_int32),
         ("no_recheck", ctypes.c_int32),
         ("reorder", ctypes.c_int32),
+        ("score", ctypes.c_int32),
     ]
 
 
@@ -100,6 +102,12 @@ def _load():
     lib.tod_knn_score.restype = ctypes.c_int
     lib.tod_lof.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, vp, st_p]
     lib.tod_lof.restype = ctypes.c_int
+    lib.tod_knn_decision.argtypes = [vp, i64, vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp,
+                                      st_p]
+    lib.tod_knn_decision.restype = ctypes.c_int
+    lib.tod_knn_classify.argtypes = [vp, i64, vp, i64, i64, i32, vp, i32, opt_p, vp, sz, vp, vp,
+                                     st_p]
+    lib.tod_knn_classify.restype = ctypes.c_int
     lib.tod_nwr_workspace_size.argtypes = [i64, i64, i64, opt_p]
     lib.tod_nwr_workspace_size.restype = sz
     lib.tod_nwr.argtypes = [vp, i64, vp, i64, i64, ctypes.c_double, opt_p, vp, sz, vp, vp, i64, vp,
@@ -126,7 +134,8 @@ def last_error() -> str:
 
 
 def options(precision="auto", exclude_self=False, shortlist=0, query_block=0, ref_splits=0,
-            margin_scale=1.0, force_fallback=False, no_recheck=False, reorder=0) -> tod_options:
+            margin_scale=1.0, force_fallback=False, no_recheck=False, reorder=0,
+            score="kth") -> tod_options:
     o = tod_options()
     _lib.tod_default_options(ctypes.byref(o))
     o.precision = PRECISIONS[precision] if isinstance(precision, str) else int(precision)
@@ -138,6 +147,7 @@ def options(precision="auto", exclude_self=False, shortlist=0, query_block=0, re
     o.force_fallback = int(bool(force_fallback))
     o.no_recheck = int(bool(no_recheck))
     o.reorder = int(reorder)
+    o.score = SCORES[score] if isinstance(score, str) else int(score)
     return o
 
 
@@ -152,8 +162,9 @@ def _check(status: int, where: str):
         raise TodError(status, where, last_error())
 
 
-def tod_workspace_size(nq: int, nr: int, d: int, k: int, lof: bool = False, opts=None) -> int:
-    return int(_lib.tod_workspace_size(int(nq), int(nr), int(d), int(k), int(bool(lof)),
+def tod_workspace_size(nq: int, nr: int, d: int, k: int, mode: int = 0, opts=None) -> int:
+    """mode 0: kNN / scores / decision, 1 (or True): LOF, 2: classifier."""
+    return int(_lib.tod_workspace_size(int(nq), int(nr), int(d), int(k), int(mode),
                                        ctypes.byref(opts) if opts is not None else None))
 
 
@@ -285,6 +296,54 @@ def tod_lof(x, k: int, opts=None, workspace=None, stream=None, stats=None,
                       ctypes.byref(stats) if stats is not None else None)
     _check(st, "tod_lof")
     return (lof, score, idx, dist) if return_lists else (lof, score)
+
+
+def tod_knn_decision(xq, xr, k: int, opts=None, workspace=None, stream=None, stats=None,
+                     return_lists: bool = False):
+    """kNN-OD scores of new points xq against the fitted set xr (nothing excluded)."""
+    torch = _torch()
+    _dev_matrix(xq, "xq")
+    _dev_matrix(xr, "xr")
+    nq, d = xq.shape
+    nr = xr.shape[0]
+    if xr.shape[1] != d:
+        raise ValueError("xq and xr must have the same number of columns")
+    score = torch.empty((nq,), dtype=torch.float32, device=xq.device)
+    idx = dist = None
+    if return_lists:
+        idx = torch.empty((nq, k), dtype=torch.int64, device=xq.device)
+        dist = torch.empty((nq, k), dtype=torch.float32, device=xq.device)
+    need = tod_workspace_size(nq, nr, d, k, 0, opts)
+    wsbuf, wsp, wsn = _ws(workspace, need, xq.device)
+    st = _lib.tod_knn_decision(_p(xq), nq, _p(xr), nr, d, int(k),
+                               ctypes.byref(opts) if opts is not None else None, wsp, wsn,
+                               _stream(stream), _p(score), _p(idx), _p(dist),
+                               ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_knn_decision")
+    return (score, idx, dist) if return_lists else score
+
+
+def tod_knn_classify(xq, xr, labels_r, k: int, n_classes: int, opts=None, workspace=None,
+                     stream=None, stats=None):
+    """Majority-vote class of every row of xq among its k nearest rows of xr -> int32 [nq]."""
+    torch = _torch()
+    _dev_matrix(xq, "xq")
+    _dev_matrix(xr, "xr")
+    if (not isinstance(labels_r, torch.Tensor) or not labels_r.is_cuda
+            or labels_r.dtype != torch.int32 or labels_r.dim() != 1
+            or labels_r.shape[0] != xr.shape[0] or not labels_r.is_contiguous()):
+        raise TypeError("labels_r must be a contiguous int32 CUDA tensor of length nr")
+    nq, d = xq.shape
+    nr = xr.shape[0]
+    pred = torch.empty((nq,), dtype=torch.int32, device=xq.device)
+    need = tod_workspace_size(nq, nr, d, k, 2, opts)
+    wsbuf, wsp, wsn = _ws(workspace, need, xq.device)
+    st = _lib.tod_knn_classify(_p(xq), nq, _p(xr), nr, d, int(k), _p(labels_r), int(n_classes),
+                               ctypes.byref(opts) if opts is not None else None, wsp, wsn,
+                               _stream(stream), _p(pred),
+                               ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_knn_classify")
+    return pred
 
 
 def tod_nwr_workspace_size(nq: int, nr: int, d: int, opts=None) -> int:

@@ -162,3 +162,24 @@ def test_nwr_workspace_size(tod):
     assert tod.tod_nwr_workspace_size(0, 1000, 16) == 0
     assert tod.tod_nwr_workspace_size(10, 10, 16, tod.options(precision="fp32")) == 0
     assert tod.status_string(tod.TOD_ERR_CAPACITY) == "TOD_ERR_CAPACITY"
+
+
+def test_score_and_classifier_entry_points_validate(tod):
+    lib = tod.raw_library()
+    bad = tod.options()
+    bad.score = 9
+    assert _knn(tod, opts=bad) == tod.TOD_ERR_INVALID_ARG
+    o = tod.options(exclude_self=True)
+    assert lib.tod_knn_decision(FAKE, 100, FAKE, 100, 8, 5, ctypes.byref(o), FAKE, 1 << 30, None,
+                                FAKE, None, None, None) == tod.TOD_ERR_INVALID_ARG
+    assert lib.tod_knn_decision(FAKE, 100, FAKE, 100, 8, 5, None, FAKE, 1 << 30, None, None,
+                                None, None, None) == tod.TOD_ERR_INVALID_ARG
+    for n_classes, labels, pred in ((0, FAKE, FAKE), (70000, FAKE, FAKE), (3, None, FAKE),
+                                    (3, FAKE, None)):
+        assert lib.tod_knn_classify(FAKE, 100, FAKE, 100, 8, 5, labels, n_classes, None, FAKE,
+                                    1 << 30, None, pred, None) == tod.TOD_ERR_INVALID_ARG
+    # the classifier and score aggregates keep neighbour lists in the workspace
+    base = tod.tod_workspace_size(1000, 1000, 8, 5, 0)
+    assert tod.tod_workspace_size(1000, 1000, 8, 5, 2) > base
+    assert tod.tod_workspace_size(1000, 1000, 8, 5, 0, tod.options(score="median")) > base
+    assert tod.tod_workspace_size(1000, 1000, 8, 5, 3) == 0

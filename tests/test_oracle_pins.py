@@ -370,3 +370,72 @@ def test_nwr_rejects_bad_arguments(oracle_mod):
     for phi in (-1.0, float("nan")):
         with pytest.raises(ValueError):
             oracle_mod.nwr(x, x, phi)
+
+
+# ---------------------------------------------------------------------------
+# kNN score variants (Table 1's kNN detector; Angiulli and Pizzuti's weight is
+# the sum) and the kNN classifier's vote (Appendix B).
+# ---------------------------------------------------------------------------
+
+def _score_fixture():
+    out = {}
+    with open(os.path.join(os.path.dirname(__file__), "golden", "line10_scores.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            k, name, *vals = line.split()
+            out[(int(k), name)] = [float(Fraction(v)) for v in vals]
+    return out
+
+
+@pytest.mark.parametrize("k", [2, 3])
+@pytest.mark.parametrize("method", ["mean", "median", "sum"])
+def test_score_variants_line_golden(oracle_mod, k, method):
+    x = workloads.line(10, 1)
+    _, dist = oracle_mod.knn_self(x, k)
+    got = oracle_mod.knn_score(dist, method)
+    np.testing.assert_allclose(got, _score_fixture()[(k, method)], rtol=1e-15, atol=0)
+    np.testing.assert_array_equal(oracle_mod.knn_score(dist, "kth"), dist[:, -1])
+
+
+def test_score_variants_lattice_closed_forms(oracle_mod):
+    # 9 x 9 lattice, k = 4: interior points have four neighbours at 1; a
+    # border point that is not a corner has three at 1 and a diagonal at
+    # sqrt 2; a corner has two at 1, one at sqrt 2 and one at 2.
+    x = workloads.lattice(9, 2)
+    _, dist = oracle_mod.knn_self(x, 4)
+    r2 = math.sqrt(2.0)
+    want = {"interior": (1.0, 1.0, 4.0), "border": ((3 + r2) / 4, 1.0, 3 + r2),
+            "corner": ((4 + r2) / 4, (1 + r2) / 2, 4 + r2)}
+    scores = {m: oracle_mod.knn_score(dist, m) for m in ("mean", "median", "sum")}
+    for i, (r, c) in enumerate(x.astype(int).tolist()):
+        on_edge = (r in (0, 8)) + (c in (0, 8))
+        kind = "corner" if on_edge == 2 else ("border" if on_edge == 1 else "interior")
+        for m, v in zip(("mean", "median", "sum"), want[kind]):
+            assert abs(scores[m][i] - v) <= 1e-15 * v, (i, kind, m, scores[m][i], v)
+
+
+def test_vote_hand_examples(oracle_mod):
+    # References at 0..9 on a line with labels 0,0,0,1,1,1,1,2,2,2.
+    xr = workloads.line(10, 1)
+    labels = np.array([0, 0, 0, 1, 1, 1, 1, 2, 2, 2], np.int32)
+    xq = np.array([[2.6], [2.4], [6.6], [8.9]], np.float32)
+    idx3, _ = oracle_mod.knn(xq, xr, 3)
+    assert idx3.tolist() == [[3, 2, 4], [2, 3, 1], [7, 6, 8], [9, 8, 7]]
+    assert oracle_mod.knn_vote(idx3, labels, 3).tolist() == [1, 0, 2, 2]
+    idx2, _ = oracle_mod.knn(xq, xr, 2)
+    # k = 2 near a class boundary: one vote each, the smaller label wins
+    assert oracle_mod.knn_vote(idx2, labels, 3).tolist() == [0, 0, 1, 2]
+
+
+def test_vote_matches_counting_by_hand(oracle_mod):
+    rng = np.random.default_rng(8)
+    idx = rng.integers(0, 50, (200, 7))
+    labels = rng.integers(0, 4, 50).astype(np.int32)
+    got = oracle_mod.knn_vote(idx, labels, 4)
+    for r in range(len(idx)):
+        votes = {}
+        for j in idx[r]:
+            votes[int(labels[j])] = votes.get(int(labels[j]), 0) + 1
+        top = max(votes.values())
+        assert got[r] == min(c for c, n in votes.items() if n == top)

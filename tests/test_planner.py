@@ -46,11 +46,11 @@ def test_kprime_covers_k(tod, k):
 def test_workspace_grows_with_problem(tod):
     a = tod.tod_workspace_size(10000, 10000, 32, 10)
     b = tod.tod_workspace_size(20000, 20000, 32, 10)
-    c = tod.tod_workspace_size(20000, 20000, 32, 10, lof=True)
+    c = tod.tod_workspace_size(20000, 20000, 32, 10, mode=1)
     assert 0 < a < b
     assert c > 0
     assert tod.tod_workspace_size(10, 10, 4, 11) == 0  # k > nr
-    assert tod.tod_workspace_size(10, 12, 4, 5, lof=True) == 0  # LOF needs nq == nr
+    assert tod.tod_workspace_size(10, 12, 4, 5, mode=1) == 0  # LOF needs nq == nr
 
 
 @pytest.mark.parametrize("k,expect", [(5, 32), (10, 64), (20, 64), (50, 128), (200, 256)])
