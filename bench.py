@@ -2,7 +2,8 @@
 
 One step = one tod_lof call on the whole workload: prep, fused distance tiles
 with top-K' selection, certificate + exact recheck, fallback, kNN-OD score
-and LOF for every point.  Inputs are resident in HBM before timing starts.
+and LOF for every point (--detector knn: the kNN score alone; --detector abod:
+ABOD from the same lists).  Inputs are resident in HBM before timing starts.
 For a neighbours-within-range workload (--workload N1) one step is one
 tod_nwr call as the paper defines the operator (the indices of the pairs in
 range): prep, the range tile's count and fill passes, exact verification of
@@ -35,6 +36,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--precision", default="auto")
+    ap.add_argument("--detector", default="lof", choices=("lof", "knn", "abod"),
+                    help="what one step computes on a kNN workload: LOF (with the kNN score, "
+                         "the default), the kNN score alone, or ABOD")
+    ap.add_argument("--score", default="kth", choices=("kth", "mean", "median", "sum"),
+                    help="kNN score of the step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle baseline sample")
@@ -255,18 +261,27 @@ def main():
     n, d, k = x_host.shape[0], x_host.shape[1], w.k
     dev = torch.device("cuda:0")
     x = torch.from_numpy(x_host).to(dev)
-    opts = tod.options(precision=args.precision, query_block=w.query_block)
+    opts = tod.options(precision=args.precision, query_block=w.query_block, score=args.score)
     ws = tod.Workspace()
     out = (torch.empty(n, dtype=torch.float32, device=dev),
            torch.empty(n, dtype=torch.float32, device=dev))
+
+    def step(st=None):
+        if args.detector == "lof":
+            tod.tod_lof(x, k, opts, workspace=ws, out=out, stats=st)
+        elif args.detector == "knn":
+            tod.tod_knn_score(x, k, opts, workspace=ws, stats=st)
+        else:
+            tod.tod_abod(x, min(k, 64), opts, workspace=ws, stats=st)
+
     for _ in range(args.warmup):
-        tod.tod_lof(x, k, opts, workspace=ws, out=out)
+        step()
     torch.cuda.synchronize()
     stats = []
     t0 = time.perf_counter()
     for _ in range(args.steps):
         st = tod.new_stats()
-        tod.tod_lof(x, k, opts, workspace=ws, out=out, stats=st)
+        step(st)
         stats.append(st.as_dict())
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -305,6 +320,7 @@ def main():
         "dtype": "f32+f64" if prec == "fp32" else "%s+f64" % prec.replace("fp", "f"),
         "data": "synthetic",
         "config": {"workload": "%s: %s" % (w.name, w.description), "n": n, "d": d, "k": k,
+                   "detector": args.detector, "score": args.score,
                    "filter_precision": prec, "kprime": stats[0]["kprime"],
                    "ref_splits": stats[0]["ref_splits"], "query_block": stats[0]["query_block"],
                    "parallelism": "single GPU"},

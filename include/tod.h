@@ -121,7 +121,7 @@ void tod_default_options(tod_options* opts);
 /*
  * Workspace bytes needed for these sizes and options by
  *   mode 0: tod_knn, tod_knn_score, tod_knn_decision (any query and reference sets);
- *   mode 1: tod_lof (X against itself, nq == nr);
+ *   mode 1: tod_lof, tod_abod (X against itself, nq == nr);
  *   mode 2: tod_knn_classify.
  * Returns 0 if the arguments are invalid or unsupported.
  */
@@ -192,6 +192,22 @@ tod_status tod_knn_classify(const float* xq, int64_t nq, const float* xr, int64_
                             int32_t k, const int32_t* labels_r, int32_t n_classes,
                             const tod_options* opts, void* workspace, size_t ws_bytes,
                             void* stream, int32_t* pred_out, tod_stats* stats);
+
+/*
+ * ABOD as Section 4.3 builds it from the kNN and cosine-similarity operators:
+ * for every point of X (its own row excluded), the mean over the unordered
+ * pairs {b, c} of its k nearest neighbours of the cosine of the angle between
+ * x_b - x_i and x_c - x_i (fp64, rounded to fp32).  Pairs with a
+ * zero-length difference (a duplicate of x_i) are left out; a point without
+ * any pair left scores 0.  Higher means more outlying (the neighbours lie in
+ * one direction).
+ *   score_out[n] fp32; idx_out, dist_out optional lists as in tod_knn.
+ * Requires 2 <= k <= 64 (TOD_ERR_INVALID_ARG below, TOD_ERR_UNSUPPORTED above).
+ * Workspace: mode 1 of tod_workspace_size.
+ */
+tod_status tod_abod(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
+                    void* workspace, size_t ws_bytes, void* stream, float* score_out,
+                    int64_t* idx_out, float* dist_out, tod_stats* stats);
 
 /*
  * Host-only planner (Section 6 automatic batching): fills *plan with the

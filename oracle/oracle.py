@@ -13,6 +13,7 @@ Functions:
   knn_score(dist, method="kth")           -> kNN outlier score from the k neighbour distances:
                                              k-th (default), mean, median or sum
   knn_vote(idx, labels, n_classes)        -> kNN classifier: majority label, ties to the smallest
+  abod(x, idx)                            -> angle-based score: mean cosine over neighbour pairs
   nwr(xq, xr, phi, exclude_self, rows=None) -> (row_ptr int64 [m+1], idx int64, dist fp64):
                                              neighbours within range, CSR, ascending index
 """
@@ -124,6 +125,34 @@ def knn_score(dist, method: str = "kth") -> np.ndarray:
     if method == "sum":
         return d.sum(axis=1)
     raise ValueError("unknown score method %r" % method)
+
+
+def abod(x, idx) -> np.ndarray:
+    """Angle-based outlier score (Section 4.3's ABOD built from the kNN and
+    cosine-similarity operators): for point i with neighbours N_k(i), the
+    mean over the unordered pairs {b, c} of distinct neighbours of the cosine
+    of the angle between x_b - x_i and x_c - x_i.  Differences, dot products
+    and norms in fp64, dot products summed over the columns in order; pairs
+    with a zero-length difference (a duplicate of x_i) are left out, and a
+    point without any pair left scores 0.  Higher means more outlying (the
+    neighbours lie in one direction)."""
+    x = np.asarray(x, dtype=np.float32).astype(np.float64)
+    idx = np.asarray(idx, dtype=np.int64)
+    n, k = idx.shape
+    out = np.zeros(n, dtype=np.float64)
+    for i in range(n):
+        v = x[idx[i]] - x[i]                       # k x d, exact differences
+        g = np.zeros((k, k), dtype=np.float64)
+        for t in range(v.shape[1]):                # column order, as the definition sums
+            g += np.outer(v[:, t], v[:, t])
+        total, count = 0.0, 0
+        for b in range(k):
+            for c in range(b + 1, k):
+                if g[b, b] > 0.0 and g[c, c] > 0.0:
+                    total += g[b, c] / np.sqrt(g[b, b] * g[c, c])
+                    count += 1
+        out[i] = total / count if count else 0.0
+    return out
 
 
 def knn_vote(idx, labels, n_classes: int) -> np.ndarray:

@@ -345,7 +345,7 @@ tod_status hip_fail(hipError_t e, const char* where) {
   return fail(TOD_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
 }
 
-// mode: 0 kNN lists / scores, 1 LOF, 2 classifier.
+// mode: 0 kNN lists / scores, 1 LOF, 2 classifier, 3 ABOD.
 tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d, int32_t k,
                const tod_options* opts_in, int32_t force_excl, int32_t mode, void* ws,
                size_t ws_bytes, void* stream, int64_t* idx_out, float* dist_out,
@@ -373,7 +373,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   const char* why = "";
   st = tod::make_plan(nq, nr, d, k, lof, self, o, &p, &why);
   if (st != TOD_OK) return fail(st, why);
-  if (mode == 2) p.lists = 1;
+  if (mode >= 2) p.lists = 1;
   const Layout L = tod::make_layout(p);
   if (ws_bytes < L.total)
     return fail(TOD_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) +
@@ -459,13 +459,17 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     he = tod::launch_lof(p, a, s);
     if (he != hipSuccess) return hip_fail(he, "lof launch");
   }
-  if (score_out && o.score != TOD_SCORE_KTH) {
+  if (score_out && o.score != TOD_SCORE_KTH && mode != 3) {
     he = tod::launch_score(p, a, s);
     if (he != hipSuccess) return hip_fail(he, "score launch");
   }
   if (mode == 2) {
     he = tod::launch_vote(p, a, s);
     if (he != hipSuccess) return hip_fail(he, "vote launch");
+  }
+  if (mode == 3) {
+    he = tod::launch_abod(p, a, s);
+    if (he != hipSuccess) return hip_fail(he, "abod launch");
   }
   hipEvent_t e_end = tm.mark(s);
   tod::Ctrl host;
@@ -747,6 +751,17 @@ tod_status tod_knn_classify(const float* xq, int64_t nq, const float* xr, int64_
     return fail(TOD_ERR_INVALID_ARG, "n_classes must be in [1, 65536]");
   return run(xq, nq, xr, nr, d, k, opts, 0, 2, workspace, ws_bytes, stream, nullptr, nullptr,
              nullptr, nullptr, labels_r, n_classes, pred_out, stats);
+}
+
+tod_status tod_abod(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
+                    void* workspace, size_t ws_bytes, void* stream, float* score_out,
+                    int64_t* idx_out, float* dist_out, tod_stats* stats) {
+  g_last_error.clear();
+  if (!score_out) return fail(TOD_ERR_INVALID_ARG, "null score output");
+  if (k < 2) return fail(TOD_ERR_INVALID_ARG, "ABOD needs k >= 2 (pairs of neighbours)");
+  if (k > 64) return fail(TOD_ERR_UNSUPPORTED, "ABOD supports k <= 64");
+  return run(x, n, x, n, d, k, opts, 1, 3, workspace, ws_bytes, stream, idx_out, dist_out,
+             score_out, nullptr, nullptr, 0, nullptr, stats);
 }
 
 size_t tod_nwr_workspace_size(int64_t nq, int64_t nr, int64_t d, const tod_options* opts) {

@@ -10,8 +10,10 @@
 //   vote   Appendix B's kNN classifier: the most frequent label among the k
 //          neighbours, ties going to the smallest label.  A label outside
 //          [0, n_classes) sets a flag the host turns into an error.
-// One thread per query row: O(k) and O(k^2) work per row on lists the
-// previous kernels just wrote (L2-resident).
+//   abod   Section 4.3's ABOD: the mean cosine over pairs of neighbours of
+//          the differences to them (abod_kernel below).
+// Scores and votes take one thread per query row: O(k) and O(k^2) work per
+// row on lists the previous kernels just wrote (L2-resident).
 #include "tod_internal.h"
 
 namespace tod {
@@ -74,7 +76,100 @@ vote_kernel(int64_t n, int k, int64_t nr, const int32_t* __restrict__ idx,
   pred[p] = best;
 }
 
+// ABOD as Section 4.3 builds it from the kNN and cosine-similarity operators:
+// for point i with neighbours b, c the cosine of the angle between
+// x_b - x_i and x_c - x_i, averaged over the unordered pairs of distinct
+// neighbours.  One wave per point: the Gram matrix of the k difference
+// vectors (k <= 64, b <= c: at most 2080 entries, 33 per lane) is summed in
+// fp64 over the columns in order, 16 columns at a time staged through LDS
+// as exact fp64 differences; then each lane turns its off-diagonal entries
+// into cosines (pairs with a zero-length difference are left out) and the
+// wave averages them.  A point without any pair left scores 0.
+constexpr int kAbodMaxK = 64;
+constexpr int kAbodCols = 16;
+constexpr int kAbodPer = (kAbodMaxK * (kAbodMaxK + 1) / 2 + 63) / 64;
+
+__global__ void __launch_bounds__(256)
+abod_kernel(int64_t n, int k, int d, const float* __restrict__ x, const int32_t* __restrict__ idx,
+            float* __restrict__ out, const Ctrl* ctrl) {
+#pragma clang fp contract(off)
+  __shared__ double diff[4][kAbodMaxK][kAbodCols];
+  __shared__ double norm[4][kAbodMaxK];
+  __shared__ uint32_t pairs[kAbodMaxK * (kAbodMaxK + 1) / 2];
+  if (ctrl->nonfinite) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int T = k * (k + 1) / 2;
+  // (b, c) of entry e, b <= c, row-major over the upper triangle.
+  for (int b = 0, e = 0; b < k; ++b)
+    for (int c = b; c < k; ++c, ++e)
+      if (e % 256 == (int)threadIdx.x % 256 && e < T) pairs[e] = ((uint32_t)b << 16) | (uint32_t)c;
+  __syncthreads();
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= n) return;  // uniform per wave; no block barrier follows
+  const int32_t* nb = idx + row * k;
+  const float* xi = x + row * (int64_t)d;
+  double acc[kAbodPer];
+#pragma unroll
+  for (int m = 0; m < kAbodPer; ++m) acc[m] = 0.0;
+  for (int t0 = 0; t0 < d; t0 += kAbodCols) {
+    for (int q = lane; q < k * kAbodCols; q += 64) {
+      const int b = q / kAbodCols, t = q % kAbodCols;
+      const int64_t j = nb[b];
+      diff[wave][b][t] = t0 + t < d ? (double)x[j * d + t0 + t] - (double)xi[t0 + t] : 0.0;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll
+    for (int m = 0; m < kAbodPer; ++m) {
+      const int e = lane + 64 * m;
+      if (e < T) {
+        const int b = (int)(pairs[e] >> 16), c = (int)(pairs[e] & 0xffff);
+        double s = acc[m];
+        for (int t = 0; t < kAbodCols; ++t) s = s + diff[wave][b][t] * diff[wave][c][t];
+        acc[m] = s;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  }
+#pragma unroll
+  for (int m = 0; m < kAbodPer; ++m) {
+    const int e = lane + 64 * m;
+    if (e < T && (pairs[e] >> 16) == (pairs[e] & 0xffff)) norm[wave][pairs[e] & 0xffff] = acc[m];
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  double sum = 0.0;
+  int cnt = 0;
+#pragma unroll
+  for (int m = 0; m < kAbodPer; ++m) {
+    const int e = lane + 64 * m;
+    if (e < T) {
+      const int b = (int)(pairs[e] >> 16), c = (int)(pairs[e] & 0xffff);
+      const double nbb = norm[wave][b], ncc = norm[wave][c];
+      if (b != c && nbb > 0.0 && ncc > 0.0) {
+        sum = sum + acc[m] / sqrt(nbb * ncc);
+        ++cnt;
+      }
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    sum = sum + __shfl_xor(sum, o, 64);
+    cnt += __shfl_xor(cnt, o, 64);
+  }
+  if (lane == 0) out[row] = (float)(cnt ? sum / (double)cnt : 0.0);
+}
+
 }  // namespace
+
+hipError_t launch_abod(const Plan& p, const Args& a, hipStream_t st) {
+  hipLaunchKernelGGL(abod_kernel, dim3((unsigned)((p.nq + 3) / 4)), dim3(256), 0, st, p.nq, p.k,
+                     (int)p.d, a.xq, (const int32_t*)a.idx32, a.score_out, (const Ctrl*)a.ctrl);
+  return hipGetLastError();
+}
 
 hipError_t launch_score(const Plan& p, const Args& a, hipStream_t st) {
   const unsigned g = (unsigned)((p.nq + kThreads - 1) / kThreads);

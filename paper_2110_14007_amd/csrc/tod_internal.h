@@ -176,6 +176,7 @@ hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t s);
 // from the exact lists.
 hipError_t launch_score(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_vote(const Plan& p, const Args& a, hipStream_t s);
+hipError_t launch_abod(const Plan& p, const Args& a, hipStream_t s);
 
 // Neighbours within range: fused MFMA tile with the range test (count pass:
 // candidates per (query, split); fill pass: their ids, in increasing j per

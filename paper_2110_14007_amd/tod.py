@@ -29,7 +29,8 @@ PRECISION_NAMES = {v: k for k, v in PRECISIONS.items()}
 SCORES = {"kth": 0, "largest": 0, "mean": 1, "median": 2, "sum": 3}
 
 SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
-           "tod_knn_decision", "tod_knn_classify", "tod_nwr_workspace_size", "tod_nwr", "tod_plan",
+           "tod_knn_decision", "tod_knn_classify", "tod_abod", "tod_nwr_workspace_size", "tod_nwr",
+           "tod_plan",
            "tod_status_string", "tod_last_error")
 
 
@@ -108,6 +109,8 @@ def _load():
     lib.tod_knn_classify.argtypes = [vp, i64, vp, i64, i64, i32, vp, i32, opt_p, vp, sz, vp, vp,
                                      st_p]
     lib.tod_knn_classify.restype = ctypes.c_int
+    lib.tod_abod.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, st_p]
+    lib.tod_abod.restype = ctypes.c_int
     lib.tod_nwr_workspace_size.argtypes = [i64, i64, i64, opt_p]
     lib.tod_nwr_workspace_size.restype = sz
     lib.tod_nwr.argtypes = [vp, i64, vp, i64, i64, ctypes.c_double, opt_p, vp, sz, vp, vp, i64, vp,
@@ -344,6 +347,26 @@ def tod_knn_classify(xq, xr, labels_r, k: int, n_classes: int, opts=None, worksp
                                ctypes.byref(stats) if stats is not None else None)
     _check(st, "tod_knn_classify")
     return pred
+
+
+def tod_abod(x, k: int, opts=None, workspace=None, stream=None, stats=None,
+             return_lists: bool = False):
+    """ABOD score (mean neighbour-pair cosine) of every row of x (self excluded)."""
+    torch = _torch()
+    _dev_matrix(x, "x")
+    n, d = x.shape
+    score = torch.empty((n,), dtype=torch.float32, device=x.device)
+    idx = dist = None
+    if return_lists:
+        idx = torch.empty((n, k), dtype=torch.int64, device=x.device)
+        dist = torch.empty((n, k), dtype=torch.float32, device=x.device)
+    need = tod_workspace_size(n, n, d, k, 1, opts)
+    wsbuf, wsp, wsn = _ws(workspace, need, x.device)
+    st = _lib.tod_abod(_p(x), n, d, int(k), ctypes.byref(opts) if opts is not None else None,
+                       wsp, wsn, _stream(stream), _p(score), _p(idx), _p(dist),
+                       ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_abod")
+    return (score, idx, dist) if return_lists else score
 
 
 def tod_nwr_workspace_size(nq: int, nr: int, d: int, opts=None) -> int:

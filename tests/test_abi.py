@@ -183,3 +183,15 @@ def test_score_and_classifier_entry_points_validate(tod):
     assert tod.tod_workspace_size(1000, 1000, 8, 5, 2) > base
     assert tod.tod_workspace_size(1000, 1000, 8, 5, 0, tod.options(score="median")) > base
     assert tod.tod_workspace_size(1000, 1000, 8, 5, 3) == 0
+
+
+def test_abod_entry_point_validates(tod):
+    lib = tod.raw_library()
+    assert lib.tod_abod(FAKE, 100, 8, 5, None, FAKE, 1 << 30, None, None, None, None,
+                        None) == tod.TOD_ERR_INVALID_ARG
+    assert lib.tod_abod(FAKE, 100, 8, 1, None, FAKE, 1 << 30, None, FAKE, None, None,
+                        None) == tod.TOD_ERR_INVALID_ARG
+    assert lib.tod_abod(FAKE, 100, 8, 65, None, FAKE, 1 << 30, None, FAKE, None, None,
+                        None) == tod.TOD_ERR_UNSUPPORTED
+    assert lib.tod_abod(FAKE, 100, 8, 5, None, FAKE, 100, None, FAKE, None, None,
+                        None) == tod.TOD_ERR_WORKSPACE

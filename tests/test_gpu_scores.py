@@ -132,3 +132,49 @@ def test_classifier_rejects_bad_labels(env):
     with pytest.raises(tod.TodError) as e:
         tod.tod_knn_classify(xr, xr, labels, 3, 3)
     assert e.value.status == tod.TOD_ERR_INVALID_ARG
+
+
+def _check_abod(env, x, k, allow_ties=True, **opt):
+    torch, tod, oracle = env
+    xd = torch.from_numpy(x).cuda()
+    s, idx, dist = tod.tod_abod(xd, k, tod.options(**opt), return_lists=True)
+    oidx, odist = oracle.knn_self(x, k)
+    _, exc = compare_knn(x, x, np.arange(len(x)), idx.cpu().numpy(), dist.cpu().numpy(), oidx,
+                         odist, allow_ties=allow_ties)
+    want = oracle.abod(x, oidx)
+    got = s.cpu().numpy().astype(np.float64)
+    # a mean of cosines in [-1, 1], computed in fp64 and rounded once to fp32
+    bad = [r for r in np.nonzero(np.abs(got - want) > 1e-6)[0] if r not in exc]
+    assert not bad, (bad[:5], got[bad[:5]], want[bad[:5]])
+    return got
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
+def test_abod_pins(env, prec):
+    x = workloads.line(10, 1)
+    got = _check_abod(env, x, 2, allow_ties=False, precision=prec)
+    np.testing.assert_array_equal(got, [1, -1, -1, -1, -1, -1, -1, -1, -1, 1])
+    got = _check_abod(env, x, 3, allow_ties=False, precision=prec)
+    np.testing.assert_allclose(got, [1] + [-1 / 3] * 8 + [1], atol=1e-7)
+    _check_abod(env, workloads.lattice(9, 2), 4, allow_ties=False, precision=prec)
+    xd = np.array([[0, 0], [0, 0], [1, 0], [-1, 0], [5, 5]], np.float32)
+    _check_abod(env, xd, 3, allow_ties=False, precision=prec)
+
+
+@pytest.mark.parametrize("n,d,k", [(2000, 16, 10), (3000, 32, 64), (1500, 200, 7),
+                                   (777, 512, 2)])
+def test_abod_against_oracle(env, n, d, k):
+    name = "C1" if d == 16 else ("C2" if d == 32 else "C4")
+    x, _ = workloads.generate(name, n=n)
+    x = np.ascontiguousarray(x[:, :d])
+    say("abod", n, d, k)
+    _check_abod(env, x, k)
+
+
+def test_abod_rejects_k(env):
+    torch, tod, _ = env
+    x = torch.from_numpy(workloads.line(100, 1)).cuda()
+    for k, status in ((1, tod.TOD_ERR_INVALID_ARG), (65, tod.TOD_ERR_UNSUPPORTED)):
+        with pytest.raises(tod.TodError) as e:
+            tod.tod_abod(x, k)
+        assert e.value.status == status

@@ -439,3 +439,56 @@ def test_vote_matches_counting_by_hand(oracle_mod):
             votes[int(labels[j])] = votes.get(int(labels[j]), 0) + 1
         top = max(votes.values())
         assert got[r] == min(c for c, n in votes.items() if n == top)
+
+
+# ---------------------------------------------------------------------------
+# ABOD as the paper builds it (Section 4.3): kNN, then the mean cosine
+# similarity of the difference vectors to each pair of neighbours.
+# ---------------------------------------------------------------------------
+
+def test_abod_line_closed_forms(oracle_mod):
+    # k = 2: an interior point has neighbours on both sides (cosine -1); an
+    # end point has both on one side (cosine 1).
+    x = workloads.line(10, 1)
+    idx, _ = oracle_mod.knn_self(x, 2)
+    np.testing.assert_array_equal(oracle_mod.abod(x, idx), [1, -1, -1, -1, -1, -1, -1, -1, -1, 1])
+    # k = 3: the ends see all three neighbours on one side; every other point
+    # has two on one side and one on the other: cosines (-1, -1, 1) -> -1/3.
+    idx, _ = oracle_mod.knn_self(x, 3)
+    np.testing.assert_allclose(oracle_mod.abod(x, idx), [1] + [-1 / 3] * 8 + [1], rtol=1e-15)
+
+
+def test_abod_lattice_closed_forms(oracle_mod):
+    x = workloads.lattice(9, 2)
+    idx, _ = oracle_mod.knn_self(x, 4)
+    s = oracle_mod.abod(x, idx)
+    # interior: four axis neighbours, 2 opposite pairs (-1) and 4 orthogonal (0)
+    # corner (0, 0): neighbours (0,1), (1,0), (1,1), (0,2) (the lower index of the
+    # tie at distance 2): cosines 0, 1/sqrt2, 1, 1/sqrt2, 0, 1/sqrt2
+    r2 = math.sqrt(2.0)
+    coords = x.astype(int).tolist()
+    for i, (r, c) in enumerate(coords):
+        if 1 <= r <= 7 and 1 <= c <= 7:
+            assert abs(s[i] + 1 / 3) <= 1e-15
+    assert abs(s[0] - (1 + 3 / r2) / 6) <= 1e-15
+
+
+def test_abod_invariances_and_duplicates(oracle_mod):
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((120, 5)).astype(np.float32)
+    idx, _ = oracle_mod.knn_self(x, 6)
+    s = oracle_mod.abod(x, idx)
+    # power-of-two scaling is exact and leaves every cosine unchanged; a row
+    # permutation permutes the scores
+    idx2, _ = oracle_mod.knn_self(x * 4, 6)
+    np.testing.assert_array_equal(idx2, idx)
+    np.testing.assert_allclose(oracle_mod.abod(x * 4, idx2), s, rtol=0, atol=1e-14)
+    perm = rng.permutation(len(x))
+    idx3, _ = oracle_mod.knn_self(x[perm], 6)
+    np.testing.assert_allclose(oracle_mod.abod(x[perm], idx3), s[perm], rtol=0, atol=1e-14)
+    assert np.all(np.abs(s) <= 1)
+    # a duplicate neighbour (zero-length difference) is left out of the pairs
+    xd = np.array([[0, 0], [0, 0], [1, 0], [-1, 0]], np.float32)
+    idx, _ = oracle_mod.knn_self(xd, 3)
+    assert idx[0].tolist() == [1, 2, 3]
+    assert oracle_mod.abod(xd, idx)[0] == -1.0  # only the pair (2, 3) counts
