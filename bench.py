@@ -2,8 +2,8 @@
 
 One step = one tod_lof call on the whole workload: prep, fused distance tiles
 with top-K' selection, certificate + exact recheck, fallback, kNN-OD score
-and LOF for every point (--detector knn: the kNN score alone; --detector abod:
-ABOD from the same lists).  Inputs are resident in HBM before timing starts.
+and LOF for every point (--detector knn: the kNN score alone; --detector abod
+or cof: ABOD or COF from the same lists).  Inputs are resident in HBM before timing starts.
 For a neighbours-within-range workload (--workload N1) one step is one
 tod_nwr call as the paper defines the operator (the indices of the pairs in
 range): prep, the range tile's count and fill passes, exact verification of
@@ -36,9 +36,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--precision", default="auto")
-    ap.add_argument("--detector", default="lof", choices=("lof", "knn", "abod"),
+    ap.add_argument("--detector", default="lof", choices=("lof", "knn", "abod", "cof"),
                     help="what one step computes on a kNN workload: LOF (with the kNN score, "
-                         "the default), the kNN score alone, or ABOD")
+                         "the default), the kNN score alone, ABOD or COF")
     ap.add_argument("--score", default="kth", choices=("kth", "mean", "median", "sum"),
                     help="kNN score of the step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -271,6 +271,8 @@ def main():
             tod.tod_lof(x, k, opts, workspace=ws, out=out, stats=st)
         elif args.detector == "knn":
             tod.tod_knn_score(x, k, opts, workspace=ws, stats=st)
+        elif args.detector == "cof":
+            tod.tod_cof(x, min(k, 63), opts, workspace=ws, stats=st)
         else:
             tod.tod_abod(x, min(k, 64), opts, workspace=ws, stats=st)
 

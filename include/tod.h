@@ -121,7 +121,7 @@ void tod_default_options(tod_options* opts);
 /*
  * Workspace bytes needed for these sizes and options by
  *   mode 0: tod_knn, tod_knn_score, tod_knn_decision (any query and reference sets);
- *   mode 1: tod_lof, tod_abod (X against itself, nq == nr);
+ *   mode 1: tod_lof, tod_abod, tod_cof (X against itself, nq == nr);
  *   mode 2: tod_knn_classify.
  * Returns 0 if the arguments are invalid or unsupported.
  */
@@ -208,6 +208,23 @@ tod_status tod_knn_classify(const float* xq, int64_t nq, const float* xr, int64_
 tod_status tod_abod(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
                     void* workspace, size_t ws_bytes, void* stream, float* score_out,
                     int64_t* idx_out, float* dist_out, tod_stats* stats);
+
+/*
+ * COF, the connectivity-based outlier factor (Tang et al.; Table 1), of
+ * every point of X (its own row excluded).  For point p and G = {p} plus its
+ * k nearest neighbours, the set-based nearest path starts from {p} and adds,
+ * k times, the point of G nearest to the points added so far (distance to a
+ * set = smallest distance to a member; ties to the lower row index); step i
+ * costs that distance c_i.  The average chaining distance is
+ *   ac(p) = sum_i 2 (k + 1 - i) / (k (k + 1)) c_i
+ * and COF(p) = (ac(p) + 1e-10) / (mean over the neighbours o of ac(o) + 1e-10)
+ * (fp64, rounded to fp32; the 1e-10 keeps duplicates finite, as LOF's does).
+ *   cof_out[n] fp32; knn_score_out, idx_out, dist_out optional as in tod_lof.
+ * Requires 1 <= k <= 63 (TOD_ERR_UNSUPPORTED above).  Workspace: mode 1.
+ */
+tod_status tod_cof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
+                   void* workspace, size_t ws_bytes, void* stream, float* cof_out,
+                   float* knn_score_out, int64_t* idx_out, float* dist_out, tod_stats* stats);
 
 /*
  * Host-only planner (Section 6 automatic batching): fills *plan with the

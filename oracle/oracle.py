@@ -14,6 +14,7 @@ Functions:
                                              k-th (default), mean, median or sum
   knn_vote(idx, labels, n_classes)        -> kNN classifier: majority label, ties to the smallest
   abod(x, idx)                            -> angle-based score: mean cosine over neighbour pairs
+  cof(x, idx)                             -> (cof, acdist): connectivity-based outlier factor
   nwr(xq, xr, phi, exclude_self, rows=None) -> (row_ptr int64 [m+1], idx int64, dist fp64):
                                              neighbours within range, CSR, ascending index
 """
@@ -153,6 +154,47 @@ def abod(x, idx) -> np.ndarray:
                     count += 1
         out[i] = total / count if count else 0.0
     return out
+
+
+def cof(x, idx):
+    """Connectivity-based outlier factor (Tang et al., one of Table 1's
+    proximity-based detectors), from the kNN lists.
+
+    For point p with neighbours N_k(p): the set-based nearest path over
+    G = {p} + N_k(p) starts from S = {p} and adds, k times, the point of G
+    outside S nearest to S (distance to a set = smallest distance to a
+    member; ties to the lower row index); the i-th step costs that
+    distance c_i.  The average chaining distance is
+        ac(p) = sum_i 2 (k + 1 - i) / (k (k + 1)) * c_i,
+    and COF(p) = (ac(p) + 1e-10) / (mean over o in N_k(p) of ac(o) + 1e-10)
+    (the 1e-10 keeps duplicates finite, as LOF's lrd does).  Squared
+    distances are the fp64 sums of the definition, compared squared, and
+    their square roots are the costs.  Returns (cof, ac), fp64."""
+    xd = np.asarray(x, dtype=np.float32).astype(np.float64)
+    idx = np.asarray(idx, dtype=np.int64)
+    n, k = idx.shape
+    ac = np.zeros(n, dtype=np.float64)
+    for p in range(n):
+        g = [p] + idx[p].tolist()
+        rows = xd[g]
+        d2 = np.zeros((k + 1, k + 1), dtype=np.float64)
+        for t in range(rows.shape[1]):  # every pair summed over the columns in order
+            e = rows[:, t][:, None] - rows[:, t][None, :]
+            d2 = d2 + e * e
+        in_s = [True] + [False] * k
+        best = [d2[0][j] for j in range(k + 1)]
+        total = 0.0
+        for i in range(1, k + 1):
+            cand = [j for j in range(k + 1) if not in_s[j]]
+            o = min(cand, key=lambda j: (best[j], g[j]))
+            total = total + 2.0 * (k + 1 - i) / (k * (k + 1)) * np.sqrt(best[o])
+            in_s[o] = True
+            for j in range(k + 1):
+                if not in_s[j] and d2[o][j] < best[j]:
+                    best[j] = d2[o][j]
+        ac[p] = total
+    mean_nb = np.array([sum(ac[o] for o in idx[p].tolist()) / k for p in range(n)])
+    return (ac + 1e-10) / (mean_nb + 1e-10), ac
 
 
 def knn_vote(idx, labels, n_classes: int) -> np.ndarray:

@@ -345,14 +345,14 @@ tod_status hip_fail(hipError_t e, const char* where) {
   return fail(TOD_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
 }
 
-// mode: 0 kNN lists / scores, 1 LOF, 2 classifier, 3 ABOD.
+// mode: 0 kNN lists / scores, 1 LOF, 2 classifier, 3 ABOD, 4 COF.
 tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d, int32_t k,
                const tod_options* opts_in, int32_t force_excl, int32_t mode, void* ws,
                size_t ws_bytes, void* stream, int64_t* idx_out, float* dist_out,
                float* score_out, float* lof_out, const int32_t* labels_r, int32_t n_classes,
                int32_t* pred_out, tod_stats* stats) {
   g_last_error.clear();
-  const int32_t lof = mode == 1 ? 1 : 0;
+  const int32_t lof = (mode == 1 || mode == 4) ? 1 : 0;  // COF uses LOF's buffers
   tod_options o;
   tod_status st = resolve_options(opts_in, &o);
   if (st != TOD_OK) return st;
@@ -455,9 +455,13 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   he = tod::launch_fallback(p, a, s);
   if (he != hipSuccess) return hip_fail(he, "fallback launch");
   hipEvent_t e_fb = tm.mark(s);
-  if (lof) {
+  if (mode == 1) {
     he = tod::launch_lof(p, a, s);
     if (he != hipSuccess) return hip_fail(he, "lof launch");
+  }
+  if (mode == 4) {
+    he = tod::launch_cof(p, a, s);
+    if (he != hipSuccess) return hip_fail(he, "cof launch");
   }
   if (score_out && o.score != TOD_SCORE_KTH && mode != 3) {
     he = tod::launch_score(p, a, s);
@@ -762,6 +766,16 @@ tod_status tod_abod(const float* x, int64_t n, int64_t d, int32_t k, const tod_o
   if (k > 64) return fail(TOD_ERR_UNSUPPORTED, "ABOD supports k <= 64");
   return run(x, n, x, n, d, k, opts, 1, 3, workspace, ws_bytes, stream, idx_out, dist_out,
              score_out, nullptr, nullptr, 0, nullptr, stats);
+}
+
+tod_status tod_cof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
+                   void* workspace, size_t ws_bytes, void* stream, float* cof_out,
+                   float* knn_score_out, int64_t* idx_out, float* dist_out, tod_stats* stats) {
+  g_last_error.clear();
+  if (!cof_out) return fail(TOD_ERR_INVALID_ARG, "null COF output");
+  if (k > 63) return fail(TOD_ERR_UNSUPPORTED, "COF supports k <= 63");
+  return run(x, n, x, n, d, k, opts, 1, 4, workspace, ws_bytes, stream, idx_out, dist_out,
+             knn_score_out, cof_out, nullptr, 0, nullptr, stats);
 }
 
 size_t tod_nwr_workspace_size(int64_t nq, int64_t nr, int64_t d, const tod_options* opts) {

@@ -12,8 +12,13 @@
 //          [0, n_classes) sets a flag the host turns into an error.
 //   abod   Section 4.3's ABOD: the mean cosine over pairs of neighbours of
 //          the differences to them (abod_kernel below).
+//   cof    Table 1's COF: average chaining distance of the set-based nearest
+//          path over the point and its neighbours, relative to the
+//          neighbours' (cof_ac_kernel, cof_kernel below).
 // Scores and votes take one thread per query row: O(k) and O(k^2) work per
 // row on lists the previous kernels just wrote (L2-resident).
+#include <math.h>
+
 #include "tod_internal.h"
 
 namespace tod {
@@ -163,7 +168,121 @@ abod_kernel(int64_t n, int k, int d, const float* __restrict__ x, const int32_t*
   if (lane == 0) out[row] = (float)(cnt ? sum / (double)cnt : 0.0);
 }
 
+// COF (Tang et al., Table 1): for point p and the point set G = {p} +
+// N_k(p), the set-based nearest path starts from S = {p} and adds, k times,
+// the point of G outside S nearest to S (ties to the lower row index); the
+// i-th step costs that distance c_i and the average chaining distance is
+// ac(p) = sum_i 2 (k + 1 - i) / (k (k + 1)) c_i.  One wave per point (lane l
+// stands for the l-th point of G): the squared distances of all pairs of G
+// (the fp64 column-ordered sums of the definition, at most 2016 pairs, 32 per
+// lane), then k steps of a wave-wide argmin over the points outside S.
+constexpr int kCofMaxK = 63;
+constexpr int kCofPer = ((kCofMaxK + 1) * kCofMaxK / 2 + 63) / 64;
+
+__global__ void __launch_bounds__(64)
+cof_ac_kernel(int64_t n, int k, int d, const float* __restrict__ x,
+              const int32_t* __restrict__ idx, double* __restrict__ ac, const Ctrl* ctrl) {
+#pragma clang fp contract(off)
+  __shared__ double rows[kCofMaxK + 1][kAbodCols];
+  __shared__ double d2m[kCofMaxK + 1][kCofMaxK + 2];
+  __shared__ uint32_t pairs[(kCofMaxK + 1) * kCofMaxK / 2];
+  if (ctrl->nonfinite) return;
+  const int lane = threadIdx.x;
+  const int64_t p = blockIdx.x;
+  const int m = k + 1;
+  const int T = m * (m - 1) / 2;
+  for (int b = 0, e = 0; b < m; ++b)
+    for (int c = b + 1; c < m; ++c, ++e)
+      if ((e & 63) == lane) pairs[e] = ((uint32_t)b << 16) | (uint32_t)c;
+  auto gid = [&](int l) -> int64_t { return l == 0 ? p : (int64_t)idx[p * k + l - 1]; };
+  double acc[kCofPer];
+#pragma unroll
+  for (int q = 0; q < kCofPer; ++q) acc[q] = 0.0;
+  for (int t0 = 0; t0 < d; t0 += kAbodCols) {
+    for (int q = lane; q < m * kAbodCols; q += 64) {
+      const int l = q / kAbodCols, t = q % kAbodCols;
+      rows[l][t] = t0 + t < d ? (double)x[gid(l) * d + t0 + t] : 0.0;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll
+    for (int q = 0; q < kCofPer; ++q) {
+      const int e = lane + 64 * q;
+      if (e < T) {
+        const int b = (int)(pairs[e] >> 16), c = (int)(pairs[e] & 0xffff);
+        double s = acc[q];
+        for (int t = 0; t < kAbodCols; ++t) {
+          const double df = rows[b][t] - rows[c][t];
+          s = s + df * df;
+        }
+        acc[q] = s;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  }
+#pragma unroll
+  for (int q = 0; q < kCofPer; ++q) {
+    const int e = lane + 64 * q;
+    if (e < T) {
+      const int b = (int)(pairs[e] >> 16), c = (int)(pairs[e] & 0xffff);
+      d2m[b][c] = acc[q];
+      d2m[c][b] = acc[q];
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  const bool live = lane < m;
+  bool in_s = lane == 0;
+  double best = live && lane > 0 ? d2m[0][lane] : INFINITY;
+  const uint32_t gl = live ? (uint32_t)gid(lane) : 0xffffffffu;
+  double total = 0.0;
+  for (int i = 1; i <= k; ++i) {
+    double kb = (live && !in_s) ? best : INFINITY;
+    uint32_t kg = (live && !in_s) ? gl : 0xffffffffu;
+    int kl = lane;
+    for (int o = 32; o > 0; o >>= 1) {
+      const double ob = __shfl_xor(kb, o, 64);
+      const uint32_t og = __shfl_xor(kg, o, 64);
+      const int ol = __shfl_xor(kl, o, 64);
+      if (ob < kb || (ob == kb && og < kg)) {
+        kb = ob;
+        kg = og;
+        kl = ol;
+      }
+    }
+    total = total + 2.0 * (double)(k + 1 - i) / (double)(k * (k + 1)) * sqrt(kb);
+    if (lane == kl) in_s = true;
+    if (live && !in_s && d2m[kl][lane] < best) best = d2m[kl][lane];
+  }
+  if (lane == 0) ac[p] = total;
+}
+
+__global__ void __launch_bounds__(kThreads)
+cof_kernel(int64_t n, int k, const int32_t* __restrict__ idx, const double* __restrict__ ac,
+           float* __restrict__ out, const Ctrl* ctrl) {
+#pragma clang fp contract(off)
+  if (ctrl->nonfinite) return;
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n) return;
+  double s = 0.0;
+  for (int r = 0; r < k; ++r) s = s + ac[idx[p * k + r]];
+  out[p] = (float)((ac[p] + 1e-10) / (s / (double)k + 1e-10));
+}
+
 }  // namespace
+
+hipError_t launch_cof(const Plan& p, const Args& a, hipStream_t st) {
+  hipLaunchKernelGGL(cof_ac_kernel, dim3((unsigned)p.nq), dim3(64), 0, st, p.nq, p.k, (int)p.d,
+                     a.xq, (const int32_t*)a.idx32, a.lrd, (const Ctrl*)a.ctrl);
+  hipLaunchKernelGGL(cof_kernel, dim3((unsigned)((p.nq + kThreads - 1) / kThreads)),
+                     dim3(kThreads), 0, st, p.nq, p.k, (const int32_t*)a.idx32,
+                     (const double*)a.lrd, a.lof_out, (const Ctrl*)a.ctrl);
+  return hipGetLastError();
+}
 
 hipError_t launch_abod(const Plan& p, const Args& a, hipStream_t st) {
   hipLaunchKernelGGL(abod_kernel, dim3((unsigned)((p.nq + 3) / 4)), dim3(256), 0, st, p.nq, p.k,

@@ -177,6 +177,8 @@ hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_score(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_vote(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_abod(const Plan& p, const Args& a, hipStream_t s);
+// COF: average chaining distances into lrd (fp64 [n]), COF into lof_out.
+hipError_t launch_cof(const Plan& p, const Args& a, hipStream_t s);
 
 // Neighbours within range: fused MFMA tile with the range test (count pass:
 // candidates per (query, split); fill pass: their ids, in increasing j per

@@ -29,7 +29,8 @@ PRECISION_NAMES = {v: k for k, v in PRECISIONS.items()}
 SCORES = {"kth": 0, "largest": 0, "mean": 1, "median": 2, "sum": 3}
 
 SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
-           "tod_knn_decision", "tod_knn_classify", "tod_abod", "tod_nwr_workspace_size", "tod_nwr",
+           "tod_knn_decision", "tod_knn_classify", "tod_abod", "tod_cof", "tod_nwr_workspace_size",
+           "tod_nwr",
            "tod_plan",
            "tod_status_string", "tod_last_error")
 
@@ -110,6 +111,8 @@ def _load():
                                      st_p]
     lib.tod_knn_classify.restype = ctypes.c_int
     lib.tod_abod.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, st_p]
+    lib.tod_cof.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, vp, st_p]
+    lib.tod_cof.restype = ctypes.c_int
     lib.tod_abod.restype = ctypes.c_int
     lib.tod_nwr_workspace_size.argtypes = [i64, i64, i64, opt_p]
     lib.tod_nwr_workspace_size.restype = sz
@@ -367,6 +370,27 @@ def tod_abod(x, k: int, opts=None, workspace=None, stream=None, stats=None,
                        ctypes.byref(stats) if stats is not None else None)
     _check(st, "tod_abod")
     return (score, idx, dist) if return_lists else score
+
+
+def tod_cof(x, k: int, opts=None, workspace=None, stream=None, stats=None,
+            return_lists: bool = False):
+    """COF of every row of x (self excluded) -> (cof fp32 [n], knn_score fp32 [n][, idx, dist])."""
+    torch = _torch()
+    _dev_matrix(x, "x")
+    n, d = x.shape
+    cof = torch.empty((n,), dtype=torch.float32, device=x.device)
+    score = torch.empty((n,), dtype=torch.float32, device=x.device)
+    idx = dist = None
+    if return_lists:
+        idx = torch.empty((n, k), dtype=torch.int64, device=x.device)
+        dist = torch.empty((n, k), dtype=torch.float32, device=x.device)
+    need = tod_workspace_size(n, n, d, k, 1, opts)
+    wsbuf, wsp, wsn = _ws(workspace, need, x.device)
+    st = _lib.tod_cof(_p(x), n, d, int(k), ctypes.byref(opts) if opts is not None else None,
+                      wsp, wsn, _stream(stream), _p(cof), _p(score), _p(idx), _p(dist),
+                      ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_cof")
+    return (cof, score, idx, dist) if return_lists else (cof, score)
 
 
 def tod_nwr_workspace_size(nq: int, nr: int, d: int, opts=None) -> int:

@@ -195,3 +195,13 @@ def test_abod_entry_point_validates(tod):
                         None) == tod.TOD_ERR_UNSUPPORTED
     assert lib.tod_abod(FAKE, 100, 8, 5, None, FAKE, 100, None, FAKE, None, None,
                         None) == tod.TOD_ERR_WORKSPACE
+
+
+def test_cof_entry_point_validates(tod):
+    lib = tod.raw_library()
+    assert lib.tod_cof(FAKE, 100, 8, 5, None, FAKE, 1 << 30, None, None, None, None, None,
+                       None) == tod.TOD_ERR_INVALID_ARG
+    assert lib.tod_cof(FAKE, 100, 8, 64, None, FAKE, 1 << 30, None, FAKE, None, None, None,
+                       None) == tod.TOD_ERR_UNSUPPORTED
+    assert lib.tod_cof(FAKE, 100, 8, 0, None, FAKE, 1 << 30, None, FAKE, None, None, None,
+                       None) == tod.TOD_ERR_INVALID_ARG

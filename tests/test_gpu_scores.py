@@ -178,3 +178,42 @@ def test_abod_rejects_k(env):
         with pytest.raises(tod.TodError) as e:
             tod.tod_abod(x, k)
         assert e.value.status == status
+
+
+def _check_cof(env, x, k, allow_ties=True, **opt):
+    torch, tod, oracle = env
+    xd = torch.from_numpy(x).cuda()
+    cof, score, idx, dist = tod.tod_cof(xd, k, tod.options(**opt), return_lists=True)
+    oidx, odist = oracle.knn_self(x, k)
+    _, exc = compare_knn(x, x, np.arange(len(x)), idx.cpu().numpy(), dist.cpu().numpy(), oidx,
+                         odist, allow_ties=allow_ties)
+    want, _ = oracle.cof(x, oidx)
+    # rows touched by an excused tie (their own list or a neighbour's) are excused
+    touched = set(exc)
+    for r in exc:
+        touched.update(np.nonzero((oidx == r).any(axis=1))[0].tolist())
+    compare_scores(cof.cpu().numpy(), want, np.arange(len(x)), touched, what="COF")
+    compare_scores(score.cpu().numpy(), odist[:, -1], np.arange(len(x)), set(exc),
+                   what="kNN score beside COF")
+    return cof.cpu().numpy()
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
+def test_cof_pins(env, prec):
+    x = np.array([[0], [1], [3], [6], [10]], np.float32)
+    got = _check_cof(env, x, 2, allow_ties=False, precision=prec)
+    np.testing.assert_allclose(got, [8 / 9, 8 / 9, 5 / 4, 5 / 4, 22 / 15], rtol=1e-6)
+    for x, k in ((workloads.line(10, 1), 3), (workloads.lattice(9, 2), 4)):
+        got = _check_cof(env, x, k, allow_ties=False, precision=prec)
+        np.testing.assert_allclose(got, 1.0, rtol=1e-6)
+    dup = np.zeros((6, 3), np.float32)
+    np.testing.assert_array_equal(_check_cof(env, dup, 3, allow_ties=False, precision=prec), 1.0)
+
+
+@pytest.mark.parametrize("n,d,k", [(2000, 16, 10), (1000, 32, 63), (800, 200, 5), (600, 512, 1)])
+def test_cof_against_oracle(env, n, d, k):
+    name = "C1" if d == 16 else ("C2" if d == 32 else "C4")
+    x, _ = workloads.generate(name, n=n)
+    x = np.ascontiguousarray(x[:, :d])
+    say("cof", n, d, k)
+    _check_cof(env, x, k)

@@ -492,3 +492,55 @@ def test_abod_invariances_and_duplicates(oracle_mod):
     idx, _ = oracle_mod.knn_self(xd, 3)
     assert idx[0].tolist() == [1, 2, 3]
     assert oracle_mod.abod(xd, idx)[0] == -1.0  # only the pair (2, 3) counts
+
+
+# ---------------------------------------------------------------------------
+# COF (Tang et al.; Table 1): set-based nearest path and average chaining
+# distance from the kNN lists.
+# ---------------------------------------------------------------------------
+
+def _cof_fixture():
+    out = {}
+    with open(os.path.join(os.path.dirname(__file__), "golden", "cof_gaps.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            name, *vals = line.split()
+            out[name] = [float(Fraction(v)) for v in vals]
+    return out
+
+
+def test_cof_golden_gaps(oracle_mod):
+    fx = _cof_fixture()
+    x = np.array(fx["x"], np.float32).reshape(-1, 1)
+    idx, _ = oracle_mod.knn_self(x, 2)
+    assert idx.tolist() == [[1, 2], [0, 2], [1, 0], [2, 4], [3, 2]]
+    cof, ac = oracle_mod.cof(x, idx)
+    np.testing.assert_allclose(ac, fx["ac"], rtol=1e-15)
+    np.testing.assert_allclose(cof, fx["cof"], rtol=1e-9)
+
+
+def test_cof_uniform_spacing_is_one(oracle_mod):
+    # Every step of every path costs 1 on an evenly spaced line and on the
+    # lattice interior, so ac = 1 (the weights sum to 1) and COF = 1.
+    for x, k in ((workloads.line(10, 1), 2), (workloads.line(10, 1), 3),
+                 (workloads.lattice(9, 2), 4)):
+        idx, _ = oracle_mod.knn_self(x, k)
+        cof, ac = oracle_mod.cof(x, idx)
+        np.testing.assert_allclose(ac, 1.0, rtol=1e-15)
+        np.testing.assert_allclose(cof, 1.0, rtol=1e-9)
+
+
+def test_cof_scaling_and_duplicates(oracle_mod):
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((150, 4)).astype(np.float32)
+    idx, _ = oracle_mod.knn_self(x, 5)
+    cof, ac = oracle_mod.cof(x, idx)
+    cof8, ac8 = oracle_mod.cof(x * 8, idx)  # distances scale exactly, ratios do not move
+    np.testing.assert_allclose(ac8, 8 * ac, rtol=1e-15)
+    np.testing.assert_allclose(cof8, cof, rtol=1e-9)
+    assert np.all(cof > 0)
+    dup = np.zeros((4, 2), np.float32)
+    idx, _ = oracle_mod.knn_self(dup, 3)
+    cof, ac = oracle_mod.cof(dup, idx)
+    assert np.all(ac == 0) and np.all(cof == 1.0)
