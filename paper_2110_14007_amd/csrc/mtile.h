@@ -261,9 +261,9 @@ __device__ __forceinline__ void merge_queues(uint64_t (&L)[R], const uint2* myq,
 template <int DPAD, bool FOLD>
 struct Layout {
   static constexpr int k16 = DPAD / 16;  // 16-wide k-steps
-  // LDS row stride: 32-byte rows are conflict-free as they are; longer rows
-  // get 16 bytes of padding so the eight rows of a read group hit distinct
-  // banks.
+  // LDS row stride: 32-byte rows are stored unpadded with their halves
+  // swizzled (swz); longer rows get 16 bytes of padding so the rows of a read
+  // group hit distinct banks.
   static constexpr int rowb = DPAD == 16 ? 32 : DPAD * 2 + 16;
   static constexpr int cpr = DPAD / 8;  // 16-byte chunks per row
   // Sub-tiles per stage: the stage pair, seeds and four queues stay under
@@ -274,6 +274,11 @@ struct Layout {
   static constexpr bool wide = DPAD >= 256;
   static_assert(!FOLD || DPAD == 16, "the folded seed uses the padding of 8-wide rows");
 };
+
+// Half swap of 32-byte staged rows: rows 4..7 and 8..11 of every 16 keep
+// their halves swapped, which spreads the first halves of any 8 or 16
+// consecutive rows over distinct LDS banks.
+__device__ __forceinline__ int swz(int r) { return ((r >> 2) ^ (r >> 3)) & 1; }
 
 // Stage buffers: rows of 512 elements are staged directly into LDS two
 // stages ahead (three buffers); other rows through registers (two buffers).
@@ -303,6 +308,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   constexpr bool kInterleave = NG == 1 && KC >= 16;
   constexpr int kAhead = 4;
   constexpr int ROWB = LY::rowb;
+  constexpr bool SWZ = ROWB == 32;
   constexpr int TR = 32 * NS;  // reference rows per stage
   constexpr int STAGE = TR * ROWB;
   constexpr int CPR = LY::cpr;
@@ -382,8 +388,12 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   float4 sth = make_float4(0.f, 0.f, 0.f, 0.f), suh = sth;
 
   // A fragment of sub-tile s, 16-wide k-step c: row col, elements 16c + 8h..+7.
+  // 32-byte rows store the two halves of row r swapped where bits 2 and 3 of
+  // r differ (swz), so that the 8 or 16 lanes served together by a 16-byte
+  // LDS read fall into distinct banks; the swap depends on col only.
+  const int ahalf = SWZ ? 16 * (h ^ swz(col)) : 16 * h;
   auto afrag = [&](const unsigned char* buf, int s, int c) {
-    return *reinterpret_cast<const V*>(buf + (32 * s + col) * ROWB + 32 * c + 16 * h);
+    return *reinterpret_cast<const V*>(buf + (32 * s + col) * ROWB + 32 * c + ahalf);
   };
   // Accumulator seeds of sub-tile s: -N_j/2 of rows 8g + 4h + 0..3 (plain
   // layout); zero in the fold layout, where the MFMA adds them.
@@ -405,12 +415,15 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     return v;
   };
   // Rows past the split and the query's own row (self exclusion) never survive.
-  // The row limit is one 32-bit value per sub-tile (rows >= lim are past the
-  // split), so the rare masking code keeps no 64-bit state per row.
-  auto mask = [&](f32x16& v, int64_t ts) {
-    const bool diag = selfq && ts == q0;
-    if (diag || ts + 32 > r_end) {
-      const int lim = ts + 32 > r_end ? (int)(r_end - ts) : 32;
+  // Row indices fit in 32 bits (at most 2^31 - 1 rows), so the tests are
+  // 32-bit scalar compares; the row limit is one value per sub-tile (rows >=
+  // lim are past the split).
+  const uint32_t q0u = (uint32_t)q0, endu = (uint32_t)r_end;
+  auto mask = [&](f32x16& v, uint32_t ts) {
+    const bool diag = selfq && ts == q0u;
+    const uint32_t rem = ts < endu ? endu - ts : 0u;
+    if (diag || rem < 32u) {
+      const int lim = rem < 32u ? (int)rem : 32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = out_row(r, h);
@@ -446,7 +459,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // An append writes the next free slot unconditionally and advances the
   // count only for a survivor (no exec-mask branch per value); the room made
   // beforehand keeps every written slot inside the queue.
-  auto insert = [&](const f32x16& v, int64_t ts) __attribute__((always_inline)) {
+  auto insert = [&](const f32x16& v, uint32_t ts) __attribute__((always_inline)) {
     if constexpr (kQCap == 16) {
 #pragma unroll 1
       for (int hf = 0; hf < 2; ++hf) {
@@ -497,90 +510,99 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
     const int c = tid + i * NT;                                                             \
     if (CHUNKS % NT == 0 || c < CHUNKS)                                                     \
-      *reinterpret_cast<uint4*>(stage + (B) * STAGE + (c / CPR) * ROWB + (c % CPR) * 16) =    \
-          REG[i];                                                                           \
+      *reinterpret_cast<uint4*>(stage + (B) * STAGE + (c / CPR) * ROWB +                      \
+                                ((c % CPR) ^ (SWZ ? swz(c / CPR) : 0)) * 16) = REG[i];      \
   }                                                                                         \
   if (!FOLD && tid < TR / 4) *reinterpret_cast<float4*>(hnb + (B) * TR + 4 * tid) = REGH;
 
   // One stage: its sub-tiles from LDS buffer b.
   auto stage_body = [&](int64_t t0, int b) __attribute__((always_inline)) {
-      const unsigned char* buf = stage + b * STAGE;
-      const float* hn = hnb + b * TR;
-      if (active) {
-        const int live = r_end - t0 < TR ? (int)((r_end - t0 + 31) >> 5) : NS;
-  #pragma unroll 1
-        for (int g0 = 0; g0 < live; g0 += NG) {
-          // Fast path: NG sub-tiles at once (independent MFMA chains, one
-          // reduction), with no insertion code.
-          // All A fragments and seeds of the group are read before the first
-          // MFMA, so that one LDS round trip covers the group's MFMA chains.
-          // Long rows (one wave per SIMD, nothing else to overlap with) keep
-          // kAhead fragments in flight ahead of the MFMA chain instead: the
-          // LDS reads of later k-steps then run under the MFMAs of earlier ones.
-          V af[NG][KC];
-          f32x16 acc[NG];
-  #pragma unroll
-          for (int s = 0; s < NG; ++s) {
-  #pragma unroll
-            for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
-            acc[s] = seed(hn, g0 + s);
-          }
-  #pragma unroll
-          for (int c = 0; c < KC; ++c)
-  #pragma unroll
-            for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(af[s][c], bq[c], acc[s]);
-          if constexpr (kInterleave) {
-            __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
-  #pragma unroll
-            for (int c = 0; c < KC - kAhead; ++c) {
-              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
-          } else {
-            __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
-          }
-          float ms[NG];
-  #pragma unroll
-          for (int s = 0; s < NG; ++s) {
-            mask(acc[s], t0 + 32 * (g0 + s));
-            ms[s] = max16(acc[s]);  // sub-tiles past the split are fully masked
-          }
-          float m = ms[0];
-  #pragma unroll
-          for (int s = 1; s < NG; ++s) m = max3f(m, ms[s], ms[s]);
-          if (__ballot(m > thr)) {
-            // Slow path: sub-tile by sub-tile (one copy of the insertion and
-            // merge code).  Rows of several k-steps reuse the accumulators the
-            // fast path computed; one-step rows recompute them (one MFMA),
-            // which keeps the fast path's registers free.
-            const int gl = live - g0 < NG ? live - g0 : NG;
-  #pragma unroll 1
-            for (int s = 0; s < gl; ++s) {
-              float msel = ms[0];
-  #pragma unroll
-              for (int u = 1; u < NG; ++u) msel = s == u ? ms[u] : msel;
-              if (!__ballot(msel > thr)) continue;
-              const int64_t ts = t0 + 32 * (g0 + s);
-              if constexpr (NG == 1) {
-                insert(acc[0], ts);
-              } else if constexpr (KC >= 2) {
-                f32x16 a1 = acc[0];
-  #pragma unroll
-                for (int u = 1; u < NG; ++u)
-                  if (s == u) a1 = acc[u];
-                insert(a1, ts);
-              } else {
-                f32x16 a1 = seed(hn, g0 + s);
-                a1 = mfma<ET>(afrag(buf, g0 + s, 0), bq[0], a1);
-                mask(a1, ts);
-                insert(a1, ts);
-              }
-            }
-          }
+    const unsigned char* buf = stage + b * STAGE;
+    const float* hn = hnb + b * TR;
+    if (!active) return;
+    const uint32_t t0u = (uint32_t)t0;
+    const uint32_t avail = endu - t0u;  // every scanned stage starts below r_end
+    const int live = avail < (uint32_t)TR ? (int)((avail + 31) >> 5) : NS;
+    // Only a stage holding the diagonal sub-tile or the split's end needs the
+    // masking code; the test is made once per stage, on scalars.
+    const bool smask = (selfq && q0u - t0u < (uint32_t)TR) || avail < (uint32_t)TR;
+    // Fast path over NG sub-tiles (independent MFMA chains, one reduction),
+    // with no insertion code.  All A fragments and seeds of the group are read
+    // before the first MFMA, so that one LDS round trip covers the group's
+    // MFMA chains.  Long rows (one wave per SIMD, nothing else to overlap
+    // with) keep kAhead fragments in flight ahead of the MFMA chain instead:
+    // the LDS reads of later k-steps then run under the MFMAs of earlier ones.
+    auto group = [&](int g0) __attribute__((always_inline)) {
+      V af[NG][KC];
+      f32x16 acc[NG];
+#pragma unroll
+      for (int s = 0; s < NG; ++s) {
+#pragma unroll
+        for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
+        acc[s] = seed(hn, g0 + s);
+      }
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+#pragma unroll
+        for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(af[s][c], bq[c], acc[s]);
+      if constexpr (kInterleave) {
+        __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
+#pragma unroll
+        for (int c = 0; c < KC - kAhead; ++c) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
+      }
+      // Masks first (one branch per group), then the NG independent max
+      // trees, which the scheduler interleaves.
+      if (smask) {
+#pragma unroll
+        for (int s = 0; s < NG; ++s) mask(acc[s], t0u + 32u * (uint32_t)(g0 + s));
+      }
+      float ms[NG];
+#pragma unroll
+      for (int s = 0; s < NG; ++s) ms[s] = max16(acc[s]);  // past the split: fully masked
+      float m = ms[0];
+#pragma unroll
+      for (int s = 1; s < NG; s += 2) m = max3f(m, ms[s], ms[s + 1 < NG ? s + 1 : s]);
+      if (!__ballot(m > thr)) return;
+      // Slow path: sub-tile by sub-tile (one copy of the insertion and merge
+      // code).  With one sub-tile per group the accumulators are reused;
+      // otherwise the sub-tile is recomputed (KC MFMAs, bit-identical), which
+      // keeps the fast path's accumulators dead after their reduction.
+      const int gl = live - g0 < NG ? live - g0 : NG;
+#pragma unroll 1
+      for (int s = 0; s < gl; ++s) {
+        float msel = ms[0];
+#pragma unroll
+        for (int u = 1; u < NG; ++u) msel = s == u ? ms[u] : msel;
+        if (!__ballot(msel > thr)) continue;
+        uint32_t ts = t0u + 32u * (uint32_t)(g0 + s);
+        // Opaque to the optimizer: otherwise it carries the 16 row ids
+        // ts + out_row(r, h) through the fast path as per-lane induction
+        // variables (16 additions per sub-tile) instead of forming them here.
+        asm volatile("" : "+s"(ts));
+        if constexpr (NG == 1) {
+          insert(acc[0], ts);
+        } else {
+          f32x16 a1 = seed(hn, g0 + s);
+#pragma unroll
+          for (int c = 0; c < KC; ++c) a1 = mfma<ET>(afrag(buf, g0 + s, c), bq[c], a1);
+          if (smask) mask(a1, ts);
+          insert(a1, ts);
         }
       }
+    };
+    if constexpr (NG == NS) {
+      group(0);
+    } else {
+#pragma unroll 1
+      for (int g0 = 0; g0 < live; g0 += NG) group(g0);
+    }
   };
 
   // Stage order.  With the grouped scan order (X against X, one split) the
@@ -684,7 +706,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 }
 
 template <typename ET, int DPAD, bool FOLD, int R, int W = 4, int NS = Layout<DPAD, FOLD>::ns,
-          int NG = (DPAD <= 32 ? 2 : 1)>
+          int NG = (DPAD <= 32 ? NS : 1)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st) {
   const size_t lds = lds_bytes(DPAD, FOLD, W, NS, queue_cap<R>());
