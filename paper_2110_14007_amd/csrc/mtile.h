@@ -295,11 +295,18 @@ __host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int n
 // At least two waves per SIMD for lists of up to 32 entries and rows of up to
 // 128 elements: the register budget then stays within 256 per lane, which
 // lets the compiler keep the MFMA accumulators in VGPRs (no AGPR copies
-// around every sub-tile).  64-entry lists and wider rows need more registers
-// and run one wave per SIMD.
+// around every sub-tile).  16-entry lists on 16-element rows fit three waves
+// (at most 168 registers; their 48 KiB of LDS also admits three workgroups
+// per CU).  64-entry lists and wider rows need more registers and run one
+// wave per SIMD.
+template <int DPAD, int R>
+__host__ __device__ constexpr int min_waves() {
+  return R >= 32 || DPAD >= 256 ? 1 : (DPAD == 16 && R <= 8 ? 3 : 2);
+}
+
 template <typename ET, int DPAD, bool FOLD, int R, int W, int NS, int NG>
 __global__ void __launch_bounds__(W * 64)
-    __attribute__((amdgpu_waves_per_eu(R >= 32 || DPAD >= 256 ? 1 : 2)))
+    __attribute__((amdgpu_waves_per_eu(min_waves<DPAD, R>())))
 mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   using V = typename Frag<ET>::V;
   using LY = Layout<DPAD, FOLD>;
@@ -705,8 +712,10 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   }
 }
 
+// Sub-tiles per fast-path group: four for rows of up to 32 elements (one
+// k-step or two), one otherwise.
 template <typename ET, int DPAD, bool FOLD, int R, int W = 4, int NS = Layout<DPAD, FOLD>::ns,
-          int NG = (DPAD <= 32 ? NS : 1)>
+          int NG = (DPAD <= 32 ? 4 : 1)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st) {
   const size_t lds = lds_bytes(DPAD, FOLD, W, NS, queue_cap<R>());
