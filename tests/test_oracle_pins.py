@@ -3,6 +3,7 @@ exact rational brute force, closed forms and invariances, never against
 itself or the HIP path."""
 import math
 import os
+import statistics
 from fractions import Fraction
 
 import numpy as np
@@ -544,3 +545,130 @@ def test_cof_scaling_and_duplicates(oracle_mod):
     idx, _ = oracle_mod.knn_self(dup, 3)
     cof, ac = oracle_mod.cof(dup, idx)
     assert np.all(ac == 0) and np.all(cof == 1.0)
+
+
+# ---------------------------------------------------------------------------
+# LOCI (Papadimitriou et al.; Table 1): counting and sampling neighbourhoods at
+# a ladder of radii, MDEF and its normalised deviation.
+# ---------------------------------------------------------------------------
+
+def _golden_value(v):
+    if v.startswith("sqrt:"):
+        return math.sqrt(float(Fraction(v[5:])))
+    return float(Fraction(v))
+
+
+def _loci_fixture():
+    rows, scores = [], {}
+    with open(os.path.join(os.path.dirname(__file__), "golden", "loci_line10.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            t = line.split()
+            if t[0] == "score":
+                scores[int(t[1])] = _golden_value(t[2])
+            else:
+                rows.append((int(t[0]), float(t[1]), int(t[2]), int(t[3]),
+                             _golden_value(t[4]), _golden_value(t[5])))
+    return rows, scores
+
+
+def test_loci_golden_line(oracle_mod):
+    rows, scores = _loci_fixture()
+    radii = [1.0, 2.0, 4.0]
+    r = oracle_mod.loci(workloads.line(10, 1), radii, alpha=0.5, n_min=1, k_sigma=3.0)
+    for p, rad, na, nr, mdef, smdef in rows:
+        li = radii.index(rad)
+        for row in (p, 9 - p):  # the line is symmetric
+            assert r["n_alpha"][row, li] == na and r["n_r"][row, li] == nr, (row, rad)
+            assert abs(r["mdef"][row, li] - mdef) <= 1e-15 * max(1.0, abs(mdef)), (row, rad)
+            assert abs(r["sigma_mdef"][row, li] - smdef) <= 1e-15, (row, rad)
+    for p, v in scores.items():
+        for row in (p, 9 - p):
+            assert abs(r["score"][row] - v) <= 1e-14 * max(1.0, abs(v)), row
+    assert not r["flag"].any()
+
+
+def _loci_by_sets(x, radii, alpha, n_min, k_sigma):
+    # The definition read directly: explicit neighbour sets per point and
+    # radius, the sample mean and the population standard deviation of the
+    # counting-neighbourhood sizes taken with the statistics module (two-pass),
+    # squared distances as plain Python float sums over the columns.
+    n = len(x)
+    pts = [[float(v) for v in row] for row in x]
+
+    def d2(p, q):
+        s = 0.0
+        for a, b in zip(pts[p], pts[q]):
+            s = s + (a - b) * (a - b)
+        return s
+
+    dd = [[d2(p, q) for q in range(n)] for p in range(n)]
+    out = []
+    for p in range(n):
+        per = []
+        for r in radii:
+            ra = alpha * r
+            samp = [q for q in range(n) if dd[p][q] <= r * r]
+            cnt = {q: sum(1 for o in range(n) if dd[q][o] <= ra * ra) for q in samp}
+            vals = [cnt[q] for q in samp]
+            nh = statistics.mean(vals)
+            sd = statistics.pstdev(vals)
+            na = sum(1 for o in range(n) if dd[p][o] <= ra * ra)
+            per.append((na, len(samp), 1.0 - na / nh, sd / nh))
+        counted = [v for v in per if v[1] >= n_min]
+        ratios = [(v[2] / v[3]) if v[3] > 0 else 0.0 for v in counted]
+        score = max(ratios) if ratios else 0.0
+        flag = any(v[2] > k_sigma * v[3] for v in counted)
+        out.append((per, score, flag))
+    return out
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_loci_brute_force_sets(oracle_mod, seed):
+    rng = np.random.default_rng(100 + seed)
+    # two blobs and a few stragglers, with repeated points (ties on the radii)
+    x = np.concatenate([rng.integers(0, 4, (20, 2)), rng.integers(8, 11, (14, 2)),
+                        rng.integers(-9, 20, (6, 2))]).astype(np.float32)
+    radii, alpha, n_min, ks = [1.0, 2.0, 3.0, 5.0, 8.0], 0.5, 4, 2.0
+    r = oracle_mod.loci(x, radii, alpha, n_min, ks)
+    ref = _loci_by_sets(x, radii, alpha, n_min, ks)
+    for p, (per, score, flag) in enumerate(ref):
+        for li, (na, nr, mdef, smdef) in enumerate(per):
+            assert r["n_alpha"][p, li] == na and r["n_r"][p, li] == nr, (p, li)
+            assert abs(r["mdef"][p, li] - mdef) <= 1e-12 * max(1.0, abs(mdef)), (p, li)
+            assert abs(r["sigma_mdef"][p, li] - smdef) <= 1e-12, (p, li)
+        assert abs(r["score"][p] - score) <= 1e-12 * max(1.0, abs(score)), p
+        assert bool(r["flag"][p]) == flag, p
+    assert r["flag"].any() and not r["flag"].all()
+
+
+def test_loci_isolated_point_flagged(oracle_mod):
+    # A 5 x 6 unit lattice (diameter sqrt(41)) and one point at (14, 15), at
+    # least sqrt(200) from every lattice point and at most sqrt(421) < 21 from
+    # any.  At r = 21 the lone point samples all 31 points; every counting
+    # neighbourhood (alpha r = 10.5) of a lattice point holds the 30 lattice
+    # points, the lone point's holds itself.
+    lat = workloads.lattice(6, 2)[:30]
+    x = np.concatenate([lat, [[14.0, 15.0]]]).astype(np.float32)
+    r = oracle_mod.loci(x, [21.0], alpha=0.5, n_min=20, k_sigma=3.0)
+    assert r["n_alpha"][30, 0] == 1 and r["n_r"][30, 0] == 31
+    assert r["flag"][30] and not r["flag"][:30].any()
+    # n_hat = (30 * 30 + 1) / 31, MDEF = 1 - 31 / 901 for the lone point
+    assert abs(r["mdef"][30, 0] - (1.0 - 31.0 / 901.0)) < 1e-15
+
+
+def test_loci_scaling_and_permutation(oracle_mod):
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal((120, 3)).astype(np.float32)
+    radii = [0.5, 0.8, 1.2, 1.9]
+    r = oracle_mod.loci(x, radii, alpha=0.5, n_min=5, k_sigma=2.5)
+    # power-of-two scaling of points and radii moves no squared distance or
+    # threshold off its scaled value: every output is identical
+    r4 = oracle_mod.loci(x * 4, [4 * v for v in radii], alpha=0.5, n_min=5, k_sigma=2.5)
+    for key in r:
+        np.testing.assert_array_equal(r4[key], r[key])
+    perm = rng.permutation(120)
+    rp = oracle_mod.loci(x[perm], radii, alpha=0.5, n_min=5, k_sigma=2.5)
+    for key in r:
+        np.testing.assert_array_equal(rp[key], r[key][perm])
