@@ -7,7 +7,9 @@ or cof: ABOD or COF from the same lists).  Inputs are resident in HBM before tim
 For a neighbours-within-range workload (--workload N1) one step is one
 tod_nwr call as the paper defines the operator (the indices of the pairs in
 range): prep, the range tile's count and fill passes, exact verification of
-the uncertain pairs and the CSR output.
+the uncertain pairs and the CSR output.  For the LOCI workload (--workload L1)
+one step is one tod_loci call: neighbours within the largest radius, then the
+per-radius neighbourhood counts, sums, MDEF, score and flag of every point.
 
 Prints ONE JSON line (see the design doc for the field definitions).
 """
@@ -27,6 +29,7 @@ METRIC = "kNN-OD scored points/sec and distance-pairs/sec (1 MI355X); % of MFMA/
 # Peaks used for the roofline fraction (MI355X: 256 CUs x 4 SIMD, 2.4 GHz).
 PEAK_MFMA_F16 = 2500.0      # TFLOP/s, dense fp16 / bf16 MFMA
 PEAK_VALU_F32 = 157.3       # TFLOP/s, published fp32 vector peak (packed FMA)
+PEAK_HBM_GBS = 8000.0       # GB/s, HBM3E
 
 
 def parse():
@@ -239,6 +242,114 @@ def bench_nwr(args, w):
     print(json.dumps(line), flush=True)
 
 
+def cpu_baseline_loci(x, p, target_s):
+    """The oracle's LOCI on a bounded sample: the first m rows of the workload
+    taken as a point set of their own (LOCI of n points costs O(n^2) pairs,
+    so the oracle's pair rate divided by the workload's n is its point rate
+    on the whole workload)."""
+    from oracle import oracle
+    n = x.shape[0]
+    m, t = 2000, 0.0
+    while True:
+        t0 = time.perf_counter()
+        oracle.loci(x[:m], p["radii"], p["alpha"], p["n_min"], p["k_sigma"])
+        t = time.perf_counter() - t0
+        if t >= target_s / 4 or m >= min(n, 12000):
+            break
+        m = min(2 * m, n, 12000)
+    pairs_s = float(m) * float(m) / t
+    return {
+        "value": pairs_s / n,
+        "unit": "points/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "numpy fp64 LOCI of the first %d rows as their own point set (%.3g pairs in "
+                  "%.1f s = %.3g pairs/s), divided by n = %d pairs per point"
+                  % (m, float(m) * m, t, pairs_s, n),
+    }
+
+
+def bench_loci(args, w):
+    """One step = one tod_loci call: neighbours within the largest radius
+    (prep, range tile count and fill passes, exact verification, CSR), then
+    the LOCI count and sum kernels."""
+    import numpy as np
+    import torch
+
+    from paper_2110_14007_amd import tod, workloads
+
+    x_host, _ = workloads.generate(w.name)
+    n, d = x_host.shape
+    p = w.extra
+    x = torch.from_numpy(x_host).to("cuda:0")
+    opts = tod.options(precision=args.precision)
+    ws = tod.Workspace()
+    st = tod.new_stats()
+    tod.tod_loci(x, p["radii"], p["alpha"], p["n_min"], p["k_sigma"], opts, workspace=ws,
+                 stats=st)  # sizes the workspace
+    cap = int(st.pairs_in_range)
+
+    def step(s=None):
+        return tod.tod_loci(x, p["radii"], p["alpha"], p["n_min"], p["k_sigma"], opts,
+                            capacity=cap, grow=False, workspace=ws, stats=s)
+
+    for _ in range(max(args.warmup - 1, 0)):
+        step()
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        s = tod.new_stats()
+        step(s)
+        stats.append(s.as_dict())
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    def avg(key):
+        return float(np.mean([s[key] for s in stats]))
+
+    prec = stats[0]["precision"]
+    nl = len(p["radii"])
+    nls = 8 if nl <= 8 else (16 if nl <= 16 else 32)
+    pairs = float(stats[0]["pairs_in_range"])
+    # Algorithmic HBM bytes of the two LOCI kernels: each reads the pair ids
+    # (8 B) and the radius index (1 B, written by the first); the count tables
+    # (2 x n x nls int32) are written once and read once.  The rows and the
+    # count rows gathered per pair are cache-resident (x: 16 n B, table: 4 n nls B).
+    loci_bytes = pairs * (8 + 1) * 2 + pairs * 1 + 2.0 * n * nls * 4 * 2
+    loci_ms = avg("ms_score")
+    achieved = loci_bytes / (loci_ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(n / (ms_step * 1e-3), 1),
+        "unit": "points/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "%s+f64" % prec.replace("fp", "f"),
+        "data": "synthetic",
+        "config": {"workload": "%s: %s" % (w.name, w.description), "n": n, "d": d,
+                   "radii": [round(r, 6) for r in p["radii"]], "alpha": p["alpha"],
+                   "n_min": p["n_min"], "k_sigma": p["k_sigma"], "filter_precision": prec,
+                   "parallelism": "single GPU"},
+        "pairs_per_s": float(n) * float(n) / (ms_step * 1e-3),
+        "pairs_in_range": int(pairs),
+        "phase_ms": {key: round(avg(key), 4) for key in ("ms_prep", "ms_tile", "ms_recheck",
+                                                         "ms_score", "ms_total")},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": None, "kernel": "loci_count+loci_sum", "launch_ms": round(loci_ms, 4)},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_loci(x_host, p, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -256,6 +367,9 @@ def main():
     w = workloads.WORKLOADS[args.workload]
     if w.name.startswith("N"):
         bench_nwr(args, w)
+        return
+    if w.name.startswith("L"):
+        bench_loci(args, w)
         return
     x_host, _ = workloads.generate(args.workload)
     n, d, k = x_host.shape[0], x_host.shape[1], w.k

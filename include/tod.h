@@ -54,8 +54,8 @@ typedef enum {
   TOD_ERR_UNSUPPORTED = 4, /* k > 256, d > 4096, or more than 2^31 - 1 rows */
   TOD_ERR_HIP = 5,         /* a HIP launch or runtime call failed; see tod_last_error() */
   TOD_ERR_INTERNAL = 6,
-  TOD_ERR_CAPACITY = 7     /* tod_nwr: more pairs in range than the output capacity (the row
-                            * offsets and the total are still written) */
+  TOD_ERR_CAPACITY = 7     /* tod_nwr, tod_loci: more pairs in range than the output capacity
+                            * (tod_nwr still writes the row offsets and the total) */
 } tod_status;
 
 /* Precision of the shortlist filter (the exact recheck always works from the
@@ -273,6 +273,56 @@ tod_status tod_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
                    double phi, const tod_options* opts, void* workspace, size_t ws_bytes,
                    void* stream, int64_t* row_ptr_out, int64_t capacity, int64_t* idx_out,
                    float* dist_out, int64_t* total_out, tod_stats* stats);
+
+/*
+ * LOCI, the multi-granularity deviation factor of Papadimitriou et al.
+ * (one of Table 1's proximity-based detectors; like LOF it is built on
+ * neighbours within range, Section 5.3), at a ladder of sampling radii
+ * r_0 < r_1 < ... < r_{L-1}.  For every row p of X and every radius r_l:
+ *   n_alpha[p][l] = |{q : d(p, q) <= alpha r_l}|  (counting neighbourhood)
+ *   n_r[p][l]     = |{q : d(p, q) <= r_l}|        (sampling neighbourhood)
+ * (p itself belongs to both); n_hat and sigma are the mean and the population
+ * standard deviation of n_alpha[q][l] over q in the sampling neighbourhood,
+ *   MDEF = 1 - n_alpha[p][l] / n_hat,   sigma_MDEF = sigma / n_hat.
+ * Membership is exact, as in tod_nwr: d(p, q) <= r iff the fp64 squared
+ * distance summed over the columns in order is <= fl(r * r), and
+ * d(p, q) <= alpha r iff it is <= fl(fl(alpha * r)^2).  The neighbourhood
+ * sums S1 = sum n_alpha[q][l] and S2 = sum n_alpha[q][l]^2 are exact 64-bit
+ * integers; then, in fp64 and in this order, n_hat = S1 / n_r,
+ * var = S2 / n_r - n_hat * n_hat (negative values become 0),
+ * sigma = sqrt(var), MDEF, sigma_MDEF.  A radius counts for p when
+ * n_r[p][l] >= n_min.  flag_out[p] = 1 when MDEF > k_sigma * sigma_MDEF at a
+ * counted radius; score_out[p] = the largest MDEF / sigma_MDEF over the
+ * counted radii, where a radius with sigma_MDEF = 0 (all samples equal, so
+ * MDEF = 0) contributes 0, and 0 when no radius counts.
+ *   radii               HOST array [n_radii] fp64, strictly increasing, >= 0,
+ *                       finite; 1 <= n_radii <= 32.
+ *   alpha               in (0, 1]; n_min >= 1; k_sigma finite, >= 0.
+ *   capacity            pairs (p, q) with d(p, q) <= r_{L-1}, self pairs
+ *                       included, that the workspace holds.  If more are in
+ *                       range the call returns TOD_ERR_CAPACITY and, when
+ *                       stats is given, stats->pairs_in_range = the number
+ *                       needed (size the workspace for it and call again).
+ *   score_out[n]        fp64 (device).
+ *   flag_out[n]         int32 (device), nullable.
+ *   n_alpha_out, n_r_out [n * n_radii] int32 (device), nullable, row-major
+ *                       (radius fastest).
+ *   mdef_out, sigma_mdef_out [n * n_radii] fp64 (device), nullable.
+ * opts as tod_nwr (precision AUTO / FP16 / BF16, ref_splits, margin_scale,
+ * force_fallback); exclude_self must be 0 (p samples itself).  Requires
+ * n <= 2^20, which keeps S2 below 2^63 (TOD_ERR_UNSUPPORTED above).
+ * Workspace: tod_loci_workspace_size(n, d, n_radii, capacity, opts) bytes,
+ * 256-byte aligned; stats: the neighbours-within-range pass's fields, with
+ * ms_score the time of the two LOCI kernels.
+ */
+size_t tod_loci_workspace_size(int64_t n, int64_t d, int32_t n_radii, int64_t capacity,
+                               const tod_options* opts);
+tod_status tod_loci(const float* x, int64_t n, int64_t d, const double* radii, int32_t n_radii,
+                    double alpha, int32_t n_min, double k_sigma, int64_t capacity,
+                    const tod_options* opts, void* workspace, size_t ws_bytes, void* stream,
+                    double* score_out, int32_t* flag_out, int32_t* n_alpha_out,
+                    int32_t* n_r_out, double* mdef_out, double* sigma_mdef_out,
+                    tod_stats* stats);
 
 /* Static string naming a status code. */
 const char* tod_status_string(tod_status status);

@@ -11,7 +11,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtod.so")
 SOURCES = ["api.hip", "prep.hip", "select.hip", "lof.hip", "tile_f32.hip", "tile_f16.hip",
            "tile_bf16.hip", "mtile_f16.hip", "mtile_bf16.hip", "order.hip",
-           "rtile_f16.hip", "rtile_bf16.hip", "nwr.hip", "score.hip"]
+           "rtile_f16.hip", "rtile_bf16.hip", "nwr.hip", "score.hip", "loci.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

@@ -678,6 +678,147 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
   return TOD_OK;
 }
 
+// Bytes of a neighbours-within-range workspace whose candidate buffer holds
+// `room` pairs (-1: 64 per padded query row and 2^20 more); 0 if the sizes
+// or options are invalid.
+size_t nwr_ws_bytes(int64_t nq, int64_t nr, int64_t d, const tod_options& o, int32_t self,
+                    int64_t room) {
+  if (nq <= 0 || nr <= 0 || d <= 0 || nq > kMaxRows || nr > kMaxRows) return 0;
+  Plan p;
+  const char* why;
+  if (tod::make_plan_nwr(nq, nr, d, self, o, &p, &why) != TOD_OK) return 0;
+  const tod::NwrLayout L = tod::make_layout_nwr(p);
+  const size_t r = room >= 0 ? (size_t)room : (size_t)64 * p.nq_pad + ((size_t)1 << 20);
+  return L.cand + 512 + r * 8;
+}
+
+// LOCI workspace: the neighbour lists at the largest radius (CSR offsets,
+// ids, one radius index byte per pair), the per-radius neighbourhood sizes,
+// then the neighbours-within-range pass's own workspace.
+struct LociLayout {
+  size_t row_ptr, idx, bins, na, nr, nwr;
+};
+
+int32_t loci_stride(int32_t nl) { return nl <= 8 ? 8 : (nl <= 16 ? 16 : 32); }
+
+LociLayout loci_layout(int64_t n, int32_t nl, int64_t capacity) {
+  LociLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  const size_t cells = (size_t)n * (size_t)loci_stride(nl);
+  L.row_ptr = take(sizeof(int64_t) * (size_t)(n + 1));
+  L.idx = take(sizeof(int64_t) * (size_t)capacity);
+  L.bins = take((size_t)capacity);
+  L.na = take(sizeof(int32_t) * cells);
+  L.nr = take(sizeof(int32_t) * cells);
+  L.nwr = off;
+  return L;
+}
+
+constexpr int64_t kLociMaxRows = (int64_t)1 << 20;
+
+tod_status check_loci(int64_t n, int64_t d, const double* radii, int32_t nl, double alpha,
+                      int32_t n_min, double k_sigma, int64_t capacity) {
+  if (n <= 0 || d <= 0) return fail(TOD_ERR_INVALID_ARG, "row count and d must be positive");
+  if (n > kLociMaxRows) return fail(TOD_ERR_UNSUPPORTED, "LOCI supports at most 2^20 rows");
+  if (d > 4096) return fail(TOD_ERR_UNSUPPORTED, "d > 4096");
+  if (!radii) return fail(TOD_ERR_INVALID_ARG, "null radii");
+  if (nl < 1 || nl > tod::kLociMaxRadii)
+    return fail(TOD_ERR_INVALID_ARG, "n_radii must be in [1, 32]");
+  for (int32_t l = 0; l < nl; ++l) {
+    if (!(radii[l] >= 0.0) || isinf(radii[l]))
+      return fail(TOD_ERR_INVALID_ARG, "radii must be finite and >= 0");
+    if (l > 0 && !(radii[l] > radii[l - 1]))
+      return fail(TOD_ERR_INVALID_ARG, "radii must be strictly increasing");
+  }
+  if (!(alpha > 0.0 && alpha <= 1.0)) return fail(TOD_ERR_INVALID_ARG, "alpha must be in (0, 1]");
+  if (n_min < 1) return fail(TOD_ERR_INVALID_ARG, "n_min must be >= 1");
+  if (!(k_sigma >= 0.0) || isinf(k_sigma))
+    return fail(TOD_ERR_INVALID_ARG, "k_sigma must be finite and >= 0");
+  if (capacity < n) return fail(TOD_ERR_INVALID_ARG, "capacity must be >= n (every point is its own neighbour)");
+  return TOD_OK;
+}
+
+tod_status run_loci(const float* x, int64_t n, int64_t d, const double* radii, int32_t nl,
+                    double alpha, int32_t n_min, double k_sigma, int64_t capacity,
+                    const tod_options* opts_in, void* ws, size_t ws_bytes, void* stream,
+                    double* score_out, int32_t* flag_out, int32_t* na_out, int32_t* nr_out,
+                    double* mdef_out, double* smdef_out, tod_stats* stats) {
+  g_last_error.clear();
+  tod_options o;
+  tod_status st = resolve_options(opts_in, &o);
+  if (st != TOD_OK) return st;
+  if (o.exclude_self)
+    return fail(TOD_ERR_INVALID_ARG, "LOCI samples every point itself: exclude_self must be 0");
+  if (!x) return fail(TOD_ERR_INVALID_ARG, "null input pointer");
+  if (!score_out) return fail(TOD_ERR_INVALID_ARG, "null score output");
+  st = check_loci(n, d, radii, nl, alpha, n_min, k_sigma, capacity);
+  if (st != TOD_OK) return st;
+  if (!ws) return fail(TOD_ERR_INVALID_ARG, "null workspace");
+  if ((uintptr_t)ws & 255) return fail(TOD_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  const LociLayout L = loci_layout(n, nl, capacity);
+  if (ws_bytes <= L.nwr)
+    return fail(TOD_ERR_WORKSPACE, "workspace too small for " + std::to_string(capacity) +
+                                       " pairs: need " +
+                                       std::to_string(tod_loci_workspace_size(n, d, nl, capacity,
+                                                                              opts_in)) +
+                                       " bytes");
+  char* base = (char*)ws;
+  int64_t* row_ptr = (int64_t*)(base + L.row_ptr);
+  int64_t* idx = (int64_t*)(base + L.idx);
+  int64_t total = 0;
+  // The neighbour lists at the largest radius: exact membership, every
+  // point its own neighbour, ids ascending within a row.
+  st = run_nwr(x, n, x, n, d, radii[nl - 1], &o, base + L.nwr, ws_bytes - L.nwr, stream, row_ptr,
+               capacity, idx, nullptr, &total, stats);
+  if (st != TOD_OK) return st;
+
+  tod::LociArgs a;
+  memset(&a, 0, sizeof(a));
+  a.x = x;
+  a.n = n;
+  a.d = (int32_t)d;
+  a.nl = nl;
+  a.nls = loci_stride(nl);
+  a.n_min = n_min;
+  a.k_sigma = k_sigma;
+  a.row_ptr = row_ptr;
+  a.idx = idx;
+  a.bins = (uint8_t*)(base + L.bins);
+  a.na = (int32_t*)(base + L.na);
+  a.nr = (int32_t*)(base + L.nr);
+  for (int32_t l = 0; l < nl; ++l) {
+    a.r2[l] = radii[l] * radii[l];
+    const double ar = alpha * radii[l];
+    a.a2[l] = ar * ar;
+  }
+  a.score = score_out;
+  a.flag = flag_out;
+  a.na_out = na_out;
+  a.nr_out = nr_out;
+  a.mdef_out = mdef_out;
+  a.smdef_out = smdef_out;
+  hipStream_t s = (hipStream_t)stream;
+  Timers tm;
+  tm.on = stats != nullptr;
+  hipEvent_t e0 = tm.mark(s);
+  hipError_t he = tod::launch_loci(a, s);
+  if (he != hipSuccess) return hip_fail(he, "LOCI launch");
+  hipEvent_t e1 = tm.mark(s);
+  if (stats) {
+    he = hipStreamSynchronize(s);
+    if (he != hipSuccess) return hip_fail(he, "LOCI synchronize");
+    const float ms = Timers::ms(e0, e1);
+    stats->ms_score = ms;
+    stats->ms_total += ms;
+  }
+  return TOD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -781,14 +922,9 @@ tod_status tod_cof(const float* x, int64_t n, int64_t d, int32_t k, const tod_op
 size_t tod_nwr_workspace_size(int64_t nq, int64_t nr, int64_t d, const tod_options* opts) {
   tod_options o;
   if (resolve_options(opts, &o) != TOD_OK) return 0;
-  if (nq <= 0 || nr <= 0 || d <= 0 || nq > kMaxRows || nr > kMaxRows) return 0;
-  Plan p;
-  const char* why;
-  // Sized for separate query and reference sets (enough for any call).
-  if (tod::make_plan_nwr(nq, nr, d, 0, o, &p, &why) != TOD_OK) return 0;
-  const tod::NwrLayout L = tod::make_layout_nwr(p);
-  const size_t room = (size_t)64 * p.nq_pad + ((size_t)1 << 20);
-  return L.cand + 512 + room * 8;
+  // Sized for separate query and reference sets (enough for any call), with
+  // room for 64 candidates per query row and 2^20 more.
+  return nwr_ws_bytes(nq, nr, d, o, 0, -1);
 }
 
 tod_status tod_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
@@ -797,6 +933,34 @@ tod_status tod_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
                    float* dist_out, int64_t* total_out, tod_stats* stats) {
   return run_nwr(xq, nq, xr, nr, d, phi, opts, workspace, ws_bytes, stream, row_ptr_out,
                  capacity, idx_out, dist_out, total_out, stats);
+}
+
+size_t tod_loci_workspace_size(int64_t n, int64_t d, int32_t n_radii, int64_t capacity,
+                               const tod_options* opts) {
+  tod_options o;
+  if (resolve_options(opts, &o) != TOD_OK) return 0;
+  if (n <= 0 || d <= 0 || n > kLociMaxRows || n_radii < 1 || n_radii > tod::kLociMaxRadii ||
+      capacity < n)
+    return 0;
+  o.exclude_self = 0;
+  // The neighbours-within-range pass gets candidate room for every pair in
+  // range and a quarter more for the filter's uncertain ones, so that one
+  // fill pass covers all rows (a batch per few hundred rows would leave
+  // the GPU mostly idle).
+  const size_t nwr = nwr_ws_bytes(n, n, d, o, 1, capacity + capacity / 4 + ((int64_t)1 << 20));
+  if (nwr == 0) return 0;
+  return loci_layout(n, n_radii, capacity).nwr + nwr;
+}
+
+tod_status tod_loci(const float* x, int64_t n, int64_t d, const double* radii, int32_t n_radii,
+                    double alpha, int32_t n_min, double k_sigma, int64_t capacity,
+                    const tod_options* opts, void* workspace, size_t ws_bytes, void* stream,
+                    double* score_out, int32_t* flag_out, int32_t* n_alpha_out,
+                    int32_t* n_r_out, double* mdef_out, double* sigma_mdef_out,
+                    tod_stats* stats) {
+  return run_loci(x, n, d, radii, n_radii, alpha, n_min, k_sigma, capacity, opts, workspace,
+                  ws_bytes, stream, score_out, flag_out, n_alpha_out, n_r_out, mdef_out,
+                  sigma_mdef_out, stats);
 }
 
 tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,

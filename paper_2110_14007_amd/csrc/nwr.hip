@@ -31,33 +31,6 @@ constexpr int kScanT = 256;
 constexpr int kScanPer = 16;
 constexpr int kScanChunk = kScanT * kScanPer;
 
-// Exact squared distance of two fp32 rows, as the definition states it.
-__device__ __forceinline__ double exact_d2(const float* __restrict__ q,
-                                           const float* __restrict__ r, int d) {
-#pragma clang fp contract(off)
-  double s = 0.0;
-  if ((d & 3) == 0) {
-    for (int t = 0; t < d; t += 4) {
-      const float4 x = *reinterpret_cast<const float4*>(q + t);
-      const float4 y = *reinterpret_cast<const float4*>(r + t);
-      double e = (double)x.x - (double)y.x;
-      s = s + e * e;
-      e = (double)x.y - (double)y.y;
-      s = s + e * e;
-      e = (double)x.z - (double)y.z;
-      s = s + e * e;
-      e = (double)x.w - (double)y.w;
-      s = s + e * e;
-    }
-  } else {
-    for (int t = 0; t < d; ++t) {
-      const double e = (double)q[t] - (double)r[t];
-      s = s + e * e;
-    }
-  }
-  return s;
-}
-
 // Range test of one pair with the pair's own reference norm and radius
 // (the tile's per-row thresholds use the reference maxima): +1 in range for
 // certain, -1 out of range for certain, 0 undecided.  acc is the pair's fp32

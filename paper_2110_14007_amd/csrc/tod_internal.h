@@ -147,6 +147,63 @@ constexpr int64_t kOrderMinRows = 4096;
 int32_t order_blocks(int64_t nr);
 hipError_t launch_order(const Plan& p, const Args& a, hipStream_t s);
 
+// Exact squared distance of two fp32 rows, as the definition states it: fp64,
+// columns in order, ((double)x - (double)y)^2 added one at a time with no
+// fused multiply-add.  Rows of a multiple of four elements are read as float4
+// (16-byte aligned rows).
+__device__ __forceinline__ double exact_d2(const float* __restrict__ q,
+                                           const float* __restrict__ r, int d) {
+#pragma clang fp contract(off)
+  double s = 0.0;
+  if ((d & 3) == 0) {
+    for (int t = 0; t < d; t += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(q + t);
+      const float4 y = *reinterpret_cast<const float4*>(r + t);
+      double e = (double)x.x - (double)y.x;
+      s = s + e * e;
+      e = (double)x.y - (double)y.y;
+      s = s + e * e;
+      e = (double)x.z - (double)y.z;
+      s = s + e * e;
+      e = (double)x.w - (double)y.w;
+      s = s + e * e;
+    }
+  } else {
+    for (int t = 0; t < d; ++t) {
+      const double e = (double)q[t] - (double)r[t];
+      s = s + e * e;
+    }
+  }
+  return s;
+}
+
+// LOCI (Papadimitriou et al.): arguments of the two passes over the
+// neighbours within the largest radius (tod_nwr's CSR, self pairs included).
+constexpr int kLociMaxRadii = 32;
+struct LociArgs {
+  const float* x;
+  int64_t n;
+  int32_t d;
+  int32_t nl;   // radii
+  int32_t nls;  // row stride of na / nr (8, 16 or 32 >= nl)
+  int32_t n_min;
+  double k_sigma;
+  const int64_t* row_ptr;
+  const int64_t* idx;
+  uint8_t* bins;  // per pair: index of the first sampling radius that holds it
+  int32_t* na;    // [n x nls] counting-neighbourhood sizes n(p, alpha r_l)
+  int32_t* nr;    // [n x nls] sampling-neighbourhood sizes n(p, r_l)
+  double r2[kLociMaxRadii];  // fl(r_l * r_l)
+  double a2[kLociMaxRadii];  // fl(fl(alpha * r_l)^2)
+  double* score;
+  int32_t* flag;
+  int32_t* na_out;
+  int32_t* nr_out;
+  double* mdef_out;
+  double* smdef_out;
+};
+hipError_t launch_loci(const LociArgs& a, hipStream_t s);
+
 // Fallback scan grid and the most chunks one failing row is cut into.
 constexpr int kFbGrid = 1024;
 constexpr int kFbMaxChunks = 64;

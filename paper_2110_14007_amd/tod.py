@@ -30,7 +30,7 @@ SCORES = {"kth": 0, "largest": 0, "mean": 1, "median": 2, "sum": 3}
 
 SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
            "tod_knn_decision", "tod_knn_classify", "tod_abod", "tod_cof", "tod_nwr_workspace_size",
-           "tod_nwr",
+           "tod_nwr", "tod_loci_workspace_size", "tod_loci",
            "tod_plan",
            "tod_status_string", "tod_last_error")
 
@@ -119,6 +119,12 @@ def _load():
     lib.tod_nwr.argtypes = [vp, i64, vp, i64, i64, ctypes.c_double, opt_p, vp, sz, vp, vp, i64, vp,
                             vp, ctypes.POINTER(i64), st_p]
     lib.tod_nwr.restype = ctypes.c_int
+    dbl = ctypes.c_double
+    lib.tod_loci_workspace_size.argtypes = [i64, i64, i32, i64, opt_p]
+    lib.tod_loci_workspace_size.restype = sz
+    lib.tod_loci.argtypes = [vp, i64, i64, ctypes.POINTER(dbl), i32, dbl, i32, dbl, i64, opt_p, vp,
+                             sz, vp, vp, vp, vp, vp, vp, vp, st_p]
+    lib.tod_loci.restype = ctypes.c_int
     lib.tod_plan.argtypes = [i64, i64, i64, i32, opt_p, st_p]
     lib.tod_plan.restype = ctypes.c_int
     lib.tod_status_string.argtypes = [ctypes.c_int]
@@ -441,6 +447,60 @@ def tod_nwr(xq, xr, phi: float, opts=None, workspace=None, stream=None, stats=No
     _check(st, "tod_nwr")
     n = int(total.value)
     return row_ptr, idx[:n], (dist[:n] if dist is not None else None)
+
+
+def tod_loci_workspace_size(n: int, d: int, n_radii: int, capacity: int, opts=None) -> int:
+    return int(_lib.tod_loci_workspace_size(int(n), int(d), int(n_radii), int(capacity),
+                                            ctypes.byref(opts) if opts is not None else None))
+
+
+def tod_loci(x, radii, alpha: float = 0.5, n_min: int = 20, k_sigma: float = 3.0, opts=None,
+             capacity=None, grow: bool = True, workspace=None, stream=None, stats=None,
+             return_all: bool = False):
+    """LOCI at the ladder of sampling radii -> (score fp64 [n], flag int32 [n]).
+
+    With return_all, a third element holds n_alpha, n_r (int32 [n, L]), mdef
+    and sigma_mdef (fp64 [n, L]).  ``capacity`` is the number of pairs within
+    the largest radius (self pairs included) the workspace is sized for
+    (default 64 per row); if more are in range and ``grow`` is set, the
+    workspace is resized to the count the library reports and the call is
+    made once more, else TodError(TOD_ERR_CAPACITY) is raised.
+    """
+    torch = _torch()
+    _dev_matrix(x, "x")
+    n, d = x.shape
+    rad = [float(r) for r in radii]
+    nl = len(rad)
+    rarr = (ctypes.c_double * max(nl, 1))(*rad)
+    dev = x.device
+    score = torch.empty((n,), dtype=torch.float64, device=dev)
+    flag = torch.empty((n,), dtype=torch.int32, device=dev)
+    extra = None
+    if return_all:
+        extra = {"n_alpha": torch.empty((n, nl), dtype=torch.int32, device=dev),
+                 "n_r": torch.empty((n, nl), dtype=torch.int32, device=dev),
+                 "mdef": torch.empty((n, nl), dtype=torch.float64, device=dev),
+                 "sigma_mdef": torch.empty((n, nl), dtype=torch.float64, device=dev)}
+    st = stats if stats is not None else new_stats()
+    optp = ctypes.byref(opts) if opts is not None else None
+    cap = int(capacity) if capacity is not None else 64 * n
+    for _ in range(2):
+        need = tod_loci_workspace_size(n, d, nl, cap, opts)
+        if need == 0:  # arguments the size query rejects: let the call report why
+            need = 256
+        wsbuf, wsp, wsn = _ws(workspace, need, dev)
+        rc = _lib.tod_loci(_p(x), n, d, rarr, nl, float(alpha), int(n_min), float(k_sigma), cap,
+                           optp, wsp, wsn, _stream(stream), _p(score), _p(flag),
+                           _p(extra["n_alpha"]) if extra else None,
+                           _p(extra["n_r"]) if extra else None,
+                           _p(extra["mdef"]) if extra else None,
+                           _p(extra["sigma_mdef"]) if extra else None, ctypes.byref(st))
+        if rc != TOD_ERR_CAPACITY or not grow:
+            break
+        cap = int(st.pairs_in_range)
+    _check(rc, "tod_loci")
+    del wsbuf
+    return (score, flag, extra) if return_all else (score, flag)
 
 
 def raw_library():

@@ -26,6 +26,15 @@ the same generator.  Labels: 1 = outlier.
                              2,970 points each) + 300 outliers 10*N(0, I);
                              phi = 0.9 sqrt(2d), 90 % of the typical distance
                              between two points of one cluster             (neighbours within range)
+  L1  n=20,000   d=4   C2's recipe in 4 dimensions (5 Gaussian components, 19,600
+                       points, 400 box outliers); sampling radii 0.5 * 5^(l/7),
+                       l = 0..7 (0.5 to 2.5), alpha = 1/2, n_min = 20,
+                       k_sigma = 3                                         (LOCI)
+
+L1 is LOCI's workload: the detector is meant for low-dimensional data, where
+counting neighbourhoods at half the sampling radius are not empty; its radii
+span the clusters' scale (the median sampling neighbourhood grows from 17 to
+3,300 points) and about 5.4e7 pairs lie within the largest.
 
 N1 stands in for the paper's 30,000-sample synthetic set of its NWR runtime
 breakdown (Table 5); the paper states neither its dimension nor its
@@ -69,6 +78,11 @@ WORKLOADS = {
     "N1": Workload("N1", 30_000, 200, 0, 6, "fp16", False, 0,
                    "NWR, n=30000 d=200 phi=18: 10-cluster Gaussian mixture + 1% N(0,100I) "
                    "outliers, fp16 filter", {"phi": 18.0}),
+    "L1": Workload("L1", 20_000, 4, 0, 7, "fp16", False, 0,
+                   "LOCI, n=20000 d=4: 5-Gaussian mixture + 2% uniform box outliers, 8 radii "
+                   "0.5..2.5, alpha 0.5, n_min 20, k_sigma 3",
+                   {"radii": [0.5 * 5.0 ** (i / 7.0) for i in range(8)], "alpha": 0.5,
+                    "n_min": 20, "k_sigma": 3.0}),
 }
 
 
@@ -94,7 +108,7 @@ def generate(name: str, n: int | None = None):
         n_out = max(1, n * 100 // 2000)
         inl = rng.standard_normal((n - n_out, d))
         out = rng.uniform(-6.0, 6.0, (n_out, d))
-    elif name == "C2":
+    elif name in ("C2", "L1"):
         n_out = max(1, n * 2 // 100)
         n_in = n - n_out
         means = rng.uniform(-10.0, 10.0, (5, d))
