@@ -109,7 +109,7 @@ def cpu_baseline(x, k, target_s):
 # their shared headers and the planner that picks their template arguments.
 TILE_SOURCES = ("api.hip", "tod_internal.h", "wave.h", "halfwave.h", "tile.h", "tile_f32.hip",
                 "tile_f16.hip", "tile_bf16.hip", "mtile.h", "mtile_f16.hip", "mtile_bf16.hip",
-                "order.hip", "rtile.h", "rtile_f16.hip", "rtile_bf16.hip")
+                "order.hip", "rtile.h", "rtile_f16.hip", "rtile_bf16.hip", "nwr.hip", "loci.hip")
 
 
 def kernel_sources_digest():
@@ -343,7 +343,8 @@ def bench_loci(args, w):
                                                          "ms_score", "ms_total")},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                     "traffic": None, "kernel": "loci_count+loci_sum", "launch_ms": round(loci_ms, 4)},
+                     "traffic": recorded_traffic(w.name, "loci_count+loci_sum"),
+                     "kernel": "loci_count+loci_sum", "launch_ms": round(loci_ms, 4)},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline_loci(x_host, p, args.cpu_seconds)
