@@ -842,11 +842,20 @@ size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t 
   if (lof && nq != nr) return 0;
   Plan p;
   const char* why;
-  // Modes 0 and 2 size for separate query and reference sets (enough for any
-  // call of those entry points); mode 1 for X against itself.
+  // Mode 1 sizes for X against itself.  Modes 0 and 2 serve separate query
+  // and reference sets and X against itself (tod_knn_score, or tod_knn with
+  // xq == xr), so they take the larger of the two layouts.
   if (tod::make_plan(nq, nr, d, k, lof, lof, o, &p, &why) != TOD_OK) return 0;
   if (mode == 2) p.lists = 1;
-  return tod::make_layout(p).total;
+  size_t total = tod::make_layout(p).total;
+  if (!lof && nq == nr) {
+    Plan ps;
+    if (tod::make_plan(nq, nr, d, k, 0, 1, o, &ps, &why) != TOD_OK) return 0;
+    if (mode == 2) ps.lists = 1;
+    const size_t t2 = tod::make_layout(ps).total;
+    total = t2 > total ? t2 : total;
+  }
+  return total;
 }
 
 tod_status tod_knn(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,

@@ -31,6 +31,7 @@ namespace tod {
 namespace {
 
 constexpr int kW = 4;  // waves per workgroup, one point per wave at a time
+constexpr int kU = 4;  // pairs per lane in flight
 
 template <int NLM>
 __global__ void __launch_bounds__(kW * 64) loci_count_kernel(LociArgs a) {
@@ -43,22 +44,34 @@ __global__ void __launch_bounds__(kW * 64) loci_count_kernel(LociArgs a) {
     int cr[NLM], ca[NLM];  // pairs within r_l / alpha r_l seen by this lane
 #pragma unroll
     for (int l = 0; l < NLM; ++l) cr[l] = ca[l] = 0;
-    for (int64_t e = a.row_ptr[p] + lane; e < e1; e += 64) {
-      const int64_t q = a.idx[e];
-      const double d2 = exact_d2(xp, a.x + q * a.d, a.d);
-      int br = 0, ba = 0;  // first radius index holding the pair (nl: none)
+    // kU pairs per lane per trip: their ids, then their rows' loads, are in
+    // flight together (one pair at a time leaves the wave waiting on each
+    // dependent gather).
+    for (int64_t e0 = a.row_ptr[p]; e0 < e1; e0 += 64 * kU) {
+      int64_t q[kU];
 #pragma unroll
-      for (int l = 0; l < NLM; ++l) {
-        if (l < nl) {
-          br += a.r2[l] < d2 ? 1 : 0;
-          ba += a.a2[l] < d2 ? 1 : 0;
-        }
+      for (int u = 0; u < kU; ++u) {
+        const int64_t e = e0 + 64 * u + lane;
+        q[u] = e < e1 ? a.idx[e] : -1;
       }
-      a.bins[e] = (uint8_t)br;
 #pragma unroll
-      for (int l = 0; l < NLM; ++l) {
-        cr[l] += l >= br ? 1 : 0;
-        ca[l] += l >= ba ? 1 : 0;
+      for (int u = 0; u < kU; ++u) {
+        if (q[u] < 0) continue;
+        const double d2 = exact_d2(xp, a.x + q[u] * a.d, a.d);
+        int br = 0, ba = 0;  // first radius index holding the pair (nl: none)
+#pragma unroll
+        for (int l = 0; l < NLM; ++l) {
+          if (l < nl) {
+            br += a.r2[l] < d2 ? 1 : 0;
+            ba += a.a2[l] < d2 ? 1 : 0;
+          }
+        }
+        a.bins[e0 + 64 * u + lane] = (uint8_t)br;
+#pragma unroll
+        for (int l = 0; l < NLM; ++l) {
+          cr[l] += l >= br ? 1 : 0;
+          ca[l] += l >= ba ? 1 : 0;
+        }
       }
     }
     int32_t* nrp = a.nr + p * a.nls;
@@ -91,24 +104,35 @@ __global__ void __launch_bounds__(kW * 64) loci_sum_kernel(LociArgs a) {
 #pragma unroll
     for (int l = 0; l < NLM; ++l) s1[l] = s2[l] = 0;
     const int64_t e1 = a.row_ptr[p + 1];
-    for (int64_t e = a.row_ptr[p] + lane; e < e1; e += 64) {
-      const int64_t q = a.idx[e];
-      const int b = a.bins[e];
-      // n(q, alpha r_l) for every l: the row of q, 16-byte chunks (the row
-      // stride nls is a multiple of 8).
-      const int4* nq4 = reinterpret_cast<const int4*>(a.na + q * nls);
+    for (int64_t e0 = a.row_ptr[p]; e0 < e1; e0 += 64 * kU) {
+      // kU pairs per lane per trip, their loads in flight together.
+      int64_t q[kU];
+      int b[kU];
 #pragma unroll
-      for (int c = 0; c < NLM / 4; ++c) {
-        if (4 * c < nl) {
-          const int4 v = nq4[c];
-          const int vv[4] = {v.x, v.y, v.z, v.w};
+      for (int u = 0; u < kU; ++u) {
+        const int64_t e = e0 + 64 * u + lane;
+        const bool live = e < e1;
+        q[u] = live ? a.idx[e] : 0;
+        b[u] = live ? (int)a.bins[e] : NLM;  // past the row: contributes to no radius
+      }
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int l = 4 * c + u;
-            if (l < nl && l >= b) {
-              const uint64_t w = (uint32_t)vv[u];
-              s1[l] += w;
-              s2[l] += w * w;
+      for (int u = 0; u < kU; ++u) {
+        // n(q, alpha r_l) for every l: the row of q, 16-byte chunks (the row
+        // stride nls is a multiple of 8).
+        const int4* nq4 = reinterpret_cast<const int4*>(a.na + q[u] * nls);
+#pragma unroll
+        for (int c = 0; c < NLM / 4; ++c) {
+          if (4 * c < nl) {
+            const int4 v = nq4[c];
+            const int vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int l = 4 * c + t;
+              if (l < nl && l >= b[u]) {
+                const uint64_t w = (uint32_t)vv[t];
+                s1[l] += w;
+                s2[l] += w * w;
+              }
             }
           }
         }
