@@ -577,11 +577,24 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 #pragma unroll
       for (int s = 1; s < NG; s += 2) m = max3f(m, ms[s], ms[s + 1 < NG ? s + 1 : s]);
       if (!__ballot(m > thr)) return;
-      // Slow path: sub-tile by sub-tile (one copy of the insertion and merge
-      // code).  With one sub-tile per group the accumulators are reused;
-      // otherwise the sub-tile is recomputed (KC MFMAs, bit-identical), which
-      // keeps the fast path's accumulators dead after their reduction.
+      // Slow path: sub-tile by sub-tile.  Rows of several k-steps reuse the
+      // group's accumulators, one copy of the insertion code per sub-tile (a
+      // recomputation would put its LDS reads and MFMA chain on the latency
+      // of every slow entry, which the workgroup's other waves wait out at the
+      // next stage barrier).  Rows of one k-step recompute the sub-tile (one
+      // MFMA, bit-identical), which keeps the fast path's accumulators dead
+      // after their reduction and the kernel at three waves per SIMD.
       const int gl = live - g0 < NG ? live - g0 : NG;
+      if constexpr (NG > 1 && KC >= 2) {
+#pragma unroll
+        for (int s = 0; s < NG; ++s) {
+          if (s >= gl || !__ballot(ms[s] > thr)) continue;
+          uint32_t ts = t0u + 32u * (uint32_t)(g0 + s);
+          asm volatile("" : "+s"(ts));  // ids formed here (see below)
+          insert(acc[s], ts);
+        }
+        return;
+      }
 #pragma unroll 1
       for (int s = 0; s < gl; ++s) {
         float msel = ms[0];
