@@ -94,6 +94,11 @@ typedef struct {
                           * thresholds tighten early.  Results are identical either way. */
   int32_t score;         /* tod_score: the kNN outlier score of tod_knn_score, tod_knn_decision
                           * and tod_lof's knn_score_out */
+  int32_t tail_parts;    /* fp16 / bf16 filter with one reference split: the workgroups of a
+                          * query block's last, partly filled round of the GPU scan the
+                          * references in this many parts on separate workgroups (their lists
+                          * are merged before the recheck); 0 = planner, 1 = off, at most 8.
+                          * Results are identical either way. */
 } tod_options;
 
 /* Plan and per-phase timings of one call (filled when a non-NULL pointer is
@@ -107,12 +112,15 @@ typedef struct {
   int64_t blocks;         /* number of query blocks */
   int64_t rows_certified; /* rows whose shortlist passed the certificate */
   int64_t rows_fallback;  /* rows recomputed exactly */
-  int64_t tile_launches;  /* launches of the fused distance + selection kernel */
+  int64_t tile_launches;  /* launches of the fused distance + selection kernel (a block with a
+                           * tail split takes two) */
   float ms_prep, ms_tile, ms_recheck, ms_fallback, ms_score, ms_total;
   int32_t reordered;      /* 1 if the scan used the grouped row order (see tod_options.reorder) */
   int64_t pairs_candidate; /* tod_nwr: pairs the filter could not rule out of range */
   int64_t pairs_uncertain; /* tod_nwr: candidates whose range test needed the exact distance */
   int64_t pairs_in_range;  /* tod_nwr: pairs within the threshold */
+  int32_t tail_parts;      /* parts the last partly filled round was scanned in (1: none) */
+  int64_t tail_rows;       /* query rows scanned in parts, summed over the blocks */
 } tod_stats;
 
 /* Fill *opts with defaults (AUTO precision, planner-chosen sizes). */
@@ -230,7 +238,8 @@ tod_status tod_cof(const float* x, int64_t n, int64_t d, int32_t k, const tod_op
  * Host-only planner (Section 6 automatic batching): fills *plan with the
  * precision, K', query block, reference splits and block count that tod_knn
  * would use, without touching the GPU.  Only the plan fields of tod_stats
- * are written.
+ * are written; tile_launches counts one launch per block (the tail split is
+ * decided at run time from the GPU's occupancy).
  */
 tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,
                     tod_stats* plan);

@@ -38,6 +38,9 @@ constexpr int64_t kMaxRows = 0x7fffffffLL;
 constexpr int64_t kMaxD = 4096;
 constexpr int32_t kMaxK = 256;
 constexpr int32_t kMaxKPrime = 256;
+// Tail split: at most 8 pieces, and a tail region of at most 2^18 lists.
+constexpr int32_t kMaxTailParts = 8;
+constexpr int64_t kTailLists = 1 << 18;
 
 tod_status resolve_options(const tod_options* in, tod_options* out) {
   tod_default_options(out);
@@ -59,6 +62,8 @@ tod_status resolve_options(const tod_options* in, tod_options* out) {
     return fail(TOD_ERR_INVALID_ARG, "reorder must be -1, 0 or 1");
   if (out->score < TOD_SCORE_KTH || out->score > TOD_SCORE_SUM)
     return fail(TOD_ERR_INVALID_ARG, "unknown score");
+  if (out->tail_parts < 0 || out->tail_parts > kMaxTailParts)
+    return fail(TOD_ERR_INVALID_ARG, "tail_parts must be in [0, 8]");
   return TOD_OK;
 }
 
@@ -178,6 +183,16 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   // group on); by default from kOrderMinRows references on.
   const bool want = o.reorder > 0 || (o.reorder == 0 && nr >= kOrderMinRows);
   p->order = (self && p->tile_kind == 1 && p->splits == 1 && want) ? 1 : 0;
+  // Tail split of the register-list tile with one reference split.
+  p->tail_parts = 1;
+  p->tail_auto = 0;
+  p->tail_lists = 0;
+  if (p->tile_kind == 1 && p->splits == 1 && o.tail_parts != 1) {
+    p->tail_parts = o.tail_parts == 0 ? kMaxTailParts : o.tail_parts;
+    p->tail_auto = o.tail_parts == 0 ? 1 : 0;
+    const int64_t want_lists = p->query_block * p->tail_parts;
+    p->tail_lists = want_lists < kTailLists ? want_lists : kTailLists;
+  }
   return TOD_OK;
 }
 
@@ -200,6 +215,7 @@ Layout make_layout(const Plan& p) {
   L.n64_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
   L.rho_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
   L.partial = take(sizeof(uint64_t) * p.query_block * p.splits * p.kprime);
+  L.ptail = take(sizeof(uint64_t) * p.tail_lists * p.kprime);
   L.worklist = take(sizeof(int32_t) * p.nq);
   // Chunk lists exist only when fewer than kFbGrid rows fail, so kFbGrid
   // lists of k entries always suffice.
@@ -409,6 +425,10 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.n64_q = (double*)(base + L.n64_q);
   a.rho_q = (double*)(base + L.rho_q);
   a.partial = (uint64_t*)(base + L.partial);
+  a.parts = 1;
+  a.tail_parts = 1;
+  a.tail_q0 = p.nq;
+  a.ptail = p.tail_lists ? (uint64_t*)(base + L.ptail) : nullptr;
   a.worklist = (int32_t*)(base + L.worklist);
   a.fbpart = (uint2*)(base + L.fbpart);
   a.fbidx = (uint32_t*)(base + L.fbidx);
@@ -438,14 +458,25 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   hipEvent_t e_prep = tm.mark(s);
   std::vector<std::pair<hipEvent_t, hipEvent_t>> tile_ev;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> rc_ev;
+  int32_t tail_parts = 1;
+  int64_t tail_rows = 0, launches = 0;
   for (int64_t b = 0; b < p.blocks; ++b) {
     const int64_t q0 = b * p.query_block;
     const int64_t rows = nq - q0 < p.query_block ? nq - q0 : p.query_block;
     hipEvent_t ts = tm.mark(s);
-    he = tod::launch_tile(p, a, q0, rows, s);
+    tod::TileTail tt{rows, 1};
+    he = tod::launch_tile(p, a, q0, rows, s, &tt);
     if (he != hipSuccess) return hip_fail(he, "tile launch");
     hipEvent_t te = tm.mark(s);
-    he = tod::launch_recheck(p, a, q0, rows, s);
+    tod::Args ar = a;
+    ar.tail_q0 = tt.q0;
+    ar.tail_parts = tt.parts;
+    launches += (tt.q0 > 0 ? 1 : 0) + (tt.parts > 1 ? 1 : 0);
+    if (tt.parts > 1) {
+      tail_parts = tt.parts > tail_parts ? tt.parts : tail_parts;
+      tail_rows += rows - tt.q0;
+    }
+    he = tod::launch_recheck(p, ar, q0, rows, s);
     if (he != hipSuccess) return hip_fail(he, "recheck launch");
     hipEvent_t re = tm.mark(s);
     tile_ev.emplace_back(ts, te);
@@ -489,9 +520,11 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     stats->blocks = p.blocks;
     stats->rows_certified = (int64_t)host.certified;
     stats->rows_fallback = (int64_t)host.worklist_count;
-    stats->tile_launches = p.blocks;
+    stats->tile_launches = launches;
     stats->reordered = p.order;
     stats->pairs_candidate = stats->pairs_uncertain = stats->pairs_in_range = 0;
+    stats->tail_parts = tail_parts;
+    stats->tail_rows = tail_rows;
     stats->ms_prep = Timers::ms(e0, e_prep);
     float t = 0.0f, r = 0.0f;
     for (auto& pr : tile_ev) t += Timers::ms(pr.first, pr.second);
@@ -670,6 +703,8 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
     stats->pairs_candidate = g[L.groups];
     stats->pairs_uncertain = (int64_t)host.uncertain;
     stats->pairs_in_range = total;
+    stats->tail_parts = 1;
+    stats->tail_rows = 0;
   }
   if (host.internal) return fail(TOD_ERR_INTERNAL, "range tile passes disagree");
   if (idx_out && total > capacity)

@@ -339,8 +339,11 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   const int64_t group = (int64_t)blockIdx.x * W + wave;
   const bool active = group * 32 < q_rows;  // uniform per wave
   const int64_t q0 = q_begin + group * 32;
+  // blockIdx.y: the reference split, or with the tail split (a.parts > 1,
+  // one split) the piece of the scan order this workgroup takes.
   const int split = blockIdx.y;
-  const int64_t r_begin = (int64_t)split * a.split_len;
+  const bool pieces = a.parts > 1;
+  const int64_t r_begin = pieces ? 0 : (int64_t)split * a.split_len;
   const int64_t r_end = r_begin + a.split_len < a.nr ? r_begin + a.split_len : a.nr;
   const int64_t r_end32 = (r_end + 31) & ~(int64_t)31;  // rows < r_end32 exist (padded copy)
   const bool selfq = a.exclude_self != 0;
@@ -638,8 +641,18 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     for (int i = 1; i < kOrdC; ++i) g = a.cstart[i] <= p0 ? i : g;
     st0 = (int)((a.cstart[g] - r_begin) / TR);
   }
-  // First row of the i-th stage scanned (i < 2 nst + 2; stages past the last
-  // one wrap round and are loaded but never read).
+  // Tail split: piece `split` of `parts` takes the stages [ib, ib + nscan) of
+  // the scan order.
+  int nscan = nst;
+  if (pieces) {
+    // 32-bit: nst < 2^26 and parts <= 8
+    const int ib = (int)((uint32_t)(split * nst) / (uint32_t)a.parts);
+    nscan = (int)((uint32_t)((split + 1) * nst) / (uint32_t)a.parts) - ib;
+    st0 += ib;
+    st0 = st0 >= nst ? st0 - nst : st0;
+  }
+  // First row of the i-th stage scanned (i < nscan + 2 <= nst + 2; stages past
+  // the last one wrap round and are loaded but never read).
   auto t_of = [&](int i) -> int64_t {
     int s = st0 + i;
     s = s >= nst ? s - nst : s;
@@ -670,7 +683,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     dl_issue(t_of(0), 0);
     dl_issue(t_of(1), 1);
     dl_barrier<TR / W + 1>();
-    for (int it = 0; it < nst; ++it) {
+    for (int it = 0; it < nscan; ++it) {
       // Buffer (it + 2) % 3 was last read in trip it - 1, before its barrier.
       dl_issue(t_of(it + 2), (it + 2) % 3);
       stage_body(t_of(it), it % 3);
@@ -692,16 +705,16 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       stage_body(t_of(it), 0);
       TOD_MT_PUT(1, su, suh)
       stage_barrier();
-      if (++it >= nst) break;
+      if (++it >= nscan) break;
       TOD_MT_FETCH(t_of(it + 2), su, suh)
       stage_body(t_of(it), 1);
       TOD_MT_PUT(0, st, sth)
       stage_barrier();
-      if (++it >= nst) break;
+      if (++it >= nscan) break;
     }
   } else {
     __syncthreads();
-    for (int it = 0; it < nst; ++it) {
+    for (int it = 0; it < nscan; ++it) {
       TOD_MT_FETCH(t_of(it + 1), st, sth)
       stage_body(t_of(it), it & 1);
       TOD_MT_PUT((it + 1) & 1, st, sth)
@@ -715,7 +728,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     while (__ballot(cnt > 0)) flush();
     const int64_t ql = group * 32 + col;
     if (ql < q_rows) {
-      uint64_t* dst = a.partial + (ql * a.splits + split) * (2 * R) + h * R;
+      uint64_t* dst = a.partial + (ql * (pieces ? a.parts : a.splits) + split) * (2 * R) + h * R;
 #pragma unroll
       for (int i = 0; i < R; ++i) {
         const uint64_t e = L[i];
@@ -727,10 +740,16 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 
 // Sub-tiles per fast-path group: four for rows of up to 32 elements (one
 // k-step or two), one otherwise.
+//
+// Tail split: a block of G workgroups on a GPU that runs S of them at once
+// ends with a round of G mod S workgroups that leaves most of the GPU idle.
+// With one reference split, those workgroups' scans are cut into P pieces on
+// P times as many workgroups (tail_pieces picks P), in a second launch whose
+// lists go to the tail region.
 template <typename ET, int DPAD, bool FOLD, int R, int W = 4, int NS = Layout<DPAD, FOLD>::ns,
           int NG = (DPAD <= 32 ? 4 : 1)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                        hipStream_t st) {
+                        hipStream_t st, TileTail* tail) {
   const size_t lds = lds_bytes(DPAD, FOLD, W, NS, queue_cap<R>());
   const auto kern = mtile_kernel<ET, DPAD, FOLD, R, W, NS, NG>;
   if (lds > 65536) {
@@ -739,34 +758,70 @@ hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q
     if (e != hipSuccess) return e;
   }
   const int64_t groups = (q_rows + 31) / 32;
-  const dim3 grid((unsigned)((groups + W - 1) / W), (unsigned)p.splits);
-  hipLaunchKernelGGL(kern, grid, dim3(W * 64), lds, st, a, q_begin, q_rows);
+  const int64_t wgs = (groups + W - 1) / W;
+  int64_t main_wgs = wgs;
+  int parts = 1;
+  if (p.splits == 1 && p.tail_parts > 1 && a.ptail) {
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, (const void*)kern, W * 64, lds) ==
+            hipSuccess &&
+        cus > 0 && per > 0) {
+      const int64_t slots = (int64_t)cus * per;
+      const int64_t tw = wgs % slots;
+      const int64_t trows = q_rows - (wgs - tw) * (W * 32);
+      const int64_t nst = (a.nr + 32 * NS - 1) / (32 * NS);
+      parts = tail_pieces(tw, slots, cus, p.tail_parts, p.tail_auto != 0, nst, p.tail_lists,
+                          trows);
+      if (parts > 1) main_wgs = wgs - tw;
+    } else {
+      (void)hipGetLastError();  // no occupancy figures: no tail split
+    }
+  }
+  const int64_t main_rows = main_wgs * (W * 32) < q_rows ? main_wgs * (W * 32) : q_rows;
+  if (main_wgs > 0) {
+    hipLaunchKernelGGL(kern, dim3((unsigned)main_wgs, (unsigned)p.splits), dim3(W * 64), lds, st,
+                       a, q_begin, main_rows);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (tail) {
+    tail->q0 = parts > 1 ? main_rows : q_rows;
+    tail->parts = parts;
+  }
+  if (parts == 1) return hipSuccess;
+  Args b = a;
+  b.partial = a.ptail;
+  b.parts = parts;
+  hipLaunchKernelGGL(kern, dim3((unsigned)(wgs - main_wgs), (unsigned)parts), dim3(W * 64), lds,
+                     st, b, q_begin + main_rows, q_rows - main_rows);
   return hipGetLastError();
 }
 
 template <typename ET, int DPAD, bool FOLD>
 hipError_t launch_mtile_r(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                          hipStream_t st) {
+                          hipStream_t st, TileTail* tail) {
   switch (p.kprime) {
-    case 16: return launch_mtile<ET, DPAD, FOLD, 8>(p, a, q_begin, q_rows, st);
-    case 32: return launch_mtile<ET, DPAD, FOLD, 16>(p, a, q_begin, q_rows, st);
-    case 64: return launch_mtile<ET, DPAD, FOLD, 32>(p, a, q_begin, q_rows, st);
+    case 16: return launch_mtile<ET, DPAD, FOLD, 8>(p, a, q_begin, q_rows, st, tail);
+    case 32: return launch_mtile<ET, DPAD, FOLD, 16>(p, a, q_begin, q_rows, st, tail);
+    case 64: return launch_mtile<ET, DPAD, FOLD, 32>(p, a, q_begin, q_rows, st, tail);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <typename ET>
 hipError_t launch_mtile_any(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                            hipStream_t st) {
-  if (p.fold) return p.dpad_t == 16 ? launch_mtile_r<ET, 16, true>(p, a, q_begin, q_rows, st)
+                            hipStream_t st, TileTail* tail) {
+  if (p.fold) return p.dpad_t == 16 ? launch_mtile_r<ET, 16, true>(p, a, q_begin, q_rows, st, tail)
                                     : hipErrorInvalidValue;
   switch (p.dpad_t) {
-    case 16: return launch_mtile_r<ET, 16, false>(p, a, q_begin, q_rows, st);
-    case 32: return launch_mtile_r<ET, 32, false>(p, a, q_begin, q_rows, st);
-    case 64: return launch_mtile_r<ET, 64, false>(p, a, q_begin, q_rows, st);
-    case 128: return launch_mtile_r<ET, 128, false>(p, a, q_begin, q_rows, st);
-    case 256: return launch_mtile_r<ET, 256, false>(p, a, q_begin, q_rows, st);
-    case 512: return launch_mtile_r<ET, 512, false>(p, a, q_begin, q_rows, st);
+    case 16: return launch_mtile_r<ET, 16, false>(p, a, q_begin, q_rows, st, tail);
+    case 32: return launch_mtile_r<ET, 32, false>(p, a, q_begin, q_rows, st, tail);
+    case 64: return launch_mtile_r<ET, 64, false>(p, a, q_begin, q_rows, st, tail);
+    case 128: return launch_mtile_r<ET, 128, false>(p, a, q_begin, q_rows, st, tail);
+    case 256: return launch_mtile_r<ET, 256, false>(p, a, q_begin, q_rows, st, tail);
+    case 512: return launch_mtile_r<ET, 512, false>(p, a, q_begin, q_rows, st, tail);
     default: return hipErrorInvalidValue;
   }
 }

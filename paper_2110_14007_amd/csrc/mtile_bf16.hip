@@ -4,8 +4,8 @@
 namespace tod {
 
 hipError_t launch_mtile_bf16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                          hipStream_t s) {
-  return mt::launch_mtile_any<__bf16>(p, a, q_begin, q_rows, s);
+                          hipStream_t s, TileTail* tail) {
+  return mt::launch_mtile_any<__bf16>(p, a, q_begin, q_rows, s, tail);
 }
 
 }  // namespace tod

@@ -212,14 +212,18 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     const int64_t qi = a.perm ? (int64_t)a.perm[qpos] : qpos;
     const double ni = a.n64_q[qpos], rho_i = a.rho_q[qpos];
     // Final aggregation of the per-split candidate lists (Section 6.1).
-    const uint64_t* src = a.partial + ql * a.splits * KP;
+    // Rows of the tail split have one list per scanned piece.
+    const bool tl = ql >= a.tail_q0;
+    const int nlists = tl ? a.tail_parts : a.splits;
+    const uint64_t* src =
+        tl ? a.ptail + (ql - a.tail_q0) * a.tail_parts * KP : a.partial + ql * a.splits * KP;
     uint64_t list[EL];
 #pragma unroll
     for (int r = 0; r < EL; ++r) {
       const int e = r * 64 + lane;
       list[r] = e < KP ? src[e] : kEmpty;
     }
-    for (int s = 1; s < a.splits; ++s) {
+    for (int s = 1; s < nlists; ++s) {
       uint64_t other[EL];
 #pragma unroll
       for (int r = 0; r < EL; ++r) {
@@ -508,10 +512,10 @@ hipError_t launch_recheck_t(const Args& a, int64_t q_begin, int64_t q_rows, hipS
 }  // namespace
 
 hipError_t launch_tile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                       hipStream_t st) {
+                       hipStream_t st, TileTail* tail) {
   if (p.tile_kind == 1) {
-    if (p.precision == TOD_PREC_FP16) return launch_mtile_f16(p, a, q_begin, q_rows, st);
-    if (p.precision == TOD_PREC_BF16) return launch_mtile_bf16(p, a, q_begin, q_rows, st);
+    if (p.precision == TOD_PREC_FP16) return launch_mtile_f16(p, a, q_begin, q_rows, st, tail);
+    if (p.precision == TOD_PREC_BF16) return launch_mtile_bf16(p, a, q_begin, q_rows, st, tail);
     return hipErrorInvalidValue;
   }
   switch (p.precision) {

@@ -38,12 +38,48 @@ struct Plan {
   int32_t lists;       // int32 / fp64 neighbour lists kept in the workspace (LOF, score
                        // aggregates, classifier)
   int32_t order;       // 1: grouped scan order (order.hip), X against X only
+  int32_t tail_parts = 1;  // most parts a tail workgroup's scan is cut into (1: no tail split)
+  int32_t tail_auto = 0;   // 1: pick the parts by the model in tail_pieces; 0: use tail_parts
+  int64_t tail_lists = 0;  // K' lists the tail region holds (query rows x parts)
 };
+
+// Pieces for the tail split of a launch whose last round holds tw of the
+// `slots` workgroups the GPU runs at once (tw = 0: no partial round) on `cus`
+// compute units.  P pieces make tw P work items of 1/P of a scan each, which
+// take ceil(tw P / slots) rounds of 1/P.  Every extra piece costs its rows a
+// list filled from nothing and one more list to merge, charged at 2% of a
+// round.  The planner splits only a tail that leaves some compute unit idle
+// (tw < cus): a tail with a workgroup on every unit runs each of them faster
+// than a full round does, and splitting it was measured slower.  At most
+// pmax pieces, at least 4 stages per piece, and the tail rows' lists must fit
+// the tail region.  Without the planner (automatic = false) the most pieces
+// these limits allow, up to pmax.
+inline int tail_pieces(int64_t tw, int64_t slots, int64_t cus, int pmax, bool automatic,
+                       int64_t nst, int64_t cap_lists, int64_t tail_rows) {
+  if (tw <= 0 || slots <= 0 || tail_rows <= 0) return 1;
+  if (automatic && tw >= cus) return 1;
+  int best = 1;
+  double best_cost = 1.0;
+  for (int P = 2; P <= pmax; ++P) {
+    if (nst < 4 * P || tail_rows * P > cap_lists) break;
+    if (!automatic) {
+      best = P;
+      continue;
+    }
+    const double rounds = (double)((tw * P + slots - 1) / slots);
+    const double cost = rounds / P + 0.02 * (P - 1);
+    if (cost < best_cost - 1e-9) {
+      best = P;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
 
 // Workspace regions (byte offsets from the workspace base, 256-aligned).
 struct Layout {
-  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, worklist, fbpart,
-      fbidx, idx32, d64, lrd, perm, lab, cstart, bcnt, boff, total;
+  size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, ptail, worklist,
+      fbpart, fbidx, idx32, d64, lrd, perm, lab, cstart, bcnt, boff, total;
   int32_t colpart_blocks;
 };
 
@@ -88,6 +124,15 @@ struct Args {
   double* rho_q;    // quantisation radius per query, rounded up [nq_pad]
   double* rho_r;    // quantisation radius per reference when the sets differ (NWR), else null
   uint64_t* partial;   // per (query in block, split) sorted K' lists
+  // Tail split (register-list tile, one reference split): a tile launch with
+  // parts > 1 scans the references in `parts` pieces of the scan order, piece
+  // blockIdx.y, and writes list (query, piece) at partial + (query * parts +
+  // piece) * K'.  The recheck takes the rows of its block from tail_q0 on
+  // from ptail, tail_parts lists each.
+  int32_t parts;
+  int32_t tail_parts;
+  int64_t tail_q0;
+  uint64_t* ptail;
   int32_t* worklist;   // global query ids that failed the certificate
   uint2* fbpart;       // fallback chunk lists: (D^2 bits hi, lo) [kFbGrid x k]
   uint32_t* fbidx;     // fallback chunk lists: reference ids [kFbGrid x k]
@@ -213,8 +258,15 @@ int32_t colsum_blocks(int64_t nr);
 
 // Kernel launchers (return hipSuccess or the launch error).
 hipError_t launch_prep(const Plan& p, const Args& a, hipStream_t s);
+// Query rows of a block from q0 on scanned in `parts` pieces (the tail split).
+struct TileTail {
+  int64_t q0;
+  int32_t parts;
+};
+// The register-list tile fills *tail (no tail split: q0 = q_rows, parts = 1);
+// the other tile kernels leave it untouched.
 hipError_t launch_tile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                       hipStream_t s);
+                       hipStream_t s, TileTail* tail);
 hipError_t launch_tile_f32(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                            hipStream_t s);
 hipError_t launch_tile_f16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
@@ -222,9 +274,9 @@ hipError_t launch_tile_f16(const Plan& p, const Args& a, int64_t q_begin, int64_
 hipError_t launch_tile_bf16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                             hipStream_t s);
 hipError_t launch_mtile_f16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                            hipStream_t s);
+                            hipStream_t s, TileTail* tail);
 hipError_t launch_mtile_bf16(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
-                             hipStream_t s);
+                             hipStream_t s, TileTail* tail);
 hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                           hipStream_t s);
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);

@@ -48,6 +48,7 @@ class tod_options(ctypes.Structure):
         ("no_recheck", ctypes.c_int32),
         ("reorder", ctypes.c_int32),
         ("score", ctypes.c_int32),
+        ("tail_parts", ctypes.c_int32),
     ]
 
 
@@ -72,6 +73,8 @@ class tod_stats(ctypes.Structure):
         ("pairs_candidate", ctypes.c_int64),
         ("pairs_uncertain", ctypes.c_int64),
         ("pairs_in_range", ctypes.c_int64),
+        ("tail_parts", ctypes.c_int32),
+        ("tail_rows", ctypes.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -147,7 +150,7 @@ def last_error() -> str:
 
 def options(precision="auto", exclude_self=False, shortlist=0, query_block=0, ref_splits=0,
             margin_scale=1.0, force_fallback=False, no_recheck=False, reorder=0,
-            score="kth") -> tod_options:
+            score="kth", tail_parts=0) -> tod_options:
     o = tod_options()
     _lib.tod_default_options(ctypes.byref(o))
     o.precision = PRECISIONS[precision] if isinstance(precision, str) else int(precision)
@@ -160,6 +163,7 @@ def options(precision="auto", exclude_self=False, shortlist=0, query_block=0, re
     o.no_recheck = int(bool(no_recheck))
     o.reorder = int(reorder)
     o.score = SCORES[score] if isinstance(score, str) else int(score)
+    o.tail_parts = int(tail_parts)
     return o
 
 

@@ -91,7 +91,8 @@ def test_exclude_self_needs_same_set(tod):
 
 def test_bad_options_rejected(tod):
     for kw in (dict(precision=7), dict(shortlist=300), dict(shortlist=-1), dict(ref_splits=65),
-               dict(margin_scale=0.5), dict(query_block=-3)):
+               dict(margin_scale=0.5), dict(query_block=-3), dict(tail_parts=9),
+               dict(tail_parts=-1)):
         o = tod.options()
         for key, v in kw.items():
             setattr(o, key, v)

@@ -76,3 +76,29 @@ def test_reorder_rule(tod):
                             tod.options(precision="fp32", exclude_self=True))["reordered"]
     with pytest.raises(tod.TodError):
         tod.tod_plan(100, 100, 4, 3, tod.options(reorder=2))
+
+
+def test_tail_region_in_workspace(tod):
+    """The register-list tile with one reference split reserves the tail
+    split's lists (query rows x 8 pieces, at most 2^18 lists of K' entries);
+    tail_parts = 1 or a path without the tail split reserves none."""
+    n, d, k = 100_000, 32, 20  # K' = 32, one split
+    full = tod.tod_workspace_size(n, n, d, k, 1, tod.options(precision="fp16"))
+    off = tod.tod_workspace_size(n, n, d, k, 1, tod.options(precision="fp16", tail_parts=1))
+    lists = min(((n + 31) // 32 * 32) * 8, 1 << 18)
+    assert full - off == lists * 32 * 8
+    three = tod.tod_workspace_size(n, n, d, k, 1, tod.options(precision="fp16", tail_parts=3))
+    assert three - off == min(((n + 31) // 32 * 32) * 3, 1 << 18) * 32 * 8
+    small = 5000  # below the cap: the query rows times the pieces
+    two = tod.tod_workspace_size(small, small, d, k, 1, tod.options(precision="fp16", tail_parts=2,
+                                                                    ref_splits=1))
+    none = tod.tod_workspace_size(small, small, d, k, 1, tod.options(precision="fp16",
+                                                                     tail_parts=1, ref_splits=1))
+    assert two - none == ((small + 31) // 32 * 32) * 2 * 32 * 8
+    # fp32 filter (no register-list tile) and several reference splits: no tail region
+    for o in (tod.options(precision="fp32"), tod.options(precision="fp32", tail_parts=1)):
+        assert tod.tod_workspace_size(n, n, d, k, 1, o) == tod.tod_workspace_size(
+            n, n, d, k, 1, tod.options(precision="fp32", tail_parts=1))
+    assert tod.tod_workspace_size(n, n, d, k, 1, tod.options(precision="fp16", ref_splits=4)) == \
+        tod.tod_workspace_size(n, n, d, k, 1, tod.options(precision="fp16", ref_splits=4,
+                                                          tail_parts=1))
