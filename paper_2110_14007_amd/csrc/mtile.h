@@ -104,6 +104,17 @@ __device__ __forceinline__ void dl_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// f(std::integral_constant<int, 0>{}), ..., f(<N - 1>): a loop whose index is
+// a constant in every iteration, so that arrays indexed by it stay in
+// registers.
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
 // Value of v in the partner lane (lane ^ 32).
 __device__ __forceinline__ uint32_t xchg32(uint32_t v, int h) {
   const auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
@@ -280,16 +291,35 @@ struct Layout {
 // consecutive rows over distinct LDS banks.
 __device__ __forceinline__ int swz(int r) { return ((r >> 2) ^ (r >> 3)) & 1; }
 
-// Stage buffers: rows of 512 elements are staged directly into LDS two
-// stages ahead (three buffers); other rows through registers (two buffers).
-__host__ __device__ constexpr int stage_buffers(int dpad, bool fold) {
-  return dpad >= 512 && !fold ? 3 : 2;
+// Stage buffers: rows of 512 elements are staged directly into LDS, two
+// stages ahead (three buffers) for waves of 32 queries and one stage ahead
+// (two buffers, stages twice as long) for waves of 64; other rows through
+// registers (two buffers).
+__host__ __device__ constexpr int stage_buffers(int dpad, bool fold, int nq) {
+  return dpad >= 512 && !fold && nq == 1 ? 3 : 2;
 }
 
-__host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int ns, int qcap) {
-  return (size_t)stage_buffers(dpad, fold) * 32 * ns * (dpad == 16 ? 32 : dpad * 2 + 16) +
-         (fold ? 0 : (size_t)stage_buffers(dpad, fold) * 32 * ns * sizeof(float)) +
-         (size_t)w * qcap * 64 * sizeof(uint2);
+// Query columns per wave: 64 (two 32-query groups sharing every A fragment)
+// for rows of 512 elements with lists of up to 32 entries, whose 32-step MFMA
+// chains otherwise need one LDS fragment per MFMA; 32 otherwise.  The two
+// groups' operands take all 256 AGPRs; 64-entry lists for two groups (128
+// VGPRs) then leave the compiler too few registers, and it spills part of
+// the operand to scratch memory.
+__host__ __device__ constexpr int query_groups(int dpad, bool fold, int r) {
+  return dpad >= 512 && !fold && r <= 16 ? 2 : 1;
+}
+
+// Queue slots per lane and query group (two groups: 16 slots, the LDS of two
+// 24-slot queues per wave does not fit beside the stages).
+template <int R, int NQ>
+constexpr int queue_slots() { return NQ == 1 ? queue_cap<R>() : 16; }
+
+// Stage buffers, their seeds and the queues.
+__host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int ns, int qcap,
+                                               int nq) {
+  return (size_t)stage_buffers(dpad, fold, nq) * 32 * ns * (dpad == 16 ? 32 : dpad * 2 + 16) +
+         (fold ? 0 : (size_t)stage_buffers(dpad, fold, nq) * 32 * ns * sizeof(float)) +
+         (size_t)w * nq * qcap * 64 * sizeof(uint2);
 }
 
 // At least two waves per SIMD for lists of up to 32 entries and rows of up to
@@ -304,16 +334,17 @@ __host__ __device__ constexpr int min_waves() {
   return R >= 32 || DPAD >= 256 ? 1 : (DPAD == 16 && R <= 8 ? 3 : 2);
 }
 
-template <typename ET, int DPAD, bool FOLD, int R, int W, int NS, int NG>
+template <typename ET, int DPAD, bool FOLD, int R, int W, int NS, int NG, int NQ>
 __global__ void __launch_bounds__(W * 64)
     __attribute__((amdgpu_waves_per_eu(min_waves<DPAD, R>())))
 mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   using V = typename Frag<ET>::V;
   using LY = Layout<DPAD, FOLD>;
-  constexpr int kQCap = queue_cap<R>();
+  static_assert(NQ == 1 || (NG == 1 && LY::wide), "two query groups: wide rows, one sub-tile");
+  constexpr int kQCap = queue_slots<R, NQ>();
   constexpr int KC = LY::k16;
   constexpr bool kInterleave = NG == 1 && KC >= 16;
-  constexpr int kAhead = 4;
+  constexpr int kAhead = NQ > 1 ? 2 : 4;  // A fragments in flight ahead of the MFMA chain
   constexpr int ROWB = LY::rowb;
   constexpr bool SWZ = ROWB == 32;
   constexpr int TR = 32 * NS;  // reference rows per stage
@@ -323,8 +354,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   constexpr int NT = W * 64;
   constexpr int NL = (CHUNKS + NT - 1) / NT;
   static_assert(NL <= 16, "staged chunks per thread");
-  constexpr bool DL = stage_buffers(DPAD, FOLD) == 3;  // direct staging, two stages ahead
-  constexpr int NBUF = stage_buffers(DPAD, FOLD);
+  constexpr bool DL = DPAD >= 512 && !FOLD;  // direct staging
+  constexpr int NBUF = stage_buffers(DPAD, FOLD, NQ);
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* stage = smem;
   float* hnb = (float*)(smem + NBUF * STAGE);  // plain layout: seeds of the staged rows
@@ -333,12 +364,13 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, col = lane & 31;
   if (a.ctrl->nonfinite) return;  // uniform over the grid
-  const uint2* myq_r = qbase + wave * kQCap * 64 + lane;
-  uint2* myq = qbase + wave * kQCap * 64 + lane;
+  // This lane's queue of query group u: qbase + ((wave NQ + u) kQCap + i) 64 + lane.
+  uint2* const myq0 = qbase + wave * NQ * kQCap * 64 + lane;
 
+  // The wave's queries: NQ groups of 32 from q0 on (group u: q0 + 32 u ..).
   const int64_t group = (int64_t)blockIdx.x * W + wave;
-  const bool active = group * 32 < q_rows;  // uniform per wave
-  const int64_t q0 = q_begin + group * 32;
+  const bool active = group * 32 * NQ < q_rows;  // uniform per wave
+  const int64_t q0 = q_begin + group * 32 * NQ;
   // blockIdx.y: the reference split, or with the tail split (a.parts > 1,
   // one split) the piece of the scan order this workgroup takes.
   const int split = blockIdx.y;
@@ -348,13 +380,20 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   const int64_t r_end32 = (r_end + 31) & ~(int64_t)31;  // rows < r_end32 exist (padded copy)
   const bool selfq = a.exclude_self != 0;
 
-  // Query operand: 32 queries, lane holds column col, k-half h; in the fold
-  // layout the seed columns carry the constant c.
-  V bq[KC];
+  // Query operand: NQ groups of 32 queries, lane holds column col, k-half h;
+  // in the fold layout the seed columns carry the constant c.  A group past
+  // the block's rows loads the first group's rows (its lists are never written).
+  V bq[NQ][KC];
   {
-    const ET* qrow = (const ET*)a.xq_q + (active ? q0 + col : 0) * (int64_t)DPAD;
 #pragma unroll
-    for (int c = 0; c < KC; ++c) bq[c] = *reinterpret_cast<const V*>(qrow + 16 * c + 8 * h);
+    for (int u = 0; u < NQ; ++u) {
+      const bool live = active && group * 32 * NQ + 32 * u < q_rows;
+      const ET* qrow = (const ET*)a.xq_q + (live ? q0 + 32 * u + col : active ? q0 + col : 0) *
+                                               (int64_t)DPAD;
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+        bq[u][c] = *reinterpret_cast<const V*>(qrow + 16 * c + 8 * h);
+    }
     if constexpr (LY::wide) {
       // One wave per SIMD: the operand lives in AGPRs, which the MFMA reads
       // as its B operand directly.  Left to itself the compiler keeps it in
@@ -362,7 +401,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       // copies it back before every MFMA (about 110 copies per sub-tile at
       // rows of 512 elements).
 #pragma unroll
-      for (int c = 0; c < KC; ++c) asm volatile("" : "+a"(bq[c]));
+      for (int u = 0; u < NQ; ++u)
+#pragma unroll
+        for (int c = 0; c < KC; ++c) asm volatile("" : "+a"(bq[u][c]));
     }
     if constexpr (FOLD) {
       const ET cf = (ET)(float)fold_const(std::is_same<ET, _Float16>::value ? TOD_PREC_FP16
@@ -371,16 +412,23 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         V v;
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = e < 4 ? cf : (ET)0.0f;
-        bq[0] = v;
+        bq[0][0] = v;
       }
     }
   }
 
-  uint64_t L[R];
+  // Per query group u: the list, the threshold (a pair survives iff acc >
+  // thr[u]) and the entries in this lane's queue.
+  uint64_t L[NQ][R];
+  float thr[NQ];
+  int cnt[NQ];
 #pragma unroll
-  for (int i = 0; i < R; ++i) L[i] = kEmpty;
-  float thr = -INFINITY;  // a pair survives iff acc > thr
-  int cnt = 0;            // entries in this lane's queue
+  for (int u = 0; u < NQ; ++u) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) L[u][i] = kEmpty;
+    thr[u] = -INFINITY;
+    cnt[u] = 0;
+  }
 
   // Stage staging: every thread moves up to NL 16-byte chunks.  Rows past the
   // split's padded end are clamped to its last row: they are loaded but never
@@ -429,8 +477,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // 32-bit scalar compares; the row limit is one value per sub-tile (rows >=
   // lim are past the split).
   const uint32_t q0u = (uint32_t)q0, endu = (uint32_t)r_end;
-  auto mask = [&](f32x16& v, uint32_t ts) {
-    const bool diag = selfq && ts == q0u;
+  // qu: first query of the accumulator's query group.
+  auto mask = [&](f32x16& v, uint32_t ts, uint32_t qu) {
+    const bool diag = selfq && ts == qu;
     const uint32_t rem = ts < endu ? endu - ts : 0u;
     if (diag || rem < 32u) {
       const int lim = rem < 32u ? (int)rem : 32;
@@ -450,15 +499,18 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   };
   // Merge the first kMerge queue entries of every lane into the lists, move
   // the rest (at most kQCap - kMerge) to the front and tighten the threshold.
-  auto flush = [&]() __attribute__((always_inline)) {
-    merge_queues<R>(L, myq_r, cnt, h);
+  // (U: std::integral_constant of the query group.)
+  auto flush = [&](auto U) __attribute__((always_inline)) {
+    constexpr int u = decltype(U)::value;
+    uint2* const myq = myq0 + u * kQCap * 64;
+    merge_queues<R>(L[u], myq, cnt[u], h);
 #pragma unroll
     for (int i = kMerge; i < kQCap; ++i)
-      if (i < cnt) myq[(i - kMerge) * 64] = myq_r[i * 64];
-    cnt = cnt > kMerge ? cnt - kMerge : 0;
-    const uint64_t last = L[R - 1];
+      if (i < cnt[u]) myq[(i - kMerge) * 64] = myq[i * 64];
+    cnt[u] = cnt[u] > kMerge ? cnt[u] - kMerge : 0;
+    const uint64_t last = L[u][R - 1];
     const uint64_t t = xchg64(last, h);
-    thr = thr_of(h ? last : t);
+    thr[u] = thr_of(h ? last : t);
   };
   // Append this lane's survivors of a sub-tile to its queue.
   //   16-slot queue: half a sub-tile at a time, merging whenever the half
@@ -469,34 +521,40 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // An append writes the next free slot unconditionally and advances the
   // count only for a survivor (no exec-mask branch per value); the room made
   // beforehand keeps every written slot inside the queue.
-  auto insert = [&](const f32x16& v, uint32_t ts) __attribute__((always_inline)) {
+  // (v by value, halves as whole vectors: a per-element choice between
+  // v[r] and v[8 + r] on a loop counter can become a dynamic index, which
+  // puts the accumulators in scratch memory.)
+  auto insert = [&](auto U, const f32x16 v, uint32_t ts) __attribute__((always_inline)) {
+    constexpr int u = decltype(U)::value;
+    uint2* const myq = myq0 + u * kQCap * 64;
     if constexpr (kQCap == 16) {
+      typedef float f32x8 __attribute__((ext_vector_type(8)));
+      const f32x8 lo = __builtin_shufflevector(v, v, 0, 1, 2, 3, 4, 5, 6, 7);
+      const f32x8 hi = __builtin_shufflevector(v, v, 8, 9, 10, 11, 12, 13, 14, 15);
 #pragma unroll 1
       for (int hf = 0; hf < 2; ++hf) {
-        float cur[8];
-#pragma unroll
-        for (int r = 0; r < 8; ++r) cur[r] = hf ? v[8 + r] : v[r];
+        const f32x8 cur = hf ? hi : lo;
         const float mh = max3f(max3f(cur[0], cur[1], cur[2]), max3f(cur[3], cur[4], cur[5]),
                                max3f(cur[6], cur[7], cur[7]));
-        if (!__ballot(mh > thr)) continue;
-        if (__ballot(cnt > kQCap - 8)) flush();
+        if (!__ballot(mh > thr[u])) continue;
+        if (__ballot(cnt[u] > kQCap - 8)) flush(U);
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-          myq[cnt * 64] =
+          myq[cnt[u] * 64] =
               make_uint2(__float_as_uint(cur[r]), (uint32_t)(ts + out_row(8 * hf + r, h)));
-          cnt += cur[r] > thr ? 1 : 0;
+          cnt[u] += cur[r] > thr[u] ? 1 : 0;
         }
       }
     } else {
-      if (__ballot(cnt > kQCap - 16)) flush();
+      if (__ballot(cnt[u] > kQCap - 16)) flush(U);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const float mq = max3f(max3f(v[4 * q], v[4 * q + 1], v[4 * q + 2]), v[4 * q + 3], v[4 * q + 3]);
-        if (__ballot(mq > thr)) {
+        if (__ballot(mq > thr[u])) {
 #pragma unroll
           for (int r = 4 * q; r < 4 * q + 4; ++r) {
-            myq[cnt * 64] = make_uint2(__float_as_uint(v[r]), (uint32_t)(ts + out_row(r, h)));
-            cnt += v[r] > thr ? 1 : 0;
+            myq[cnt[u] * 64] = make_uint2(__float_as_uint(v[r]), (uint32_t)(ts + out_row(r, h)));
+            cnt[u] += v[r] > thr[u] ? 1 : 0;
           }
         }
       }
@@ -535,7 +593,11 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     const int live = avail < (uint32_t)TR ? (int)((avail + 31) >> 5) : NS;
     // Only a stage holding the diagonal sub-tile or the split's end needs the
     // masking code; the test is made once per stage, on scalars.
-    const bool smask = (selfq && q0u - t0u < (uint32_t)TR) || avail < (uint32_t)TR;
+    // (Query group u's diagonal sub-tile starts at row q0 + 32 u.)
+    bool diag_here = false;
+#pragma unroll
+    for (int u = 0; u < NQ; ++u) diag_here = diag_here || q0u + 32u * u - t0u < (uint32_t)TR;
+    const bool smask = (selfq && diag_here) || avail < (uint32_t)TR;
     // Fast path over NG sub-tiles (independent MFMA chains, one reduction),
     // with no insertion code.  All A fragments and seeds of the group are read
     // before the first MFMA, so that one LDS round trip covers the group's
@@ -543,43 +605,69 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     // with) keep kAhead fragments in flight ahead of the MFMA chain instead:
     // the LDS reads of later k-steps then run under the MFMAs of earlier ones.
     auto group = [&](int g0) __attribute__((always_inline)) {
+      constexpr std::integral_constant<int, 0> Z{};
       V af[NG][KC];
-      f32x16 acc[NG];
+      f32x16 acc[NG][NQ];
 #pragma unroll
       for (int s = 0; s < NG; ++s) {
 #pragma unroll
         for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
-        acc[s] = seed(hn, g0 + s);
+        acc[s][0] = seed(hn, g0 + s);
+#pragma unroll
+        for (int u = 1; u < NQ; ++u) acc[s][u] = acc[s][0];
       }
+      // Every A fragment feeds the MFMAs of all NQ query groups.
 #pragma unroll
       for (int c = 0; c < KC; ++c)
 #pragma unroll
-        for (int s = 0; s < NG; ++s) acc[s] = mfma<ET>(af[s][c], bq[c], acc[s]);
+        for (int s = 0; s < NG; ++s)
+#pragma unroll
+          for (int u = 0; u < NQ; ++u) acc[s][u] = mfma<ET>(af[s][c], bq[u][c], acc[s][u]);
       if constexpr (kInterleave) {
         __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
 #pragma unroll
         for (int c = 0; c < KC - kAhead; ++c) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, NQ, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NQ * kAhead, 0);
       } else {
         __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, NG * KC, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NG * NQ * KC, 0);
       }
-      // Masks first (one branch per group), then the NG independent max
+      // Masks first (one branch per group), then the NG x NQ independent max
       // trees, which the scheduler interleaves.
       if (smask) {
 #pragma unroll
-        for (int s = 0; s < NG; ++s) mask(acc[s], t0u + 32u * (uint32_t)(g0 + s));
+        for (int s = 0; s < NG; ++s)
+#pragma unroll
+          for (int u = 0; u < NQ; ++u)
+            mask(acc[s][u], t0u + 32u * (uint32_t)(g0 + s), q0u + 32u * (uint32_t)u);
       }
-      float ms[NG];
+      float ms[NG][NQ];
 #pragma unroll
-      for (int s = 0; s < NG; ++s) ms[s] = max16(acc[s]);  // past the split: fully masked
-      float m = ms[0];
+      for (int s = 0; s < NG; ++s)
 #pragma unroll
-      for (int s = 1; s < NG; s += 2) m = max3f(m, ms[s], ms[s + 1 < NG ? s + 1 : s]);
-      if (!__ballot(m > thr)) return;
+        for (int u = 0; u < NQ; ++u) ms[s][u] = max16(acc[s][u]);  // past the split: fully masked
+      if constexpr (NQ > 1) {
+        // One sub-tile, NQ query groups: insert each group's survivors from
+        // its accumulators.
+        bool any = false;
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) any = any || ms[0][u] > thr[u];
+        if (!__ballot(any)) return;
+        uint32_t ts = t0u + 32u * (uint32_t)g0;
+        asm volatile("" : "+s"(ts));  // ids formed here (see below)
+        static_assert(NQ == 2, "two query groups");
+        constexpr std::integral_constant<int, 1> One{};
+        if (__ballot(ms[0][0] > thr[0])) insert(Z, acc[0][0], ts);
+        if (__ballot(ms[0][1] > thr[1])) insert(One, acc[0][1], ts);
+        return;
+      }
+      float m = ms[0][0];
+#pragma unroll
+      for (int s = 1; s < NG; s += 2) m = max3f(m, ms[s][0], ms[s + 1 < NG ? s + 1 : s][0]);
+      if (!__ballot(m > thr[0])) return;
       // Slow path: sub-tile by sub-tile.  Rows of several k-steps reuse the
       // group's accumulators, one copy of the insertion code per sub-tile (a
       // recomputation would put its LDS reads and MFMA chain on the latency
@@ -591,32 +679,32 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       if constexpr (NG > 1 && KC >= 2) {
 #pragma unroll
         for (int s = 0; s < NG; ++s) {
-          if (s >= gl || !__ballot(ms[s] > thr)) continue;
+          if (s >= gl || !__ballot(ms[s][0] > thr[0])) continue;
           uint32_t ts = t0u + 32u * (uint32_t)(g0 + s);
           asm volatile("" : "+s"(ts));  // ids formed here (see below)
-          insert(acc[s], ts);
+          insert(Z, acc[s][0], ts);
         }
         return;
       }
 #pragma unroll 1
       for (int s = 0; s < gl; ++s) {
-        float msel = ms[0];
+        float msel = ms[0][0];
 #pragma unroll
-        for (int u = 1; u < NG; ++u) msel = s == u ? ms[u] : msel;
-        if (!__ballot(msel > thr)) continue;
+        for (int u = 1; u < NG; ++u) msel = s == u ? ms[u][0] : msel;
+        if (!__ballot(msel > thr[0])) continue;
         uint32_t ts = t0u + 32u * (uint32_t)(g0 + s);
         // Opaque to the optimizer: otherwise it carries the 16 row ids
         // ts + out_row(r, h) through the fast path as per-lane induction
         // variables (16 additions per sub-tile) instead of forming them here.
         asm volatile("" : "+s"(ts));
         if constexpr (NG == 1) {
-          insert(acc[0], ts);
+          insert(Z, acc[0][0], ts);
         } else {
           f32x16 a1 = seed(hn, g0 + s);
 #pragma unroll
-          for (int c = 0; c < KC; ++c) a1 = mfma<ET>(afrag(buf, g0 + s, c), bq[c], a1);
-          if (smask) mask(a1, ts);
-          insert(a1, ts);
+          for (int c = 0; c < KC; ++c) a1 = mfma<ET>(afrag(buf, g0 + s, c), bq[0][c], a1);
+          if (smask) mask(a1, ts, q0u);
+          insert(Z, a1, ts);
         }
       }
     };
@@ -635,7 +723,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   const int nst = (int)((r_end - r_begin + TR - 1) / TR);
   int st0 = 0;
   if (a.cstart) {
-    const int p0 = (int)(q_begin + (int64_t)blockIdx.x * (W * 32));
+    const int p0 = (int)(q_begin + (int64_t)blockIdx.x * (W * 32 * NQ));
     int g = 0;
 #pragma unroll
     for (int i = 1; i < kOrdC; ++i) g = a.cstart[i] <= p0 ? i : g;
@@ -663,7 +751,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   if constexpr (DL) {
     // Rows of 512 elements: each wave moves 8 whole rows (one 1 KiB row per
     // instruction) and 8 seeds of every stage straight into LDS, two stages
-    // ahead, 9 loads per wave per stage.  The compiler-visible wait first
+    // ahead with three buffers, one stage ahead with two, 9 loads per wave
+    // per stage.  The compiler-visible wait first
     // retires the query operand's loads, so that the compiler, which does
     // not see the staging loads, has no load of its own left to wait for.
     static_assert(TR == 8 * W && W == 4, "direct staging: 8 rows and 8 seeds per wave");
@@ -680,14 +769,25 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         dma16((const unsigned char*)(a.hn_r + t0 + 8 * wave) + lane * 16,
               lbase + NBUF * STAGE + (b * TR + 8 * wave) * (int)sizeof(float));
     };
-    dl_issue(t_of(0), 0);
-    dl_issue(t_of(1), 1);
-    dl_barrier<TR / W + 1>();
-    for (int it = 0; it < nscan; ++it) {
-      // Buffer (it + 2) % 3 was last read in trip it - 1, before its barrier.
-      dl_issue(t_of(it + 2), (it + 2) % 3);
-      stage_body(t_of(it), it % 3);
+    if constexpr (NBUF == 3) {
+      dl_issue(t_of(0), 0);
+      dl_issue(t_of(1), 1);
       dl_barrier<TR / W + 1>();
+      for (int it = 0; it < nscan; ++it) {
+        // Buffer (it + 2) % 3 was last read in trip it - 1, before its barrier.
+        dl_issue(t_of(it + 2), (it + 2) % 3);
+        stage_body(t_of(it), it % 3);
+        dl_barrier<TR / W + 1>();
+      }
+    } else {
+      dl_issue(t_of(0), 0);
+      dl_barrier<0>();
+      for (int it = 0; it < nscan; ++it) {
+        // Buffer (it + 1) & 1 was last read in trip it - 1, before its barrier.
+        dl_issue(t_of(it + 1), (it + 1) & 1);
+        stage_body(t_of(it), it & 1);
+        dl_barrier<0>();
+      }
     }
     // No staging write may outlive the workgroup's LDS allocation.
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -725,16 +825,20 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 #undef TOD_MT_FETCH
 #undef TOD_MT_PUT
   if (active) {
-    while (__ballot(cnt > 0)) flush();
-    const int64_t ql = group * 32 + col;
-    if (ql < q_rows) {
-      uint64_t* dst = a.partial + (ql * (pieces ? a.parts : a.splits) + split) * (2 * R) + h * R;
+    static_for<0, NQ>([&](auto U) __attribute__((always_inline)) {
+      constexpr int u = decltype(U)::value;
+      while (__ballot(cnt[u] > 0)) flush(U);
+      const int64_t ql = group * 32 * NQ + 32 * u + col;
+      if (ql < q_rows) {
+        uint64_t* dst =
+            a.partial + (ql * (pieces ? a.parts : a.splits) + split) * (2 * R) + h * R;
 #pragma unroll
-      for (int i = 0; i < R; ++i) {
-        const uint64_t e = L[i];
-        dst[i] = e == kEmpty ? kEmpty : make_entry(-2.0f * acc_of(e), (uint32_t)e);
+        for (int i = 0; i < R; ++i) {
+          const uint64_t e = L[u][i];
+          dst[i] = e == kEmpty ? kEmpty : make_entry(-2.0f * acc_of(e), (uint32_t)e);
+        }
       }
-    }
+    });
   }
 }
 
@@ -747,18 +851,20 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 // P times as many workgroups (tail_pieces picks P), in a second launch whose
 // lists go to the tail region.
 template <typename ET, int DPAD, bool FOLD, int R, int W = 4, int NS = Layout<DPAD, FOLD>::ns,
-          int NG = (DPAD <= 32 ? 4 : 1)>
+          int NG = (DPAD <= 32 ? 4 : 1), int NQ = query_groups(DPAD, FOLD, R)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st, TileTail* tail) {
-  const size_t lds = lds_bytes(DPAD, FOLD, W, NS, queue_cap<R>());
-  const auto kern = mtile_kernel<ET, DPAD, FOLD, R, W, NS, NG>;
+  const size_t lds = lds_bytes(DPAD, FOLD, W, NS, queue_slots<R, NQ>(), NQ);
+  static_assert(lds_bytes(DPAD, FOLD, W, NS, queue_slots<R, NQ>(), NQ) <= 160 * 1024,
+                "LDS per workgroup");
+  const auto kern = mtile_kernel<ET, DPAD, FOLD, R, W, NS, NG, NQ>;
+  constexpr int QW = W * 32 * NQ;  // queries per workgroup
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  const int64_t groups = (q_rows + 31) / 32;
-  const int64_t wgs = (groups + W - 1) / W;
+  const int64_t wgs = (q_rows + QW - 1) / QW;
   int64_t main_wgs = wgs;
   int parts = 1;
   if (p.splits == 1 && p.tail_parts > 1 && a.ptail) {
@@ -770,7 +876,7 @@ hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q
         cus > 0 && per > 0) {
       const int64_t slots = (int64_t)cus * per;
       const int64_t tw = wgs % slots;
-      const int64_t trows = q_rows - (wgs - tw) * (W * 32);
+      const int64_t trows = q_rows - (wgs - tw) * QW;
       const int64_t nst = (a.nr + 32 * NS - 1) / (32 * NS);
       parts = tail_pieces(tw, slots, cus, p.tail_parts, p.tail_auto != 0, nst, p.tail_lists,
                           trows);
@@ -779,7 +885,7 @@ hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q
       (void)hipGetLastError();  // no occupancy figures: no tail split
     }
   }
-  const int64_t main_rows = main_wgs * (W * 32) < q_rows ? main_wgs * (W * 32) : q_rows;
+  const int64_t main_rows = main_wgs * QW < q_rows ? main_wgs * QW : q_rows;
   if (main_wgs > 0) {
     hipLaunchKernelGGL(kern, dim3((unsigned)main_wgs, (unsigned)p.splits), dim3(W * 64), lds, st,
                        a, q_begin, main_rows);

@@ -50,7 +50,7 @@ def run_knn(env, xq, xr, k, **opt):
     return [idx.cpu().numpy(), dist.cpu().numpy()], st.as_dict()
 
 
-@pytest.mark.parametrize("case", ["d32_lof", "d512_bf16", "d8_fold", "d64_fp16"])
+@pytest.mark.parametrize("case", ["d32_lof", "d512_bf16", "d512_fp16", "d8_fold", "d64_fp16"])
 def test_self_pieces_identical(env, case):
     """X against X (self excluded, grouped order): every output identical for
     2, 5 and 8 pieces, the planner's choice and no split; the 8-piece run
@@ -62,6 +62,9 @@ def test_self_pieces_identical(env, case):
     elif case == "d512_bf16":
         x, _ = workloads.generate("C4", n=2600)
         k, prec = 20, "bf16"  # K' = 64
+    elif case == "d512_fp16":
+        x, _ = workloads.generate("C4", n=3100)
+        k, prec = 20, "fp16"  # K' = 32: waves of 64 queries
     elif case == "d8_fold":
         x, _ = workloads.generate("C5", n=20000)
         k, prec = 5, "fp16"
