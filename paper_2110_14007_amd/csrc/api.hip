@@ -217,6 +217,7 @@ Layout make_layout(const Plan& p) {
   L.partial = take(sizeof(uint64_t) * p.query_block * p.splits * p.kprime);
   L.ptail = take(sizeof(uint64_t) * p.tail_lists * p.kprime);
   L.worklist = take(sizeof(int32_t) * p.nq);
+  L.fbtau = take(sizeof(double) * p.nq);
   // Chunk lists exist only when fewer than kFbGrid rows fail, so kFbGrid
   // lists of k entries always suffice.
   L.fbpart = take(sizeof(uint2) * (size_t)tod::kFbGrid * p.k);
@@ -430,6 +431,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.tail_q0 = p.nq;
   a.ptail = p.tail_lists ? (uint64_t*)(base + L.ptail) : nullptr;
   a.worklist = (int32_t*)(base + L.worklist);
+  a.fbtau = (double*)(base + L.fbtau);
   a.fbpart = (uint2*)(base + L.fbpart);
   a.fbidx = (uint32_t*)(base + L.fbidx);
   a.perm = p.order ? (int32_t*)(base + L.perm) : nullptr;

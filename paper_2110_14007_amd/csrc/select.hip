@@ -297,6 +297,7 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     } else if (lane == 0) {
       const uint32_t w = atomicAdd(&a.ctrl->worklist_count, 1u);
       a.worklist[w] = (int32_t)qi;
+      a.fbtau[w] = stau[wave];
     }
     wave_lds_sync();  // the next query reuses this wave's LDS rows
   }
@@ -376,8 +377,20 @@ __global__ void __launch_bounds__(kFbThreads) fallback_scan_kernel(Args a) {
     }
     if (tid == 0) bufcnt = 0;
     __syncthreads();
+    // Only references with D^2 <= tau' can be among the row's k nearest.
+    // tau, the k-th smallest of the D^2 the recheck measured for this row,
+    // bounds the k-th smallest D^2 over all references; the recheck sums in
+    // another order than this scan, and over at most 4096 non-negative terms
+    // the two sums differ by less than 2^-40 relative, so tau' = the next
+    // double above fl(tau (1 + 2^-30)), more than tau (1 + 2^-31), keeps
+    // every one of them.
+    const double tau = a.fbtau[w];
     uint64_t thr_d = kEmpty;
     uint32_t thr_j = 0xffffffffu;
+    if (tau < INFINITY) {
+      const double tp = nextafter(tau * (1.0 + 0x1p-30), INFINITY);
+      thr_d = (uint64_t)__double_as_longlong(tp);
+    }
     const float* qrow = a.xq + qi * d;
     for (int64_t base = j0; base < j1; base += kFbThreads) {
       // Thread tid measures reference base + tid.  The block's rows are read
@@ -430,8 +443,10 @@ __global__ void __launch_bounds__(kFbThreads) fallback_scan_kernel(Args a) {
           kd[i] = kEmpty;
           kj[i] = 0xffffffffu;
         }
-        thr_d = kd[k - 1];
-        thr_j = kj[k - 1];
+        if (lex_less(kd[k - 1], kj[k - 1], thr_d, thr_j)) {
+          thr_d = kd[k - 1];
+          thr_j = kj[k - 1];
+        }
         __syncthreads();
         if (tid == 0) bufcnt = 0;
       }

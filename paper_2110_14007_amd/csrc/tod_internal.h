@@ -79,7 +79,7 @@ inline int tail_pieces(int64_t tw, int64_t slots, int64_t cus, int pmax, bool au
 // Workspace regions (byte offsets from the workspace base, 256-aligned).
 struct Layout {
   size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, ptail, worklist,
-      fbpart, fbidx, idx32, d64, lrd, perm, lab, cstart, bcnt, boff, total;
+      fbtau, fbpart, fbidx, idx32, d64, lrd, perm, lab, cstart, bcnt, boff, total;
   int32_t colpart_blocks;
 };
 
@@ -134,6 +134,7 @@ struct Args {
   int64_t tail_q0;
   uint64_t* ptail;
   int32_t* worklist;   // global query ids that failed the certificate
+  double* fbtau;       // per worklist entry: the k-th smallest exact D^2 the recheck measured
   uint2* fbpart;       // fallback chunk lists: (D^2 bits hi, lo) [kFbGrid x k]
   uint32_t* fbidx;     // fallback chunk lists: reference ids [kFbGrid x k]
   // grouped scan order (all null when the input order is kept)
