@@ -65,10 +65,13 @@ constexpr int kMerge = 16;  // queue entries one merge takes per lane
 
 // Queue slots per lane.  16-entry lists see few insertions: a 16-slot queue
 // filled half a sub-tile at a time keeps LDS small enough for three
-// workgroups per CU.  Longer lists insert often: a 24-slot queue takes a whole
-// sub-tile after at most one merge (which leaves at most 8 entries).
+// workgroups per CU.  Longer lists insert often: a 28-slot queue takes a whole
+// sub-tile after at most one merge (which leaves at most 12 entries), and
+// merges wait until some lane holds 13 entries.  28 slots is the most that
+// keeps two workgroups per CU at rows of 32 and 64 elements; 24 slots merged
+// more often (C2's tile 8% slower), 32 slots left one workgroup per CU.
 template <int R>
-constexpr int queue_cap() { return R <= 8 ? 16 : 24; }
+constexpr int queue_cap() { return R <= 8 ? 16 : 28; }
 
 // Workgroup barrier of the two-stage staging pipeline: this wave's LDS writes
 // are complete before it, and global loads still in flight stay in flight (a
@@ -310,7 +313,7 @@ __host__ __device__ constexpr int query_groups(int dpad, bool fold, int r) {
 }
 
 // Queue slots per lane and query group (two groups: 16 slots, the LDS of two
-// 24-slot queues per wave does not fit beside the stages).
+// 28-slot queues per wave does not fit beside the stages).
 template <int R, int NQ>
 constexpr int queue_slots() { return NQ == 1 ? queue_cap<R>() : 16; }
 
@@ -515,7 +518,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // Append this lane's survivors of a sub-tile to its queue.
   //   16-slot queue: half a sub-tile at a time, merging whenever the half
   //   could overflow it (one merge site: the halves are a loop).
-  //   24-slot queue: room for the whole sub-tile is made first; then each
+  //   28-slot queue: room for the whole sub-tile is made first; then each
   //   quarter costs a max, a compare and a uniform branch unless some lane's
   //   value beats its threshold.
   // An append writes the next free slot unconditionally and advances the
