@@ -31,7 +31,7 @@ namespace tod {
 namespace {
 
 constexpr int kW = 4;  // waves per workgroup, one point per wave at a time
-constexpr int kU = 4;  // pairs per lane in flight
+constexpr int kU = 16;  // pairs per lane in flight
 
 template <int NLM>
 __global__ void __launch_bounds__(kW * 64) loci_count_kernel(LociArgs a) {
