@@ -8,8 +8,9 @@
 //   verify  one wave per row.  An uncertain candidate first gets the
 //           tile's test again with its own reference norm and radius in
 //           place of the maxima (pair_test); the ones still undecided (and
-//           every kept candidate when distances are requested) get the exact
-//           squared distance, computed as in the definition: fp64, columns in order,
+//           every kept candidate when distances are requested) are gathered
+//           in an LDS list and then get, 64 at a time, the exact squared
+//           distance, computed as in the definition: fp64, columns in order,
 //           ((double)x - (double)y)^2 added one at a time with no fused
 //           multiply-add, so the in-range decision D2 <= phi^2 is the same
 //           bit for bit as a plain fp64 evaluation.  Kept candidates get
@@ -54,8 +55,21 @@ __device__ __forceinline__ int pair_test(const Args& a, double s, double gam, do
   return 0;
 }
 
+// Candidates of one row that need their exact distance, gathered per wave
+// so that a row's pairs share one 64-lane pass of the exact sums (a pass
+// costs one sequential chain of d fp64 additions whatever the number of
+// active lanes).
+constexpr int kExactList = 256;
+
+// LDS writes of this wave are visible to its other lanes.
+__device__ __forceinline__ void wave_lds_fence() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_wave_barrier();
+}
+
 __global__ void __launch_bounds__(256)
 range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
+  __shared__ uint32_t xlist[4][kExactList];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = b0 + (int64_t)blockIdx.x * 4 + wave;
   if (row >= b0 + rows) return;  // uniform per wave
@@ -67,7 +81,25 @@ range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
   const double tt = (double)a.d + 2.0;
   const double gam = tt * 0x1p-23 / (1.0 - tt * 0x1p-23);
   const double ni = a.n64_q[row], rho_i = a.rho_q[row];
-  int kept = 0, unc = 0;
+  const uint64_t lt = (1ull << lane) - 1;  // lanes below this one
+  int kept = 0, unc = 0, nx = 0;
+  // Exact pass over the gathered list: entry = (p - beg) << 1 | uncertain.
+  auto exact_pass = [&]() {
+    wave_lds_fence();  // the list's entries are visible to every lane
+    for (int i0 = 0; i0 < nx; i0 += 64) {
+      const bool live = i0 + lane < nx;
+      const uint32_t e = live ? xlist[wave][i0 + lane] : 0u;
+      const int64_t p = beg + (e >> 1);
+      const bool u = (e & 1u) != 0;
+      double d2 = 0.0;
+      if (live) d2 = exact_d2(qrow, a.xr + (int64_t)(a.cand[p] & 0x7fffffffu) * a.d, a.d);
+      const bool keep = live && (!u || d2 <= phi2);
+      if (live) a.cand_d[p] = keep ? (float)sqrt(d2) : -1.0f;
+      kept += __popcll(__ballot(keep));
+    }
+    nx = 0;
+    wave_lds_fence();  // the list is refilled after every lane has read it
+  };
   for (int64_t p0 = beg; p0 < end; p0 += 64) {
     const int64_t p = p0 + lane;
     const bool live = p < end;
@@ -79,13 +111,18 @@ range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
     if (live && (c >> 31) && !a.force_fallback) pt = pair_test(a, s, gam, ni, rho_i, j, a.cand_d[p]);
     const bool u = live && (c >> 31) && pt == 0;
     const bool need = live && (u || (want_dist && pt >= 0));
-    double d2 = 0.0;
-    if (need) d2 = exact_d2(qrow, a.xr + (int64_t)j * a.d, a.d);
-    const bool keep = live && pt >= 0 && (!u || d2 <= phi2);
-    if (live) a.cand_d[p] = keep ? (need ? (float)sqrt(d2) : 0.0f) : -1.0f;
-    kept += __popcll(__ballot(keep));
+    // Decided without the exact distance: in range for certain (distance
+    // not asked for) or out of range.
+    const bool keep_now = live && !need && pt >= 0;
+    if (live && !need) a.cand_d[p] = keep_now ? 0.0f : -1.0f;
+    kept += __popcll(__ballot(keep_now));
     unc += __popcll(__ballot(u));
+    const uint64_t nb = __ballot(need);
+    if (nx + __popcll(nb) > kExactList) exact_pass();
+    if (need) xlist[wave][nx + __popcll(nb & lt)] = (uint32_t)((p - beg) << 1) | (u ? 1u : 0u);
+    nx += __popcll(nb);
   }
+  if (nx) exact_pass();
   if (lane == 0) {
     a.incnt[row] = kept;
     if (unc) atomicAdd((unsigned long long*)&a.ctrl->uncertain, (unsigned long long)unc);
