@@ -344,6 +344,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   using V = typename Frag<ET>::V;
   using LY = Layout<DPAD, FOLD>;
   static_assert(NQ == 1 || (NG == 1 && LY::wide), "two query groups: wide rows, one sub-tile");
+  static_assert(NG <= NS && NS % NG == 0, "fast-path groups tile the stage");
   constexpr int kQCap = queue_slots<R, NQ>();
   constexpr int KC = LY::k16;
   constexpr bool kInterleave = NG == 1 && KC >= 16;
@@ -846,7 +847,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 }
 
 // Sub-tiles per fast-path group: four for rows of up to 32 elements (one
-// k-step or two), one otherwise.
+// k-step or two), two (the whole stage) for rows of 64, one otherwise.  Two
+// independent MFMA chains at 64 took the C3 tile from 198 to 184 ms.
 //
 // Tail split: a block of G workgroups on a GPU that runs S of them at once
 // ends with a round of G mod S workgroups that leaves most of the GPU idle.
@@ -854,7 +856,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 // P times as many workgroups (tail_pieces picks P), in a second launch whose
 // lists go to the tail region.
 template <typename ET, int DPAD, bool FOLD, int R, int W = 4, int NS = Layout<DPAD, FOLD>::ns,
-          int NG = (DPAD <= 32 ? 4 : 1), int NQ = query_groups(DPAD, FOLD, R)>
+          int NG = (DPAD <= 32 ? 4 : (DPAD == 64 ? 2 : 1)), int NQ = query_groups(DPAD, FOLD, R)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st, TileTail* tail) {
   const size_t lds = lds_bytes(DPAD, FOLD, W, NS, queue_slots<R, NQ>(), NQ);
