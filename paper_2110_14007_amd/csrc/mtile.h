@@ -18,7 +18,7 @@
 // the accumulator mapped to an unsigned key that ascends as acc descends, and
 // the reference index below it.  Both lanes keep the acc of entry K'-1 as a
 // threshold; a sub-tile costs a max3 reduction and one compare per lane unless
-// some accumulator beats it.  Survivors are appended to an LDS queue (16 or 24
+// some accumulator beats it.  Survivors are appended to an LDS queue (16 or 28
 // slots) of their lane.  When a queue could overflow, the whole wave merges: every lane
 // sorts its queue, each pair merges its two queues and then the merged queue
 // with its list by bitonic stages whose cross-lane step is v_permlane32_swap.
