@@ -1,9 +1,15 @@
 """Throughput of the kNN-OD / LOF hot path on one MI355X.
 
-One step = one tod_lof call on the whole workload: prep, fused distance tiles
-with top-K' selection, certificate + exact recheck, fallback, kNN-OD score
-and LOF for every point (--detector knn: the kNN score alone; --detector abod
-or cof: ABOD or COF from the same lists).  Inputs are resident in HBM before timing starts.
+With no --workload, the headline line is the largest configuration, C5
+(n = 4,000,000, d = 8, k = 5, kNN-OD), and the line carries C1-C4 as
+sub-results under "configs", each run as its workload specifies it (filter
+precision; LOF where the workload asks for it).
+
+One step = one library call on the whole workload: prep, fused distance tiles
+with top-K' selection, certificate + exact recheck, fallback and the scores
+of every point.  The detector is the workload's own (tod_lof for C1 and C2,
+tod_knn_score for C3-C5) unless --detector says otherwise (knn, lof, abod,
+cof).  Inputs are resident in HBM before timing starts.
 For a neighbours-within-range workload (--workload N1) one step is one
 tod_nwr call as the paper defines the operator (the indices of the pairs in
 range): prep, the range tile's count and fill passes, exact verification of
@@ -37,16 +43,22 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="C2")
-    ap.add_argument("--precision", default="auto")
-    ap.add_argument("--detector", default="lof", choices=("lof", "knn", "abod", "cof"),
-                    help="what one step computes on a kNN workload: LOF (with the kNN score, "
-                         "the default), the kNN score alone, ABOD or COF")
+    ap.add_argument("--workload", default=None,
+                    help="one workload only (C1-C5, N1, L1); default: C5 as the headline with "
+                         "C1-C4 as sub-results")
+    ap.add_argument("--precision", default=None,
+                    help="filter precision (auto, fp32, fp16, bf16); default: the workload's")
+    ap.add_argument("--detector", default=None, choices=("lof", "knn", "abod", "cof"),
+                    help="what one step computes on a kNN workload; default: the workload's "
+                         "(LOF with the kNN score for C1 and C2, the kNN score for C3-C5)")
     ap.add_argument("--score", default="kth", choices=("kth", "mean", "median", "sum"),
                     help="kNN score of the step")
+    ap.add_argument("--sub-steps", type=int, default=5,
+                    help="timed steps of each sub-result (one warm-up step each)")
+    ap.add_argument("--no-sub", action="store_true", help="headline line without sub-results")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="target wall time of the oracle baseline sample")
+                    help="target wall time of the oracle baseline sample (N1, L1)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of the benchmark, run a plain device-to-device copy of this "
                          "many MiB (calibrates the HBM byte counters against a known size)")
@@ -72,36 +84,31 @@ def copy_calibration(mib, steps):
                       "GB_s": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
-def cpu_baseline(x, k, target_s):
-    """The oracle (exact fp64 brute force) on a bounded sample of query rows.
-
-    Rows are taken in a seeded random order without repetition, in batches
-    that double until about target_s seconds of oracle time have been spent.
-    """
-    import numpy as np
-
+def cpu_baseline(x, k, rows, lof_full=False):
+    """The oracle (exact fp64 brute force, every host core in the affinity
+    mask) on the seeded sample `rows` of query rows, each scanned against the
+    whole reference set.  With lof_full the whole workload is run instead:
+    the oracle's kNN of every row and its LOF."""
     from oracle import oracle
     n = x.shape[0]
-    order = np.random.default_rng(2024).permutation(n).astype(np.int64)
-    rows_done, t_total = 0, 0.0
-    batch = 256
-    while t_total < target_s and rows_done < n:
-        m = min(batch, n - rows_done)
-        rows = np.sort(order[rows_done:rows_done + m])
-        t0 = time.perf_counter()
+    t0 = time.perf_counter()
+    if lof_full:
+        oidx, odist = oracle.knn_self(x, k)
+        oracle.lof(oidx, odist)
+        m = n
+    else:
         oracle.knn_self(x, k, rows=rows)
-        t_total += time.perf_counter() - t0
-        rows_done += m
-        if t_total < target_s / 4:
-            batch *= 2
+        m = len(rows)
+    t = time.perf_counter() - t0
+    what = ("exact fp64 kNN (k=%d) and LOF of all %d rows" % (k, n) if lof_full else
+            "exact fp64 kNN (k=%d) of %d seeded query rows (default_rng sample of the workload) "
+            "against all %d reference rows" % (k, m, n))
     return {
-        "value": rows_done / t_total,
+        "value": m / t,
         "unit": "points/s",
         "cores": oracle.default_threads(),
         "kind": "oracle",
-        "sample": "exact fp64 kNN (k=%d) of %d distinct seeded-random query rows against all %d "
-                  "reference rows, %.1f s of oracle time; the O(n k) LOF tail is not timed"
-                  % (k, rows_done, n, t_total),
+        "sample": "%s, %.2f s of oracle time (%.3g pairs/s)" % (what, t, float(m) * n / t),
     }
 
 
@@ -183,7 +190,7 @@ def bench_nwr(args, w):
     n, d = x_host.shape
     phi = float(w.extra["phi"])
     x = torch.from_numpy(x_host).to("cuda:0")
-    opts = tod.options(precision=args.precision, exclude_self=True)
+    opts = tod.options(precision=args.precision or w.precision, exclude_self=True)
     ws = tod.Workspace()
     rp, idx, _ = tod.tod_nwr(x, x, phi, opts, workspace=ws, with_dist=False)  # sizes the outputs
     cap = int(idx.numel())
@@ -282,7 +289,7 @@ def bench_loci(args, w):
     n, d = x_host.shape
     p = w.extra
     x = torch.from_numpy(x_host).to("cuda:0")
-    opts = tod.options(precision=args.precision)
+    opts = tod.options(precision=args.precision or w.precision)
     ws = tod.Workspace()
     st = tod.new_stats()
     tod.tod_loci(x, p["radii"], p["alpha"], p["n_min"], p["k_sigma"], opts, workspace=ws,
@@ -351,104 +358,212 @@ def bench_loci(args, w):
     print(json.dumps(line), flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py measures one GPU only: --gpus %d is not supported (the path has no "
-              "multi-GPU mode)" % args.gpus, file=sys.stderr)
-        sys.exit(2)
-    if args.copy_mib:
-        copy_calibration(args.copy_mib, args.steps)
-        return
+
+
+# Peak VALU issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 3.93e13 lane
+# operations per second (fp32, unpacked, one operation per lane per clock).
+PEAK_VALU_OPS = 39.32        # T lane-ops/s
+
+
+def tile_rooflines(prec, d, pairs, launches, tile_ms):
+    """Both views of the dominant kernel, the fused distance tile, per launch.
+
+    mfma: the cross-term's 2d flop per pair (d as given, not padded) against
+    the dense MFMA peak (an fp32 filter: against the fp32 vector peak).
+    alu:  the selection's one fp32 compare per pair (an fp32 filter adds its
+    d multiply-adds) against the VALU issue peak.
+    The binding view is the one whose floor time is longer."""
+    launch_s = tile_ms / launches * 1e-3
+    per_launch = pairs / launches
+    if prec == "fp32":
+        mf_peak, ops_pair = PEAK_VALU_F32, d + 1.0
+    else:
+        mf_peak, ops_pair = PEAK_MFMA_F16, 1.0
+    mf = 2.0 * d * per_launch / launch_s / 1e12
+    alu = ops_pair * per_launch / launch_s / 1e12
+    views = {
+        "mfma": {"bound": "mfma", "achieved": round(mf, 3), "peak": mf_peak, "unit": "TFLOP/s",
+                 "frac": round(mf / mf_peak, 4),
+                 "ops": "2d flop per pair (cross-term)"},
+        "alu": {"bound": "alu", "achieved": round(alu, 3), "peak": PEAK_VALU_OPS,
+                "unit": "TFLOP/s", "frac": round(alu / PEAK_VALU_OPS, 4),
+                "ops": "%g fp32 VALU op per pair (%s)" % (
+                    ops_pair, "threshold compare" if prec != "fp32" else "FMA chain + compare")},
+    }
+    floor_mf = 2.0 * d * pairs / (mf_peak * 1e12)
+    floor_alu = ops_pair * pairs / (PEAK_VALU_OPS * 1e12)
+    bind = "mfma" if floor_mf >= floor_alu else "alu"
+    return bind, views
+
+
+def bench_knn(w, x_host, steps, warmup, precision, detector, score="kth"):
+    """Time `steps` calls of the workload's detector; returns the measurement."""
     import numpy as np
     import torch
 
-    from paper_2110_14007_amd import tod, workloads
+    from paper_2110_14007_amd import tod
 
-    w = workloads.WORKLOADS[args.workload]
-    if w.name.startswith("N"):
-        bench_nwr(args, w)
-        return
-    if w.name.startswith("L"):
-        bench_loci(args, w)
-        return
-    x_host, _ = workloads.generate(args.workload)
     n, d, k = x_host.shape[0], x_host.shape[1], w.k
     dev = torch.device("cuda:0")
     x = torch.from_numpy(x_host).to(dev)
-    opts = tod.options(precision=args.precision, query_block=w.query_block, score=args.score)
+    opts = tod.options(precision=precision, query_block=w.query_block, score=score)
     ws = tod.Workspace()
     out = (torch.empty(n, dtype=torch.float32, device=dev),
            torch.empty(n, dtype=torch.float32, device=dev))
 
     def step(st=None):
-        if args.detector == "lof":
+        if detector == "lof":
             tod.tod_lof(x, k, opts, workspace=ws, out=out, stats=st)
-        elif args.detector == "knn":
+        elif detector == "knn":
             tod.tod_knn_score(x, k, opts, workspace=ws, stats=st)
-        elif args.detector == "cof":
+        elif detector == "cof":
             tod.tod_cof(x, min(k, 63), opts, workspace=ws, stats=st)
         else:
             tod.tod_abod(x, min(k, 64), opts, workspace=ws, stats=st)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     stats = []
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         st = tod.new_stats()
         step(st)
         stats.append(st.as_dict())
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / args.steps
-    value = n / (ms_step * 1e-3)
-    pairs_s = float(n) * float(n) / (ms_step * 1e-3)
+    ms_step = (t1 - t0) * 1e3 / steps
+    del x, ws, out
+    torch.cuda.empty_cache()
 
     def avg(key):
         return float(np.mean([s[key] for s in stats]))
 
     prec = stats[0]["precision"]
     launches = stats[0]["tile_launches"]
-    tile_ms = avg("ms_tile") / launches  # average duration of one tile launch
-    flops_per_launch = 2.0 * d * float(n) * float(n) / launches
-    achieved = flops_per_launch / (tile_ms * 1e-3) / 1e12
-    if prec == "fp32":
-        bound, peak = "alu", PEAK_VALU_F32
-    else:
-        bound, peak = "mfma", PEAK_MFMA_F16
-    kname = "tile<%s,K'=%d>" % (prec, stats[0]["kprime"])
-    roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                "traffic": recorded_traffic(args.workload, kname),
-                "kernel": kname, "launch_ms": round(tile_ms, 4)}
+    pairs = float(n) * float(n)
+    bind, views = tile_rooflines(prec, d, pairs, launches, avg("ms_tile"))
+    return {
+        "n": n, "d": d, "k": k, "detector": detector, "score": score, "prec": prec,
+        "ms_step": ms_step, "value": n / (ms_step * 1e-3), "pairs_s": pairs / (ms_step * 1e-3),
+        "phase_ms": {key: round(avg(key), 4) for key in
+                     ("ms_prep", "ms_tile", "ms_recheck", "ms_fallback", "ms_score", "ms_total")},
+        "kprime": stats[0]["kprime"], "ref_splits": stats[0]["ref_splits"],
+        "query_block": stats[0]["query_block"], "blocks": stats[0]["blocks"],
+        "launches": launches, "launch_ms": avg("ms_tile") / launches,
+        "rows_fallback": stats[0]["rows_fallback"], "bind": bind, "views": views,
+    }
+
+
+def knn_roofline(wname, m):
+    """The line's `roofline` object: the binding view of the tile kernel, the
+    other view beside it, and the recorded HBM traffic per launch."""
+    kname = "tile<%s,K'=%d>" % (m["prec"], m["kprime"])
+    r = dict(m["views"][m["bind"]])
+    r["traffic"] = recorded_traffic(wname, kname)
+    r["kernel"] = kname
+    r["launch_ms"] = round(m["launch_ms"], 4)
+    other = "alu" if m["bind"] == "mfma" else "mfma"
+    r["other_view"] = m["views"][other]
+    return r
+
+
+def knn_defaults(w, args):
+    precision = args.precision or w.precision
+    detector = args.detector or ("lof" if w.lof else "knn")
+    return precision, detector
+
+
+def knn_line(args, w):
+    """The JSON line of one kNN workload (headline fields)."""
+    from paper_2110_14007_amd import workloads
+    x_host, _ = workloads.generate(w.name)
+    precision, detector = knn_defaults(w, args)
+    m = bench_knn(w, x_host, args.steps, args.warmup, precision, detector, args.score)
     line = {
         "metric": METRIC,
-        "value": round(value, 1),
+        "value": round(m["value"], 1),
         "unit": "points/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "ms_per_step": round(m["ms_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32+f64" if prec == "fp32" else "%s+f64" % prec.replace("fp", "f"),
+        "dtype": "f32+f64" if m["prec"] == "fp32" else "%s+f64" % m["prec"].replace("fp", "f"),
         "data": "synthetic",
-        "config": {"workload": "%s: %s" % (w.name, w.description), "n": n, "d": d, "k": k,
-                   "detector": args.detector, "score": args.score,
-                   "filter_precision": prec, "kprime": stats[0]["kprime"],
-                   "ref_splits": stats[0]["ref_splits"], "query_block": stats[0]["query_block"],
+        "config": {"workload": "%s: %s" % (w.name, w.description), "n": m["n"], "d": m["d"],
+                   "k": m["k"], "detector": detector, "score": args.score,
+                   "filter_precision": m["prec"], "kprime": m["kprime"],
+                   "ref_splits": m["ref_splits"], "query_block": m["query_block"],
                    "parallelism": "single GPU"},
-        "pairs_per_s": pairs_s,
-        "phase_ms": {key: round(avg(key), 4) for key in
-                     ("ms_prep", "ms_tile", "ms_recheck", "ms_fallback", "ms_score", "ms_total")},
-        "rows_fallback": stats[0]["rows_fallback"],
-        "roofline": roofline,
+        "pairs_per_s": m["pairs_s"],
+        "phase_ms": m["phase_ms"],
+        "rows_fallback": m["rows_fallback"],
+        "roofline": knn_roofline(w.name, m),
     }
+    return line, x_host
+
+
+def sub_result(args, w, precision=None, label=None):
+    """One configuration as a sub-result: its own precision and detector,
+    ms/step, tile time, both roofline views and the oracle's rate on a seeded
+    sample of its rows (C1: the whole oracle, kNN and LOF)."""
+    from paper_2110_14007_amd import workloads
+    x_host, _ = workloads.generate(w.name)
+    prec_w, detector = knn_defaults(w, args)
+    precision = precision or prec_w
+    m = bench_knn(w, x_host, args.sub_steps, 1, precision, detector)
+    r = {"workload": label or w.name, "n": m["n"], "d": m["d"], "k": m["k"],
+         "detector": detector, "filter_precision": m["prec"], "kprime": m["kprime"],
+         "ms_per_step": round(m["ms_step"], 4), "points_per_s": round(m["value"], 1),
+         "pairs_per_s": m["pairs_s"], "tile_ms": round(m["phase_ms"]["ms_tile"], 4),
+         "phase_ms": m["phase_ms"], "rows_fallback": m["rows_fallback"],
+         "roofline": knn_roofline(w.name, m), "steps": args.sub_steps}
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(x_host, k, args.cpu_seconds)
+        if w.name == "C1":
+            r["oracle"] = cpu_baseline(x_host, w.k, None, lof_full=True)
+        else:
+            r["oracle"] = cpu_baseline(x_host, w.k, workloads.sample_rows(w.name, count=256))
+    return r
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: --gpus %d is not supported (the path runs on "
+              "one GPU; no multi-GPU mode is built)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    if args.copy_mib:
+        copy_calibration(args.copy_mib, args.steps)
+        return
+    from paper_2110_14007_amd import workloads
+
+    name = args.workload or "C5"
+    w = workloads.WORKLOADS[name]
+    if w.name.startswith("N"):
+        bench_nwr(args, w)
+        return
+    if w.name.startswith("L"):
+        bench_loci(args, w)
+        return
+    line, x_host = knn_line(args, w)
+    if not args.no_cpu_baseline:
+        if w.name == "C1":
+            line["cpu_baseline"] = cpu_baseline(x_host, w.k, None, lof_full=True)
+        else:
+            line["cpu_baseline"] = cpu_baseline(x_host, w.k, workloads.sample_rows(w.name))
+    del x_host
+    if args.workload is None and not args.no_sub:
+        subs = []
+        for sub in ("C1", "C2", "C3", "C4"):
+            subs.append(sub_result(args, workloads.WORKLOADS[sub]))
+            print("# %s done" % sub, file=sys.stderr, flush=True)
+        # the library's default filter at C4 (fp16) beside the workload's bf16
+        subs.append(sub_result(args, workloads.WORKLOADS["C4"], precision="auto",
+                               label="C4 (library default filter)"))
+        line["configs"] = subs
     print(json.dumps(line), flush=True)
 
 

@@ -85,9 +85,15 @@ __device__ __forceinline__ int tile_row(int r, int lane) {
 
 __host__ __device__ constexpr int row_bytes(int dpad, int es) { return dpad * es + 16; }
 
+// Rows longer than the register-operand shapes are staged in column slabs of
+// kSlabBytes per row (32 rows per slab), so LDS use does not grow with d:
+// at most 33 KiB of slab plus the lists (K' = 256: 72 KiB) per workgroup.
+constexpr int kSlabBytes = 1024;
+
 // LDS bytes of the tile kernel for these parameters (host and device agree).
+// dbuf: the double-buffered whole-row staging of the register-operand shapes.
 __host__ __device__ constexpr size_t lds_bytes(int dpad, int es, int kp, int w, bool dbuf) {
-  return (size_t)(dbuf ? 2 : 1) * 32 * row_bytes(dpad, es) + 256 +
+  return (dbuf ? (size_t)2 * 32 * row_bytes(dpad, es) : (size_t)32 * (kSlabBytes + 16)) + 256 +
          (size_t)w * 32 * (kp + kQ) * sizeof(uint64_t);
 }
 
@@ -154,7 +160,8 @@ tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   constexpr int ES = Elem<PREC>::size;
   constexpr bool QREG = DPAD > 0;  // query operand held in registers
   const int dpad = QREG ? DPAD : a.dpad;
-  const int rowb = row_bytes(dpad, ES);
+  // Staged row stride: whole rows (register-operand shapes) or one slab.
+  const int rowb = QREG ? row_bytes(dpad, ES) : kSlabBytes + 16;
   const int tile_bytes = 32 * rowb;
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* tiles = smem;
@@ -229,93 +236,138 @@ tile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     }
     if (tid < 8) *reinterpret_cast<float4*>(hnbuf + b * 32 + 4 * tid) = sth;
   };
-  auto copy_sync = [&](int64_t t0) {  // single-buffer staging for large d
-    for (int c = tid; c < n16; c += W * 64) {
-      const int row = c / cpr, cc = c % cpr;
-      *reinterpret_cast<uint4*>(tiles + row * rowb + cc * 16) =
-          *reinterpret_cast<const uint4*>(xr_bytes + (t0 + row) * (int64_t)dpad * ES + cc * 16);
+  // Long rows: columns [c0, c0 + w) of the tile's 32 rows (one slab, w * ES
+  // <= kSlabBytes), single-buffered; the seeds come with the first slab.
+  auto copy_slab = [&](int64_t t0, int c0, int w) {
+    const int scpr = w * ES / 16;
+    for (int c = tid; c < 32 * scpr; c += W * 64) {
+      const int row = c / scpr, cc = c % scpr;
+      *reinterpret_cast<uint4*>(tiles + row * rowb + cc * 16) = *reinterpret_cast<const uint4*>(
+          xr_bytes + ((t0 + row) * (int64_t)dpad + c0) * ES + cc * 16);
     }
-    if (tid < 8)
+    if (c0 == 0 && tid < 8)
       *reinterpret_cast<float4*>(hnbuf + 4 * tid) =
           *reinterpret_cast<const float4*>(a.hn_r + t0 + 4 * tid);
   };
+  constexpr int kSlabE = kSlabBytes / ES;  // elements per slab row
 
   if constexpr (QREG) {
     fetch(r_begin);
     put(0);
   }
   __syncthreads();
+  // Seeds of the tile's accumulators: -N_j/2 of the rows this lane holds.
+  auto seed_fp32 = [&](const float* hn, float (&acc)[16]) {
+    const float* hnp = hn + 16 * (lane >> 5);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 v = *reinterpret_cast<const float4*>(hnp + 4 * g);
+      acc[4 * g + 0] = v.x;
+      acc[4 * g + 1] = v.y;
+      acc[4 * g + 2] = v.z;
+      acc[4 * g + 3] = v.w;
+    }
+  };
+  auto seed_mfma = [&](const float* hn, floatx16& cacc) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 v = *reinterpret_cast<const float4*>(hn + 8 * g + 4 * (lane >> 5));
+      cacc[4 * g + 0] = v.x;
+      cacc[4 * g + 1] = v.y;
+      cacc[4 * g + 2] = v.z;
+      cacc[4 * g + 3] = v.w;
+    }
+  };
+  // Add the products of columns [c0, c0 + w) (staged rows in buf, whose
+  // column 0 is column c0) to the accumulators.
+  // Chunk c (4 columns) of the FMA chain: query values q4, staged rows at rbase.
+  auto fma_chunk = [&](const unsigned char* rbase, int c, float4 q4, float (&acc)[16]) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float4 rv = *reinterpret_cast<const float4*>(rbase + r * rowb + 16 * c);
+      acc[r] = fmaf(q4.x, rv.x, acc[r]);
+      acc[r] = fmaf(q4.y, rv.y, acc[r]);
+      acc[r] = fmaf(q4.z, rv.z, acc[r]);
+      acc[r] = fmaf(q4.w, rv.w, acc[r]);
+    }
+  };
+  auto accum_fp32 = [&](const unsigned char* buf, int c0, int w, float (&acc)[16]) {
+    const unsigned char* rbase = buf + 16 * (lane >> 5) * rowb;
+    if constexpr (QREG && PREC == TOD_PREC_FP32) {
+#pragma unroll
+      for (int c = 0; c < KC; ++c) fma_chunk(rbase, c, qv[c], acc);
+    } else {
+#pragma nounroll
+      for (int c = 0; c < w / 4; ++c)
+        fma_chunk(rbase, c, *reinterpret_cast<const float4*>(qrow + c0 + 4 * c), acc);
+    }
+  };
+  auto accum_mfma = [&](const unsigned char* buf, int c0, int w, floatx16& cacc) {
+    if constexpr (PREC != TOD_PREC_FP32) {
+      using V = typename Elem<PREC>::V;
+      const unsigned char* arow = buf + myq * rowb + (lane >> 5) * 16;
+      auto step = [&](int c, V bv) {
+        const V av = *reinterpret_cast<const V*>(arow + 32 * c);
+        if constexpr (PREC == TOD_PREC_FP16)
+          cacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, cacc, 0, 0, 0);
+        else
+          cacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, cacc, 0, 0, 0);
+      };
+      if constexpr (QREG) {
+#pragma unroll
+        for (int c = 0; c < KC; ++c) step(c, qv[c]);
+      } else {
+#pragma nounroll
+        for (int c = 0; c < w / 16; ++c)
+          step(c, *reinterpret_cast<const V*>(qrow + c0 + 16 * c + 8 * (lane >> 5)));
+      }
+    }
+  };
   int it = 0;
   for (int64_t t0 = r_begin; t0 < r_end; t0 += 32, ++it) {
     const bool nxt = t0 + 32 < r_end;
+    float acc[16];
     if constexpr (QREG) {
       if (nxt) fetch(t0 + 32);
-    } else {
-      copy_sync(t0);
-      __syncthreads();
-    }
-    const int b = QREG ? (it & 1) : 0;
-    const unsigned char* buf = tiles + b * tile_bytes;
-    const float* hn = hnbuf + b * 32;
-    if (active) {
-      float acc[16];
-      if constexpr (PREC == TOD_PREC_FP32) {
-        const float* hnp = hn + 16 * (lane >> 5);
+      const int b = it & 1;
+      const unsigned char* buf = tiles + b * tile_bytes;
+      const float* hn = hnbuf + b * 32;
+      if (active) {
+        if constexpr (PREC == TOD_PREC_FP32) {
+          seed_fp32(hn, acc);
+          accum_fp32(buf, 0, dpad, acc);
+        } else {
+          floatx16 cacc;
+          seed_mfma(hn, cacc);
+          accum_mfma(buf, 0, dpad, cacc);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const float4 v = *reinterpret_cast<const float4*>(hnp + 4 * g);
-          acc[4 * g + 0] = v.x;
-          acc[4 * g + 1] = v.y;
-          acc[4 * g + 2] = v.z;
-          acc[4 * g + 3] = v.w;
+          for (int r = 0; r < 16; ++r) acc[r] = cacc[r];
         }
-        const unsigned char* rbase = buf + 16 * (lane >> 5) * rowb;
-        const int nc = QREG ? KC : dpad / 4;
-#pragma unroll
-        for (int c = 0; c < nc; ++c) {
-          float4 q4;
-          if constexpr (QREG)
-            q4 = qv[c];
-          else
-            q4 = *reinterpret_cast<const float4*>(qrow + 4 * c);
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float4 rv = *reinterpret_cast<const float4*>(rbase + r * rowb + 16 * c);
-            acc[r] = fmaf(q4.x, rv.x, acc[r]);
-            acc[r] = fmaf(q4.y, rv.y, acc[r]);
-            acc[r] = fmaf(q4.z, rv.z, acc[r]);
-            acc[r] = fmaf(q4.w, rv.w, acc[r]);
+      }
+    } else {
+      // Slab by slab: every wave takes part in the staging and barriers.
+      floatx16 cacc;
+      for (int c0 = 0; c0 < dpad; c0 += kSlabE) {
+        const int w = dpad - c0 < kSlabE ? dpad - c0 : kSlabE;
+        if (c0) __syncthreads();  // the previous slab has been consumed
+        copy_slab(t0, c0, w);
+        __syncthreads();
+        if (active) {
+          if constexpr (PREC == TOD_PREC_FP32) {
+            if (c0 == 0) seed_fp32(hnbuf, acc);
+            accum_fp32(tiles, c0, w, acc);
+          } else {
+            if (c0 == 0) seed_mfma(hnbuf, cacc);
+            accum_mfma(tiles, c0, w, cacc);
           }
         }
-      } else {
-        using V = typename Elem<PREC>::V;
-        floatx16 cacc;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const float4 v = *reinterpret_cast<const float4*>(hn + 8 * g + 4 * (lane >> 5));
-          cacc[4 * g + 0] = v.x;
-          cacc[4 * g + 1] = v.y;
-          cacc[4 * g + 2] = v.z;
-          cacc[4 * g + 3] = v.w;
-        }
-        const unsigned char* arow = buf + myq * rowb + (lane >> 5) * 16;
-        const int nc = QREG ? KC : dpad / 16;
-#pragma unroll
-        for (int c = 0; c < nc; ++c) {
-          const V av = *reinterpret_cast<const V*>(arow + 32 * c);
-          V bv;
-          if constexpr (QREG)
-            bv = qv[c];
-          else
-            bv = *reinterpret_cast<const V*>(qrow + 16 * c + 8 * (lane >> 5));
-          if constexpr (PREC == TOD_PREC_FP16)
-            cacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bv, cacc, 0, 0, 0);
-          else
-            cacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, cacc, 0, 0, 0);
-        }
+      }
+      if constexpr (PREC != TOD_PREC_FP32) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[r] = cacc[r];
       }
+    }
+    if (active) {
       const bool diag = selfq && t0 == q0;
       if (diag || t0 + 32 > r_end) {
 #pragma unroll

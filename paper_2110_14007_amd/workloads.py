@@ -55,7 +55,10 @@ class Workload:
     d: int
     k: int
     seed: int
-    precision: str  # filter precision the workload is specified with
+    # Filter precision the workload is specified with.  C1, C2 and C5 state
+    # only the input type (fp32); the final lists are exact whatever the
+    # filter, so those take the planner's choice ("auto").
+    precision: str
     lof: bool  # whether the workload also asks for LOF
     query_block: int = 0  # 0 = planner's choice
     description: str = ""
@@ -63,9 +66,9 @@ class Workload:
 
 
 WORKLOADS = {
-    "C1": Workload("C1", 2_000, 16, 10, 1, "fp32", True, 0,
+    "C1": Workload("C1", 2_000, 16, 10, 1, "auto", True, 0,
                    "kNN-OD + LOF, n=2000 d=16 k=10: N(0,I) inliers + 5% U[-6,6] outliers"),
-    "C2": Workload("C2", 100_000, 32, 20, 2, "fp32", True, 0,
+    "C2": Workload("C2", 100_000, 32, 20, 2, "auto", True, 0,
                    "kNN + LOF, n=100000 d=32 k=20: 5-Gaussian mixture + 2% uniform box outliers"),
     "C3": Workload("C3", 1_000_000, 64, 10, 3, "fp16", False, 65_536,
                    "kNN-OD, n=1000000 d=64 k=10: 10-cluster Gaussian mixture + 1% N(0,100I) "
@@ -73,7 +76,7 @@ WORKLOADS = {
     "C4": Workload("C4", 200_000, 512, 50, 4, "bf16", False, 0,
                    "kNN-OD, n=200000 d=512 k=50: rank-32 latent x projection + noise, 0.5% "
                    "full-rank outliers, bf16 filter"),
-    "C5": Workload("C5", 4_000_000, 8, 5, 5, "fp32", False, 0,
+    "C5": Workload("C5", 4_000_000, 8, 5, 5, "auto", False, 0,
                    "kNN-OD, n=4000000 d=8 k=5: U[0,1]^8 + 0.1% U[1.5,3]^8 outliers"),
     "N1": Workload("N1", 30_000, 200, 0, 6, "fp16", False, 0,
                    "NWR, n=30000 d=200 phi=18: 10-cluster Gaussian mixture + 1% N(0,100I) "

@@ -61,12 +61,13 @@ def check_properties(x, k, score, idx, dist, lofv):
         assert np.all(np.isfinite(lofv)) and np.all(lofv > 0)
 
 
-def run_config(env, name, nrows=2048, lof_rows=0, cross_check=None):
+def run_config(env, name, nrows=2048, lof_rows=0, cross_check=None, repeat=False):
     _, _, oracle = env
     w = workloads.WORKLOADS[name]
     x, _ = workloads.generate(name)
     say("%s: generated %s" % (name, x.shape))
-    score, idx, dist, lofv, st = gpu_lists(env, x, w.k, w.lof, query_block=w.query_block)
+    lof = w.lof or lof_rows > 0
+    score, idx, dist, lofv, st = gpu_lists(env, x, w.k, lof, query_block=w.query_block)
     say("%s: gpu stats %s" % (name, st))
     check_properties(x, w.k, score, idx, dist, lofv)
     rows = workloads.sample_rows(name, count=nrows)
@@ -79,28 +80,45 @@ def run_config(env, name, nrows=2048, lof_rows=0, cross_check=None):
         olof, _, _ = oracle.lof_rows(x, w.k, r)
         compare_scores(lofv[r], olof, what="LOF")
         say("%s: LOF of %d sampled rows matches the oracle" % (name, len(r)))
+    if repeat:
+        # The same call again: every output bit for bit, on every row.
+        s2, i2, d2, l2, _ = gpu_lists(env, x, w.k, lof, query_block=w.query_block)
+        np.testing.assert_array_equal(i2, idx)
+        np.testing.assert_array_equal(d2, dist)
+        np.testing.assert_array_equal(s2, score)
+        if lof:
+            np.testing.assert_array_equal(l2, lofv)
+        # The filter's own lists, unverified (no_recheck keeps the shortlist's
+        # first k in key order): two runs of the fused tile agree bit for bit.
+        r1 = gpu_lists(env, x, w.k, False, query_block=w.query_block, no_recheck=True)
+        r2 = gpu_lists(env, x, w.k, False, query_block=w.query_block, no_recheck=True)
+        np.testing.assert_array_equal(r1[1], r2[1])
+        np.testing.assert_array_equal(r1[2], r2[2])
+        say("%s: two runs identical on every row (verified and unverified)" % name)
     if cross_check:
-        s2, i2, d2, l2, st2 = gpu_lists(env, x, w.k, w.lof, query_block=w.query_block,
+        s2, i2, d2, l2, st2 = gpu_lists(env, x, w.k, lof, query_block=w.query_block,
                                         precision=cross_check)
         say("%s: %s filter stats %s" % (name, cross_check, st2))
         np.testing.assert_array_equal(i2, idx)
         np.testing.assert_array_equal(d2, dist)
-        if lofv is not None:
+        if lof:
             np.testing.assert_array_equal(l2, lofv)
     return st
 
 
 def test_C2_full_size(env):
-    run_config(env, "C2", nrows=2048, lof_rows=24, cross_check="fp32")
+    run_config(env, "C2", nrows=2048, lof_rows=64, cross_check="fp32")
 
 
 def test_C3_full_size(env):
-    run_config(env, "C3", nrows=1024, cross_check="fp32")
+    run_config(env, "C3", nrows=2048, lof_rows=32, cross_check="fp32", repeat=True)
 
 
 def test_C4_full_size(env):
-    run_config(env, "C4", nrows=256, cross_check="bf16")
+    # the workload's bf16 filter against the library's default (fp16)
+    st = run_config(env, "C4", nrows=2048, lof_rows=2, cross_check="bf16")
+    assert st["precision"] == "fp16"
 
 
 def test_C5_full_size(env):
-    run_config(env, "C5", nrows=1024, cross_check="fp32")
+    run_config(env, "C5", nrows=2048, lof_rows=32, cross_check="fp32", repeat=True)
