@@ -25,7 +25,9 @@
  *   - Every data pointer is a DEVICE pointer (HIP), owned by the caller.
  *     Inputs are fp32, row-major, contiguous, 16-byte aligned.
  *   - The library allocates no device memory: the caller passes a workspace
- *     of at least tod_workspace_size() bytes (256-byte aligned).
+ *     (256-byte aligned).  tod_workspace_size() bytes run the queries in as
+ *     few blocks as the planner likes; a smaller workspace makes the kNN
+ *     entry points plan smaller query blocks (tod_plan_workspace).
  *   - Distances are Euclidean (not squared).  Index outputs are 0-based rows
  *     of the reference set.  Output rows are sorted by (distance, index).
  *   - Arguments are validated on the host before any HIP call; on an
@@ -50,7 +52,7 @@ typedef enum {
   TOD_OK = 0,
   TOD_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, k out of range, bad struct_size */
   TOD_ERR_NONFINITE = 2,   /* NaN or Inf in the input (the rounding analysis needs finite data) */
-  TOD_ERR_WORKSPACE = 3,   /* workspace smaller than tod_workspace_size() or misaligned */
+  TOD_ERR_WORKSPACE = 3,   /* workspace misaligned, or too small for one 32-row query block */
   TOD_ERR_UNSUPPORTED = 4, /* k > 256, d > 4096, or more than 2^31 - 1 rows */
   TOD_ERR_HIP = 5,         /* a HIP launch or runtime call failed; see tod_last_error() */
   TOD_ERR_INTERNAL = 6,
@@ -243,6 +245,23 @@ tod_status tod_cof(const float* x, int64_t n, int64_t d, int32_t k, const tod_op
  */
 tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,
                     tod_stats* plan);
+
+/*
+ * The plan a call would use with a workspace of ws_bytes (Section 6:
+ * automatic batching sized to the memory at hand; the paper batches so that
+ * large inputs fit a GPU's memory).  A workspace smaller than
+ * tod_workspace_size() is not an error by itself: the query block shrinks to
+ * what the room beside the fixed buffers (quantised copies, norms, radii,
+ * worklist, neighbour lists) holds, at S x K' x 8 bytes per query row, the
+ * reference splits S follow the smaller block, and the rows run in more
+ * blocks with identical results.  TOD_ERR_WORKSPACE if not even one 32-row
+ * block fits, or if opts fixes query_block or ref_splits and the plan does
+ * not fit.  mode as in tod_workspace_size; the plan is for X against itself
+ * when mode == 1 or opts->exclude_self is set, else for separate sets.
+ * Host only, like tod_plan.
+ */
+tod_status tod_plan_workspace(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t mode,
+                              const tod_options* opts, size_t ws_bytes, tod_stats* plan);
 
 /*
  * Neighbours within range (NWR, Section 5.3: the case study of provable

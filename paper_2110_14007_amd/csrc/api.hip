@@ -84,6 +84,27 @@ tod_status check_sizes(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t exc
 
 namespace tod {
 
+// Reference splits for a query block of qb rows (Section 6 customised cdist
+// batching): enough waves for two per SIMD on 256 CUs x 4 SIMDs, but at
+// least 2048 references per split (every split keeps its own K' list per
+// query, so splits cost selection work), and at most 16.
+int64_t auto_splits(int64_t qb, int64_t nr) {
+  const int64_t waves = (qb + 31) / 32;
+  int64_t s = (2048 + waves - 1) / waves;
+  const int64_t cap = nr / 2048 > 1 ? nr / 2048 : 1;
+  if (s > cap) s = cap;
+  if (s > 16) s = 16;
+  return s < 1 ? 1 : s;
+}
+
+// S splits of 32-row multiples (fewer if the rounding leaves some empty).
+void set_splits(Plan* p, int64_t s) {
+  if (s < 1) s = 1;
+  const int64_t len = round_up((p->nr + s - 1) / s, 32);
+  p->splits = (int32_t)((p->nr + len - 1) / len);
+  p->split_len = len;
+}
+
 tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, int32_t self,
                      const tod_options& o, Plan* p, const char** why) {
   *why = "";
@@ -142,26 +163,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   if (qb > p->nq_pad) qb = p->nq_pad;
   p->query_block = qb;
   p->blocks = (nq + qb - 1) / qb;
-  // Reference splits (Section 6 customised cdist batching): enough waves for
-  // two per SIMD on 256 CUs x 4 SIMDs, but at least 2048 references per
-  // split (every split keeps its own K' list per query, so splits cost
-  // selection work).
-  const int64_t waves = (qb + 31) / 32;
-  int64_t s;
-  if (o.ref_splits > 0) {
-    s = o.ref_splits;
-  } else {
-    const int64_t target = 2048;
-    s = (target + waves - 1) / waves;
-    const int64_t cap = nr / 2048 > 1 ? nr / 2048 : 1;
-    if (s > cap) s = cap;
-    if (s > 16) s = 16;
-  }
-  if (s < 1) s = 1;
-  int64_t len = round_up((nr + s - 1) / s, 32);
-  s = (nr + len - 1) / len;
-  p->splits = (int32_t)s;
-  p->split_len = len;
+  set_splits(p, o.ref_splits > 0 ? o.ref_splits : auto_splits(qb, nr));
   p->waves_per_group = kp <= 32 ? 4 : (kp == 64 ? 2 : 1);
   // The register-list MFMA kernel covers fp16 / bf16 filters whose query
   // operand fits in registers and whose shortlist is 16, 32 or 64 long.  Rows
@@ -243,6 +245,55 @@ Layout make_layout(const Plan& p) {
   return L;
 }
 
+// Automatic batching sized to the caller's memory (Section 6): when the
+// workspace is smaller than the plan's layout, the tail split's region is
+// dropped first; if that is not enough, the query block shrinks to
+// what the room left beside the fixed buffers holds (partial lists of
+// S x K' entries per query row), the reference splits follow the smaller
+// block (and shrink too if the room demands it).  Fails only when not even
+// one 32-row block fits, or when the caller fixed the query block or the
+// splits.
+tod_status fit_plan(Plan* p, size_t ws_bytes, const tod_options& o, std::string* why) {
+  if (o.query_block > 0 || o.ref_splits > 0) {
+    *why = "the query block or the reference splits were fixed by the caller";
+    return TOD_ERR_WORKSPACE;
+  }
+  // The tail split's lists go first: the same blocks without it.
+  Plan q = *p;
+  q.tail_parts = 1;
+  q.tail_auto = 0;
+  q.tail_lists = 0;
+  if (make_layout(q).total <= ws_bytes) {
+    *p = q;
+    return TOD_OK;
+  }
+  q.query_block = 0;  // no partial lists: the fixed part of the layout
+  const size_t fixed = make_layout(q).total;
+  const size_t per = (size_t)q.kprime * sizeof(uint64_t);  // partial-list bytes per row and split
+  if (ws_bytes < fixed + 32 * per + 256) {
+    *why = "not even one 32-row query block fits: need at least " +
+           std::to_string(fixed + 32 * per + 256) + " bytes";
+    return TOD_ERR_WORKSPACE;
+  }
+  const size_t room = ws_bytes - fixed - 256;  // the partial region's alignment slack
+  int64_t qb = (int64_t)(room / per) / 32 * 32;
+  if (qb > q.nq_pad) qb = q.nq_pad;
+  int64_t s = auto_splits(qb, q.nr);
+  const int64_t smax = (int64_t)(room / ((size_t)qb * per));
+  if (s > smax) s = smax;
+  q.query_block = qb;
+  q.blocks = (q.nq + qb - 1) / qb;
+  set_splits(&q, s);
+  const bool want = o.reorder > 0 || (o.reorder == 0 && q.nr >= kOrderMinRows);
+  q.order = (q.self && q.tile_kind == 1 && q.splits == 1 && want) ? 1 : 0;
+  if (make_layout(q).total > ws_bytes) {
+    *why = "internal: the fitted plan does not fit";
+    return TOD_ERR_INTERNAL;
+  }
+  *p = q;
+  return TOD_OK;
+}
+
 // Neighbours within range: the fp16 / bf16 MFMA range tile (rtile.h) over
 // rows padded to a power of two of at least 16 elements, reference splits by
 // the kNN rule, no query blocks of its own (the batches follow from the
@@ -273,20 +324,7 @@ tod_status make_plan_nwr(int64_t nq, int64_t nr, int64_t d, int32_t self, const 
   p->nr_pad = round_up(nr, 32);
   p->query_block = p->nq_pad;
   p->blocks = 1;
-  const int64_t waves = p->nq_pad / 32;
-  int64_t s;
-  if (o.ref_splits > 0) {
-    s = o.ref_splits;
-  } else {
-    s = (2048 + waves - 1) / waves;
-    const int64_t cap = nr / 2048 > 1 ? nr / 2048 : 1;
-    if (s > cap) s = cap;
-    if (s > 16) s = 16;
-  }
-  if (s < 1) s = 1;
-  const int64_t len = round_up((nr + s - 1) / s, 32);
-  p->splits = (int32_t)((nr + len - 1) / len);
-  p->split_len = len;
+  set_splits(p, o.ref_splits > 0 ? o.ref_splits : auto_splits(p->nq_pad, nr));
   p->waves_per_group = 4;
   p->tile_kind = 2;
   return TOD_OK;
@@ -367,7 +405,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
                const tod_options* opts_in, int32_t force_excl, int32_t mode, void* ws,
                size_t ws_bytes, void* stream, int64_t* idx_out, float* dist_out,
                float* score_out, float* lof_out, const int32_t* labels_r, int32_t n_classes,
-               int32_t* pred_out, tod_stats* stats) {
+               int32_t* pred_out, tod_stats* stats, bool events = true) {
   g_last_error.clear();
   const int32_t lof = (mode == 1 || mode == 4) ? 1 : 0;  // COF uses LOF's buffers
   tod_options o;
@@ -391,10 +429,15 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   st = tod::make_plan(nq, nr, d, k, lof, self, o, &p, &why);
   if (st != TOD_OK) return fail(st, why);
   if (mode >= 2) p.lists = 1;
-  const Layout L = tod::make_layout(p);
-  if (ws_bytes < L.total)
-    return fail(TOD_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) +
-                                       " bytes, got " + std::to_string(ws_bytes));
+  Layout L = tod::make_layout(p);
+  if (ws_bytes < L.total) {
+    std::string w;
+    st = tod::fit_plan(&p, ws_bytes, o, &w);
+    if (st != TOD_OK)
+      return fail(st, "workspace of " + std::to_string(ws_bytes) + " bytes too small (" + w +
+                          "; the one-block plan needs " + std::to_string(L.total) + ")");
+    L = tod::make_layout(p);
+  }
   char* base = (char*)ws;
   Args a;
   memset(&a, 0, sizeof(a));
@@ -453,7 +496,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
 
   hipStream_t s = (hipStream_t)stream;
   Timers tm;
-  tm.on = stats != nullptr;
+  tm.on = stats != nullptr && events;
   hipEvent_t e0 = tm.mark(s);
   hipError_t he = tod::launch_prep(p, a, s);
   if (he != hipSuccess) return hip_fail(he, "prep launch");
@@ -1023,6 +1066,44 @@ tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_opti
   const char* why;
   st = tod::make_plan(nq, nr, d, k, 0, o.exclude_self ? 1 : 0, o, &p, &why);
   if (st != TOD_OK) return fail(st, why);
+  plan->precision = p.precision;
+  plan->kprime = p.kprime;
+  plan->ref_splits = p.splits;
+  plan->query_block = p.query_block;
+  plan->blocks = p.blocks;
+  plan->tile_launches = p.blocks;
+  plan->reordered = p.order;
+  return TOD_OK;
+}
+
+tod_status tod_plan_workspace(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t mode,
+                              const tod_options* opts, size_t ws_bytes, tod_stats* plan) {
+  g_last_error.clear();
+  if (!plan || plan->struct_size != sizeof(tod_stats))
+    return fail(TOD_ERR_INVALID_ARG, "plan must point to a tod_stats with struct_size set");
+  if (mode < 0 || mode > 2) return fail(TOD_ERR_INVALID_ARG, "mode must be 0, 1 or 2");
+  tod_options o;
+  tod_status st = resolve_options(opts, &o);
+  if (st != TOD_OK) return st;
+  const int32_t lof = mode == 1 ? 1 : 0;
+  if (lof) o.exclude_self = 1;
+  if (lof && nq != nr) return fail(TOD_ERR_INVALID_ARG, "mode 1 is X against itself: nq == nr");
+  st = check_sizes(nq, nr, d, k, o.exclude_self);
+  if (st != TOD_OK) return st;
+  Plan p;
+  const char* why;
+  const int32_t self = o.exclude_self ? 1 : 0;
+  st = tod::make_plan(nq, nr, d, k, lof, self, o, &p, &why);
+  if (st != TOD_OK) return fail(st, why);
+  if (mode == 2) p.lists = 1;
+  const size_t need = tod::make_layout(p).total;
+  if (ws_bytes < need) {
+    std::string w;
+    st = tod::fit_plan(&p, ws_bytes, o, &w);
+    if (st != TOD_OK)
+      return fail(st, "workspace of " + std::to_string(ws_bytes) + " bytes too small (" + w +
+                          "; the one-block plan needs " + std::to_string(need) + ")");
+  }
   plan->precision = p.precision;
   plan->kprime = p.kprime;
   plan->ref_splits = p.splits;

@@ -2,6 +2,8 @@
 // kernels of libtod.  Not part of the public ABI.
 #pragma once
 
+#include <string>
+
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -312,6 +314,7 @@ hipError_t launch_range_emit(const Args& a, int64_t b0, int64_t rows, hipStream_
 tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, int32_t self,
                      const tod_options& o, Plan* plan, const char** why);
 Layout make_layout(const Plan& p);
+
 tod_status make_plan_nwr(int64_t nq, int64_t nr, int64_t d, int32_t self, const tod_options& o,
                          Plan* plan, const char** why);
 // NWR workspace regions; cand is the first byte of the candidate room.

@@ -31,7 +31,7 @@ SCORES = {"kth": 0, "largest": 0, "mean": 1, "median": 2, "sum": 3}
 SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
            "tod_knn_decision", "tod_knn_classify", "tod_abod", "tod_cof", "tod_nwr_workspace_size",
            "tod_nwr", "tod_loci_workspace_size", "tod_loci",
-           "tod_plan",
+           "tod_plan", "tod_plan_workspace",
            "tod_status_string", "tod_last_error")
 
 
@@ -130,6 +130,8 @@ def _load():
     lib.tod_loci.restype = ctypes.c_int
     lib.tod_plan.argtypes = [i64, i64, i64, i32, opt_p, st_p]
     lib.tod_plan.restype = ctypes.c_int
+    lib.tod_plan_workspace.argtypes = [i64, i64, i64, i32, i32, opt_p, sz, st_p]
+    lib.tod_plan_workspace.restype = ctypes.c_int
     lib.tod_status_string.argtypes = [ctypes.c_int]
     lib.tod_status_string.restype = ctypes.c_char_p
     lib.tod_last_error.argtypes = []
@@ -184,6 +186,19 @@ def tod_workspace_size(nq: int, nr: int, d: int, k: int, mode: int = 0, opts=Non
                                        ctypes.byref(opts) if opts is not None else None))
 
 
+def tod_plan_workspace(nq: int, nr: int, d: int, k: int, ws_bytes: int, mode: int = 0,
+                       opts=None) -> dict:
+    """Plan of a call with a workspace of ws_bytes (host only)."""
+    s = new_stats()
+    st = _lib.tod_plan_workspace(int(nq), int(nr), int(d), int(k), int(mode),
+                                 ctypes.byref(opts) if opts is not None else None,
+                                 ctypes.c_size_t(int(ws_bytes)), ctypes.byref(s))
+    _check(st, "tod_plan_workspace")
+    return {"precision": PRECISION_NAMES[s.precision], "kprime": s.kprime,
+            "ref_splits": s.ref_splits, "query_block": s.query_block, "blocks": s.blocks,
+            "reordered": s.reordered}
+
+
 def tod_plan(nq: int, nr: int, d: int, k: int, opts=None) -> dict:
     s = new_stats()
     _check(_lib.tod_plan(int(nq), int(nr), int(d), int(k),
@@ -223,6 +238,19 @@ class Workspace:
         torch = _torch()
         if self.buf is None or self.buf.numel() < nbytes or self.buf.device != device:
             self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        return self.buf
+
+
+class FixedWorkspace:
+    """A device workspace of a fixed size chosen by the caller.  The library
+    plans its query blocks to fit it (automatic batching sized to memory);
+    a workspace below the fixed buffers plus one 32-row block is an error."""
+
+    def __init__(self, nbytes: int, device="cuda:0"):
+        torch = _torch()
+        self.buf = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+    def get(self, nbytes: int, device):
         return self.buf
 
 

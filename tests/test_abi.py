@@ -100,11 +100,18 @@ def test_bad_options_rejected(tod):
 
 
 def test_workspace_too_small_and_misaligned(tod):
+    # A workspace smaller than the one-block plan is planned into smaller query
+    # blocks; below the fixed buffers plus one 32-row block the call fails.
     need = tod.tod_workspace_size(100, 100, 8, 5)
     assert need > 0
     other = ctypes.c_void_p(0x200000)  # separate query and reference sets
-    assert _knn(tod, xr=other, ws_bytes=need - 1) == tod.TOD_ERR_WORKSPACE
-    assert "workspace too small" in tod.last_error()
+    assert _knn(tod, xr=other, ws_bytes=need // 8) == tod.TOD_ERR_WORKSPACE
+    assert "too small" in tod.last_error() and "32-row" in tod.last_error()
+    # a caller-fixed query block is not re-planned
+    o64 = tod.options(query_block=64)
+    need64 = tod.tod_workspace_size(100, 100, 8, 5, 0, o64)
+    assert _knn(tod, xr=other, ws_bytes=need64 - 1, opts=o64) == tod.TOD_ERR_WORKSPACE
+    assert "fixed by the caller" in tod.last_error()
     assert _knn(tod, ws=ctypes.c_void_p(0x100010)) == tod.TOD_ERR_WORKSPACE
 
 

@@ -102,3 +102,38 @@ def test_tail_region_in_workspace(tod):
     assert tod.tod_workspace_size(n, n, d, k, 1, tod.options(precision="fp16", ref_splits=4)) == \
         tod.tod_workspace_size(n, n, d, k, 1, tod.options(precision="fp16", ref_splits=4,
                                                           tail_parts=1))
+
+
+def test_workspace_sized_batching(tod):
+    # Automatic batching sized to the caller's memory: smaller workspaces give
+    # smaller query blocks (more blocks), down to one 32-row block.
+    n, d, k = 100_000, 32, 20
+    full = tod.tod_workspace_size(n, n, d, k, 1)
+    big = tod.tod_plan_workspace(n, n, d, k, full, mode=1)
+    assert big["blocks"] == 1 and big["query_block"] >= n
+    prev = big
+    sizes = [full * f // 100 for f in (60, 45, 35, 30)]
+    for ws in sizes:
+        p = tod.tod_plan_workspace(n, n, d, k, ws, mode=1)
+        assert p["query_block"] % 32 == 0 and p["query_block"] <= prev["query_block"]
+        assert p["blocks"] == -(-n // p["query_block"])
+        prev = p
+    assert prev["blocks"] > 1
+    # the smallest workspace that still plans: bisect on the host planner
+    lo, hi = 0, sizes[-1]
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        try:
+            tod.tod_plan_workspace(n, n, d, k, mid, mode=1)
+            hi = mid
+        except tod.TodError as e:
+            assert e.status == tod.TOD_ERR_WORKSPACE
+            lo = mid
+    p = tod.tod_plan_workspace(n, n, d, k, hi, mode=1)
+    assert p["query_block"] == 32 and p["ref_splits"] == 1
+    with pytest.raises(tod.TodError) as e:
+        tod.tod_plan_workspace(n, n, d, k, hi - 1, mode=1)
+    assert "32-row" in str(e.value)
+    # a caller-fixed block is never re-planned
+    with pytest.raises(tod.TodError):
+        tod.tod_plan_workspace(n, n, d, k, sizes[0], mode=1, opts=tod.options(query_block=n))
