@@ -12,6 +12,13 @@ LIB = os.path.join(HERE, "libtod.so")
 SOURCES = ["api.hip", "prep.hip", "select.hip", "lof.hip", "tile_f32.hip", "tile_f16.hip",
            "tile_bf16.hip", "mtile_f16.hip", "mtile_bf16.hip", "order.hip",
            "rtile_f16.hip", "rtile_bf16.hip", "nwr.hip", "score.hip", "loci.hip"]
+# The fused tile kernels take maxima of MFMA accumulators (fmax, so that the
+# compiler sees the reads and inserts the wait states an MFMA result needs
+# before a VALU reads it).  Their operands are never NaN (prep rejects
+# non-finite input; masked entries are -inf), and -fno-honor-nans lets the
+# compiler form v_max3_f32 without quieting every operand first.
+NO_NAN_SOURCES = {"mtile_f16.hip", "mtile_bf16.hip", "tile_f32.hip", "tile_f16.hip",
+                  "tile_bf16.hip"}
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [
@@ -28,7 +35,8 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(src: str) -> str:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
-        cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        extra = ["-fno-honor-nans"] if src in NO_NAN_SOURCES else []
+        cmd = [HIPCC, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         out = "\n".join(line for line in (r.stdout + r.stderr).splitlines()
                         if "packed-fp32-ops" not in line)

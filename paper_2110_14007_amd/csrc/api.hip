@@ -267,31 +267,41 @@ tod_status fit_plan(Plan* p, size_t ws_bytes, const tod_options& o, std::string*
     *p = q;
     return TOD_OK;
   }
-  q.query_block = 0;  // no partial lists: the fixed part of the layout
-  const size_t fixed = make_layout(q).total;
+  // The grouped scan order needs buffers of its own and applies only with one
+  // split; a shrunken plan may end up with one split where the one-block plan
+  // had several.  The order's buffers are therefore reserved first (where the
+  // order could apply), and left out only when the block does not fit beside
+  // them: the order is an optimisation, the block is not.
   const size_t per = (size_t)q.kprime * sizeof(uint64_t);  // partial-list bytes per row and split
-  if (ws_bytes < fixed + 32 * per + 256) {
-    *why = "not even one 32-row query block fits: need at least " +
-           std::to_string(fixed + 32 * per + 256) + " bytes";
-    return TOD_ERR_WORKSPACE;
-  }
-  const size_t room = ws_bytes - fixed - 256;  // the partial region's alignment slack
-  int64_t qb = (int64_t)(room / per) / 32 * 32;
-  if (qb > q.nq_pad) qb = q.nq_pad;
-  int64_t s = auto_splits(qb, q.nr);
-  const int64_t smax = (int64_t)(room / ((size_t)qb * per));
-  if (s > smax) s = smax;
-  q.query_block = qb;
-  q.blocks = (q.nq + qb - 1) / qb;
-  set_splits(&q, s);
   const bool want = o.reorder > 0 || (o.reorder == 0 && q.nr >= kOrderMinRows);
-  q.order = (q.self && q.tile_kind == 1 && q.splits == 1 && want) ? 1 : 0;
-  if (make_layout(q).total > ws_bytes) {
-    *why = "internal: the fitted plan does not fit";
-    return TOD_ERR_INTERNAL;
+  const bool may_order = q.self && q.tile_kind == 1 && want;
+  size_t need = 0;
+  for (int with_order = may_order ? 1 : 0; with_order >= 0; --with_order) {
+    Plan f = q;
+    f.query_block = 0;  // no partial lists: the fixed part of the layout
+    f.order = with_order;
+    const size_t fixed = make_layout(f).total;
+    need = fixed + 32 * per + 256;
+    if (ws_bytes < need) continue;
+    const size_t room = ws_bytes - fixed - 256;  // the partial region's alignment slack
+    int64_t qb = (int64_t)(room / per) / 32 * 32;
+    if (qb > f.nq_pad) qb = f.nq_pad;
+    int64_t s = auto_splits(qb, f.nr);
+    const int64_t smax = (int64_t)(room / ((size_t)qb * per));
+    if (s > smax) s = smax;
+    f.query_block = qb;
+    f.blocks = (f.nq + qb - 1) / qb;
+    set_splits(&f, s);
+    f.order = (with_order && f.splits == 1) ? 1 : 0;
+    if (make_layout(f).total > ws_bytes) {
+      *why = "internal: the fitted plan does not fit";
+      return TOD_ERR_INTERNAL;
+    }
+    *p = f;
+    return TOD_OK;
   }
-  *p = q;
-  return TOD_OK;
+  *why = "not even one 32-row query block fits: need at least " + std::to_string(need) + " bytes";
+  return TOD_ERR_WORKSPACE;
 }
 
 // Neighbours within range: the fp16 / bf16 MFMA range tile (rtile.h) over

@@ -90,11 +90,13 @@ __device__ __forceinline__ uint32_t lds_off(const void* p) {
 // address lds + 16 * lane (global_load_lds_dwordx4; lds must be wave-uniform).
 // Issued from asm so that the compiler, which cannot tell the LDS buffers
 // apart, does not wait for every staging load before each LDS read; the
-// caller orders them with dl_barrier().  M0 is set right before the load.
+// caller orders them with dl_barrier().  M0 is set right before the load,
+// with the one wait state an LDS DMA needs after an SALU write of M0 (the
+// compiler inserts it for its own code, never inside asm).
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g),
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g),
                "s"(__builtin_amdgcn_readfirstlane(lds))
                : "memory", "m0");
 }
@@ -193,10 +195,15 @@ __device__ __forceinline__ float thr_of(uint64_t e) {
   return e == kEmpty ? -INFINITY : acc_of(e);
 }
 
+// Maximum of three (v_max3_f32, formed by the compiler).  It must stay
+// visible to the compiler: the hardware does not interlock a VALU read of an
+// MFMA result, and the compiler inserts the wait states such a read needs
+// (12 after v_mfma_f32_32x32x16_{f16,bf16} on gfx950) only for instructions
+// it generates itself, not for inline asm.  An asm v_max3_f32 here could read
+// an accumulator the MFMA had not yet written and skip a sub-tile that holds
+// a survivor.  The operands are never NaN, so fmax is the plain maximum.
 __device__ __forceinline__ float max3f(float a, float b, float c) {
-  float d;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
-  return d;
+  return __builtin_fmaxf(__builtin_fmaxf(a, b), c);
 }
 
 // Reference row (0..31 within the sub-tile) of accumulator r in this lane

@@ -66,10 +66,11 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
+// Maximum of three (v_max3_f32, formed by the compiler).  Not inline asm: the
+// compiler inserts the wait states a VALU read of an MFMA result needs only
+// for instructions it generates itself.  The operands are never NaN.
 __device__ __forceinline__ float max3(float a, float b, float c) {
-  float d;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
-  return d;
+  return __builtin_fmaxf(__builtin_fmaxf(a, b), c);
 }
 
 // Reference row (0..31 within the tile) held by accumulator r of `lane`.

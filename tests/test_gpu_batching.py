@@ -59,6 +59,7 @@ def test_lof_small_workspaces(env, prec):
         touched.update(np.nonzero((oidx == r).any(axis=1))[0].tolist())
     compare_scores(base[0], olof, rows, touched, what="LOF")
     full = tod.tod_workspace_size(n, n, d, k, 1, opts)
+    fplan = tod.tod_plan_workspace(n, n, d, k, full, 1, opts)
     least = smallest_workspace(tod, n, n, d, k, 1, opts)
     assert least < full
     for nbytes in (least, least + 40 * 32 * 8 * 64, (least + full) // 2):
@@ -69,7 +70,12 @@ def test_lof_small_workspaces(env, prec):
                                                       return_lists=True)]
         say(prec, "workspace", nbytes, "of", full, "plan", plan, "blocks", st.blocks)
         assert st.blocks == plan["blocks"] and st.query_block == plan["query_block"]
-        assert st.blocks > 1
+        assert st.ref_splits == plan["ref_splits"]
+        # a smaller workspace cuts the queries into more blocks or the
+        # references into fewer splits; the smallest one leaves 32-row blocks
+        assert st.blocks > 1 or st.ref_splits < fplan["ref_splits"]
+        if nbytes == least:
+            assert st.query_block == 32
         for u, v in zip(got, base):
             np.testing.assert_array_equal(u, v)
     with pytest.raises(tod.TodError) as e:

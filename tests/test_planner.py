@@ -137,3 +137,30 @@ def test_workspace_sized_batching(tod):
     # a caller-fixed block is never re-planned
     with pytest.raises(tod.TodError):
         tod.tod_plan_workspace(n, n, d, k, sizes[0], mode=1, opts=tod.options(query_block=n))
+
+
+@pytest.mark.parametrize("prec", ["fp16", "fp32", "bf16"])
+@pytest.mark.parametrize("mode,nq,nr", [(1, 12000, 12000), (0, 1999, 9000), (1, 100_000, 100_000)])
+def test_workspace_sweep_monotone(tod, prec, mode, nq, nr):
+    # Every workspace size either plans or is refused as too small (never an
+    # internal error), acceptance is monotone in the size, and a plan always
+    # covers every query row.  Shrinking the reference splits of a self query
+    # can switch the grouped scan order on, whose buffers the fitted layout
+    # must then hold.
+    d, k = 32, 20
+    opts = tod.options(precision=prec)
+    full = tod.tod_workspace_size(nq, nr, d, k, mode, opts)
+    accepted = False
+    for i in range(1, 161):
+        ws = full * i // 160
+        try:
+            p = tod.tod_plan_workspace(nq, nr, d, k, ws, mode=mode, opts=opts)
+        except tod.TodError as e:
+            assert e.status == tod.TOD_ERR_WORKSPACE, str(e)
+            assert not accepted, "refused %d bytes after accepting less" % ws
+            continue
+        accepted = True
+        assert p["blocks"] * p["query_block"] >= nq
+        assert p["blocks"] == -(-nq // p["query_block"])
+        assert p["query_block"] % 32 == 0 or p["blocks"] == 1
+    assert accepted
