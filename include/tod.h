@@ -152,6 +152,32 @@ tod_status tod_knn(const float* xq, int64_t nq, const float* xr, int64_t nr, int
                    void* stream, int64_t* idx_out, float* dist_out, tod_stats* stats);
 
 /*
+ * tod_knn for callers that cannot allocate device memory (serving loops that
+ * keep allocation off their path, harnesses that forbid hipMalloc): the same
+ * computation and outputs as tod_knn, with no workspace argument.  Its
+ * workspace is a static device array of TOD_NOALLOC_SCRATCH_BYTES inside the
+ * library, one per GPU (the loaded code object holds it until the process
+ * ends); the call makes no hipMalloc, hipFree, HIP event or other allocating
+ * call.  The planner fits the query blocks and reference splits into that
+ * array as it does for a small caller workspace (tod_plan_workspace with
+ * ws_bytes = TOD_NOALLOC_SCRATCH_BYTES gives the plan).
+ *   TOD_ERR_WORKSPACE  the problem does not fit the array (not even one
+ *                      32-row query block beside the fixed buffers, or
+ *                      opts fixes query_block / ref_splits beyond it): use
+ *                      tod_knn with a workspace of its own.
+ * Every call on a GPU shares that GPU's array, and the array keeps the last
+ * call's contents (each call initialises what it reads).  Calls that overlap
+ * on one GPU (other threads, other streams) race on it: the caller
+ * serialises them.  The call still synchronises `stream` before it returns,
+ * so it cannot be captured into a HIP graph.  stats, if given, carries the
+ * plan and row counts; its timings are 0 (no events are created).
+ */
+#define TOD_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+tod_status tod_knn_noalloc(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                           int32_t k, const tod_options* opts, void* stream, int64_t* idx_out,
+                           float* dist_out, tod_stats* stats);
+
+/*
  * kNN-OD scores of X against itself (each point's own row excluded), the
  * detector's fit (Appendix D's fit / decision_scores_):
  *   score_out[n] = opts->score of the k neighbour distances (default: the

@@ -12,6 +12,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -534,8 +535,10 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     he = tod::launch_recheck(p, ar, q0, rows, s);
     if (he != hipSuccess) return hip_fail(he, "recheck launch");
     hipEvent_t re = tm.mark(s);
-    tile_ev.emplace_back(ts, te);
-    rc_ev.emplace_back(te, re);
+    if (tm.on) {
+      tile_ev.emplace_back(ts, te);
+      rc_ev.emplace_back(te, re);
+    }
   }
   hipEvent_t e_rc = tm.mark(s);
   he = tod::launch_fallback(p, a, s);
@@ -726,8 +729,10 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
     if (he == hipSuccess && idx_out) he = tod::launch_range_emit(a, b0, rows, s);
     if (he != hipSuccess) return hip_fail(he, "range verify / emit launch");
     hipEvent_t re = tm.mark(s);
-    tile_ev.emplace_back(ts, te);
-    rc_ev.emplace_back(te, re);
+    if (tm.on) {
+      tile_ev.emplace_back(ts, te);
+      rc_ev.emplace_back(te, re);
+    }
   }
   hipEvent_t e_end = tm.mark(s);
   int64_t total = 0;
@@ -954,6 +959,60 @@ tod_status tod_knn(const float* xq, int64_t nq, const float* xr, int64_t nr, int
   if (!idx_out || !dist_out) return fail(TOD_ERR_INVALID_ARG, "null output pointer");
   return run(xq, nq, xr, nr, d, k, opts, 0, 0, workspace, ws_bytes, stream, idx_out, dist_out,
              nullptr, nullptr, nullptr, 0, nullptr, stats);
+}
+
+// Workspace of tod_knn_noalloc: one copy per GPU, held by the loaded code
+// object from load until the process ends.  Host code never uses this name
+// as an address (on the host it is only a stand-in for the symbol): the
+// device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[TOD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_at[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (looked up on the
+// first call on that device, with that device current).
+tod_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(TOD_ERR_UNSUPPORTED, "tod_knn_noalloc: device ordinal " + std::to_string(dev) +
+                                         " beyond the " + std::to_string(kMaxDevices) +
+                                         " devices it keeps a scratch address for");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_at[dev]) {
+    void* ptr = nullptr;
+    he = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (he != hipSuccess) return hip_fail(he, "hipGetSymbolAddress(scratch)");
+    if (!ptr || ((uintptr_t)ptr & 255))
+      return fail(TOD_ERR_INTERNAL, "tod_knn_noalloc: scratch address null or misaligned");
+    g_scratch_at[dev] = ptr;
+  }
+  *out = g_scratch_at[dev];
+  return TOD_OK;
+}
+}  // namespace
+
+tod_status tod_knn_noalloc(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
+                           int32_t k, const tod_options* opts, void* stream, int64_t* idx_out,
+                           float* dist_out, tod_stats* stats) {
+  g_last_error.clear();
+  if (!idx_out || !dist_out) return fail(TOD_ERR_INVALID_ARG, "null output pointer");
+  void* ws = nullptr;
+  tod_status st = scratch_of_current_device(&ws);
+  if (st != TOD_OK) return st;
+  // No HIP events (their creation may allocate): stats carries the plan and
+  // the row counts, with zero timings.
+  st = run(xq, nq, xr, nr, d, k, opts, 0, 0, ws, TOD_NOALLOC_SCRATCH_BYTES, stream, idx_out,
+           dist_out, nullptr, nullptr, nullptr, 0, nullptr, stats, /*events=*/false);
+  if (st == TOD_ERR_WORKSPACE)
+    return fail(st, "tod_knn_noalloc: the problem does not fit the library's static scratch of " +
+                        std::to_string(TOD_NOALLOC_SCRATCH_BYTES) + " bytes (" + g_last_error +
+                        "); use tod_knn with a workspace of its own");
+  return st;
 }
 
 tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,

@@ -28,7 +28,8 @@ PRECISIONS = {"auto": PREC_AUTO, "fp32": PREC_FP32, "fp16": PREC_FP16, "bf16": P
 PRECISION_NAMES = {v: k for k, v in PRECISIONS.items()}
 SCORES = {"kth": 0, "largest": 0, "mean": 1, "median": 2, "sum": 3}
 
-SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_score", "tod_lof",
+SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_noalloc",
+           "tod_knn_score", "tod_lof",
            "tod_knn_decision", "tod_knn_classify", "tod_abod", "tod_cof", "tod_nwr_workspace_size",
            "tod_nwr", "tod_loci_workspace_size", "tod_loci",
            "tod_plan", "tod_plan_workspace",
@@ -103,6 +104,8 @@ def _load():
     lib.tod_workspace_size.restype = sz
     lib.tod_knn.argtypes = [vp, i64, vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, st_p]
     lib.tod_knn.restype = ctypes.c_int
+    lib.tod_knn_noalloc.argtypes = [vp, i64, vp, i64, i64, i32, opt_p, vp, vp, vp, st_p]
+    lib.tod_knn_noalloc.restype = ctypes.c_int
     lib.tod_knn_score.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, st_p]
     lib.tod_knn_score.restype = ctypes.c_int
     lib.tod_lof.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, vp, st_p]
@@ -295,6 +298,38 @@ def tod_knn(xq, xr, k: int, opts=None, workspace=None, stream=None, stats=None):
                       _stream(stream), _p(idx), _p(dist),
                       ctypes.byref(stats) if stats is not None else None)
     _check(st, "tod_knn")
+    return idx, dist
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TOD_NOALLOC_SCRATCH_BYTES of include/tod.h
+
+
+def tod_knn_noalloc(xq, xr, k: int, opts=None, stream=None, stats=None, out=None):
+    """tod_knn with the library's static scratch as its workspace (no device
+    allocation inside the call) -> (idx int64 [nq,k], dist fp32 [nq,k]).
+    out: optional preallocated (idx, dist) tensors, so that the caller's side
+    allocates nothing either."""
+    torch = _torch()
+    _dev_matrix(xq, "xq")
+    _dev_matrix(xr, "xr")
+    nq, d = xq.shape
+    nr = xr.shape[0]
+    if xr.shape[1] != d:
+        raise ValueError("xq and xr must have the same number of columns")
+    if out is None:
+        idx = torch.empty((nq, k), dtype=torch.int64, device=xq.device)
+        dist = torch.empty((nq, k), dtype=torch.float32, device=xq.device)
+    else:
+        idx, dist = out
+        if (tuple(idx.shape) != (nq, k) or idx.dtype != torch.int64 or not idx.is_contiguous()
+                or tuple(dist.shape) != (nq, k) or dist.dtype != torch.float32
+                or not dist.is_contiguous()):
+            raise ValueError("out must be contiguous (int64 [nq,k], fp32 [nq,k]) tensors")
+    st = _lib.tod_knn_noalloc(_p(xq), nq, _p(xr), nr, d, int(k),
+                              ctypes.byref(opts) if opts is not None else None,
+                              _stream(stream), _p(idx), _p(dist),
+                              ctypes.byref(stats) if stats is not None else None)
+    _check(st, "tod_knn_noalloc")
     return idx, dist
 
 
