@@ -123,6 +123,9 @@ typedef struct {
   int64_t pairs_in_range;  /* tod_nwr: pairs within the threshold */
   int32_t tail_parts;      /* parts the last partly filled round was scanned in (1: none) */
   int64_t tail_rows;       /* query rows scanned in parts, summed over the blocks */
+  int32_t list_runs;       /* 2 if each shortlist was built as two runs of K'/2 entries (the
+                            * register-list tile over two pieces of the scan order: K' = 128
+                            * on rows of 129..512 elements), else 1 */
 } tod_stats;
 
 /* Fill *opts with defaults (AUTO precision, planner-chosen sizes). */

@@ -171,6 +171,18 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   // of at most 8 elements carry the accumulator seed -N_j/2 in their padding
   // (columns 8..11 of a 16-wide row); longer rows get it from LDS.
   p->tile_kind = (prec != TOD_PREC_FP32 && d <= 512 && kp <= 64) ? 1 : 0;
+  // K' = 128 on rows of 256 or more elements (bf16 at k of 33..64): the
+  // register-list kernel with 64-entry lists over two pieces of the scan
+  // order.  Every reference a piece left out has a key >= that piece's 64th,
+  // so the recheck bounds the excluded references by the smaller of the two
+  // run ends.  (A 128-entry register list beside the 128-register query
+  // operand leaves the compiler too few registers: it spills the operand to
+  // scratch memory.)
+  p->runs = 1;
+  if (prec != TOD_PREC_FP32 && d <= 512 && kp == 128 && p->dpad_t >= 256) {
+    p->tile_kind = 1;
+    p->runs = 2;
+  }
   if (p->tile_kind == 1) {
     p->waves_per_group = 4;
     if (d <= 8) {
@@ -185,12 +197,14 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   // reference split (each workgroup then scans the whole set from its own
   // group on); by default from kOrderMinRows references on.
   const bool want = o.reorder > 0 || (o.reorder == 0 && nr >= kOrderMinRows);
-  p->order = (self && p->tile_kind == 1 && p->splits == 1 && want) ? 1 : 0;
-  // Tail split of the register-list tile with one reference split.
+  // (With runs, the tile scans the whole set in pieces whatever S is.)
+  p->order = (self && p->tile_kind == 1 && (p->splits == 1 || p->runs > 1) && want) ? 1 : 0;
+  // Tail split of the register-list tile with one reference split (not with
+  // runs: their pieces already halve every workgroup's scan).
   p->tail_parts = 1;
   p->tail_auto = 0;
   p->tail_lists = 0;
-  if (p->tile_kind == 1 && p->splits == 1 && o.tail_parts != 1) {
+  if (p->tile_kind == 1 && p->splits == 1 && p->runs == 1 && o.tail_parts != 1) {
     p->tail_parts = o.tail_parts == 0 ? kMaxTailParts : o.tail_parts;
     p->tail_auto = o.tail_parts == 0 ? 1 : 0;
     const int64_t want_lists = p->query_block * p->tail_parts;
@@ -293,7 +307,7 @@ tod_status fit_plan(Plan* p, size_t ws_bytes, const tod_options& o, std::string*
     f.query_block = qb;
     f.blocks = (f.nq + qb - 1) / qb;
     set_splits(&f, s);
-    f.order = (with_order && f.splits == 1) ? 1 : 0;
+    f.order = (with_order && (f.splits == 1 || f.runs > 1)) ? 1 : 0;
     if (make_layout(f).total > ws_bytes) {
       *why = "internal: the fitted plan does not fit";
       return TOD_ERR_INTERNAL;
@@ -481,6 +495,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.rho_q = (double*)(base + L.rho_q);
   a.partial = (uint64_t*)(base + L.partial);
   a.parts = 1;
+  a.runs = p.runs;
   a.tail_parts = 1;
   a.tail_q0 = p.nq;
   a.ptail = p.tail_lists ? (uint64_t*)(base + L.ptail) : nullptr;
@@ -583,6 +598,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     stats->pairs_candidate = stats->pairs_uncertain = stats->pairs_in_range = 0;
     stats->tail_parts = tail_parts;
     stats->tail_rows = tail_rows;
+    stats->list_runs = p.runs;
     stats->ms_prep = Timers::ms(e0, e_prep);
     float t = 0.0f, r = 0.0f;
     for (auto& pr : tile_ev) t += Timers::ms(pr.first, pr.second);
@@ -765,6 +781,7 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
     stats->pairs_in_range = total;
     stats->tail_parts = 1;
     stats->tail_rows = 0;
+    stats->list_runs = 1;
   }
   if (host.internal) return fail(TOD_ERR_INTERNAL, "range tile passes disagree");
   if (idx_out && total > capacity)
@@ -1142,6 +1159,7 @@ tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_opti
   plan->blocks = p.blocks;
   plan->tile_launches = p.blocks;
   plan->reordered = p.order;
+  plan->list_runs = p.runs;
   return TOD_OK;
 }
 
@@ -1180,6 +1198,7 @@ tod_status tod_plan_workspace(int64_t nq, int64_t nr, int64_t d, int32_t k, int3
   plan->blocks = p.blocks;
   plan->tile_launches = p.blocks;
   plan->reordered = p.order;
+  plan->list_runs = p.runs;
   return TOD_OK;
 }
 

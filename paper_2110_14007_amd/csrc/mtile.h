@@ -877,6 +877,22 @@ hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q
     if (e != hipSuccess) return e;
   }
   const int64_t wgs = (q_rows + QW - 1) / QW;
+  if (p.runs > 1) {
+    // Runs: every workgroup's scan in runs x S pieces of the scan order, each
+    // piece's list at partial + (query (runs S) + piece) K'/runs, i.e. the
+    // recheck's S lists of K' entries, `runs` ascending runs each.
+    Args b = a;
+    b.parts = p.runs * p.splits;
+    b.splits = 1;
+    b.split_len = a.nr;
+    hipLaunchKernelGGL(kern, dim3((unsigned)wgs, (unsigned)b.parts), dim3(W * 64), lds, st, b,
+                       q_begin, q_rows);
+    if (tail) {
+      tail->q0 = q_rows;
+      tail->parts = 1;
+    }
+    return hipGetLastError();
+  }
   int64_t main_wgs = wgs;
   int parts = 1;
   if (p.splits == 1 && p.tail_parts > 1 && a.ptail) {
@@ -924,6 +940,12 @@ hipError_t launch_mtile_r(const Plan& p, const Args& a, int64_t q_begin, int64_t
     case 16: return launch_mtile<ET, DPAD, FOLD, 8>(p, a, q_begin, q_rows, st, tail);
     case 32: return launch_mtile<ET, DPAD, FOLD, 16>(p, a, q_begin, q_rows, st, tail);
     case 64: return launch_mtile<ET, DPAD, FOLD, 32>(p, a, q_begin, q_rows, st, tail);
+    case 128:  // two runs of 64 (rows of 256 or more elements)
+      if constexpr (DPAD >= 256 && !FOLD)
+        return p.runs == 2 ? launch_mtile<ET, DPAD, FOLD, 32>(p, a, q_begin, q_rows, st, tail)
+                           : hipErrorInvalidValue;
+      else
+        return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }

@@ -217,12 +217,27 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     const int nlists = tl ? a.tail_parts : a.splits;
     const uint64_t* src =
         tl ? a.ptail + (ql - a.tail_q0) * a.tail_parts * KP : a.partial + ql * a.splits * KP;
+    // With runs (a.runs == 2, K' = 128) a list holds two ascending runs of
+    // 64, each the best of one piece of the scan order: they are merged into
+    // one ascending list, and `cap`, the smaller of the run ends, bounds every
+    // reference a run left out (a run that is not full left none out).
+    uint64_t cap = kEmpty;
+    auto sort_runs = [&](uint64_t(&v)[EL]) __attribute__((always_inline)) {
+      if constexpr (EL == 2) {
+        if (a.runs == 2) {
+          cap = umin64(cap, umin64(shfl64(v[0], 63), shfl64(v[1], 63)));
+          v[1] = shfl_xor64(v[1], 63);  // run 1 descending: the pair is bitonic
+          bitonic_merge<2>(v, lane);
+        }
+      }
+    };
     uint64_t list[EL];
 #pragma unroll
     for (int r = 0; r < EL; ++r) {
       const int e = r * 64 + lane;
       list[r] = e < KP ? src[e] : kEmpty;
     }
+    sort_runs(list);
     for (int s = 1; s < nlists; ++s) {
       uint64_t other[EL];
 #pragma unroll
@@ -230,6 +245,7 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         const int e = r * 64 + lane;
         other[r] = e < KP ? src[(int64_t)s * KP + e] : kEmpty;
       }
+      sort_runs(other);
       merge_lists<EL>(list, other, lane);
     }
 #pragma unroll
@@ -280,7 +296,7 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         break;
       }
       // Every reference outside the first m candidates has a key >= h.
-      const uint64_t hent = m < KP ? sl[wave][m] : sl[wave][KP - 1];
+      const uint64_t hent = umin64(m < KP ? sl[wave][m] : sl[wave][KP - 1], cap);
       ok = certified(cc, ni, rho_i, hent, stau[wave]);
       if (ok || m >= KP) break;
       m = m + 16 < KP ? m + 16 : KP;

@@ -40,6 +40,9 @@ struct Plan {
   int32_t lists;       // int32 / fp64 neighbour lists kept in the workspace (LOF, score
                        // aggregates, classifier)
   int32_t order;       // 1: grouped scan order (order.hip), X against X only
+  int32_t runs = 1;    // 2: the register-list tile scans the references in 2 S pieces of the
+                       // scan order with lists of K' / 2; each query's K' slots per split
+                       // then hold two ascending runs (rows of 256+ elements, K' = 128)
   int32_t tail_parts = 1;  // most parts a tail workgroup's scan is cut into (1: no tail split)
   int32_t tail_auto = 0;   // 1: pick the parts by the model in tail_pieces; 0: use tail_parts
   int64_t tail_lists = 0;  // K' lists the tail region holds (query rows x parts)
@@ -132,6 +135,10 @@ struct Args {
   // piece) * K'.  The recheck takes the rows of its block from tail_q0 on
   // from ptail, tail_parts lists each.
   int32_t parts;
+  // runs > 1: each K' list the recheck reads holds `runs` ascending runs of
+  // K' / runs entries (pieces of the scan order); they are merged there, and
+  // every reference a run left out has a key >= that run's last entry.
+  int32_t runs;
   int32_t tail_parts;
   int64_t tail_q0;
   uint64_t* ptail;

@@ -76,6 +76,7 @@ class tod_stats(ctypes.Structure):
         ("pairs_in_range", ctypes.c_int64),
         ("tail_parts", ctypes.c_int32),
         ("tail_rows", ctypes.c_int64),
+        ("list_runs", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:
@@ -199,7 +200,7 @@ def tod_plan_workspace(nq: int, nr: int, d: int, k: int, ws_bytes: int, mode: in
     _check(st, "tod_plan_workspace")
     return {"precision": PRECISION_NAMES[s.precision], "kprime": s.kprime,
             "ref_splits": s.ref_splits, "query_block": s.query_block, "blocks": s.blocks,
-            "reordered": s.reordered}
+            "reordered": s.reordered, "list_runs": s.list_runs}
 
 
 def tod_plan(nq: int, nr: int, d: int, k: int, opts=None) -> dict:
@@ -209,7 +210,7 @@ def tod_plan(nq: int, nr: int, d: int, k: int, opts=None) -> dict:
            "tod_plan")
     return {"precision": PRECISION_NAMES[s.precision], "kprime": s.kprime,
             "ref_splits": s.ref_splits, "query_block": s.query_block, "blocks": s.blocks,
-            "reordered": bool(s.reordered)}
+            "reordered": bool(s.reordered), "list_runs": s.list_runs}
 
 
 # ---------------------------------------------------------------------------
