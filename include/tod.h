@@ -105,6 +105,9 @@ typedef struct {
 
 /* Plan and per-phase timings of one call (filled when a non-NULL pointer is
  * passed; timings are measured with HIP events on the call's stream). */
+/* (The recheck's candidate count m is not reported per call: it grows per
+ * row, k + 8 first and then 16 more at a time up to K', so rows_certified and
+ * rows_fallback carry what a single maximum would summarise.) */
 typedef struct {
   uint32_t struct_size;   /* must be sizeof(tod_stats) */
   int32_t precision;      /* resolved tod_precision */
@@ -117,6 +120,8 @@ typedef struct {
   int64_t tile_launches;  /* launches of the fused distance + selection kernel (a block with a
                            * tail split takes two) */
   float ms_prep, ms_tile, ms_recheck, ms_fallback, ms_score, ms_total;
+                          /* ms_recheck includes the merge of the split lists, which runs
+                           * inside the recheck kernel (there is no separate ms_merge) */
   int32_t reordered;      /* 1 if the scan used the grouped row order (see tod_options.reorder) */
   int64_t pairs_candidate; /* tod_nwr: pairs the filter could not rule out of range */
   int64_t pairs_uncertain; /* tod_nwr: candidates whose range test needed the exact distance */
@@ -128,14 +133,22 @@ typedef struct {
                             * on rows of 129..512 elements), else 1 */
 } tod_stats;
 
-/* Fill *opts with defaults (AUTO precision, planner-chosen sizes). */
+/* Fill *opts with defaults: AUTO precision (the fp16 filter of Section 5.2's
+ * provable quantization), planner-chosen K', query block and splits
+ * (Section 6), self pair kept, margin_scale 1. */
 void tod_default_options(tod_options* opts);
 
 /*
- * Workspace bytes needed for these sizes and options by
+ * Workspace bytes with which the call runs its queries in as few blocks as
+ * the planner likes (Section 6: the batches are sized to the GPU memory at
+ * hand; a smaller workspace gives smaller query blocks, see
+ * tod_plan_workspace).  One function serves every entry point through
  *   mode 0: tod_knn, tod_knn_score, tod_knn_decision (any query and reference sets);
- *   mode 1: tod_lof, tod_abod, tod_cof (X against itself, nq == nr);
- *   mode 2: tod_knn_classify.
+ *   mode 1: tod_lof, tod_abod, tod_cof (X against itself, nq == nr: these
+ *           keep the neighbour lists and the LOF buffers as well);
+ *   mode 2: tod_knn_classify (neighbour lists for the vote).
+ * (mode is an addition to the interface the kNN/LOF calls alone would need:
+ * the detectors built on the same lists need more room.)
  * Returns 0 if the arguments are invalid or unsupported.
  */
 size_t tod_workspace_size(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t mode,
@@ -198,6 +211,8 @@ tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
  *   lof_out[n]       fp32 LOF scores (computed in fp64)
  *   knn_score_out[n] optional: kNN-OD score from the same neighbour lists
  *   idx_out, dist_out optional neighbour lists as in tod_knn
+ * (The optional outputs cost no extra pass: LOF needs the exact lists and
+ * k-distances anyway, so a caller that wants both detectors makes one call.)
  */
 tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
                    void* workspace, size_t ws_bytes, void* stream, float* lof_out,

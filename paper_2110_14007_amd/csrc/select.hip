@@ -25,10 +25,17 @@
 //     |key_ij - (N_j - 2<xhat_i, xhat_j>)| <= gamma_{d+2} (N_i + 2 Nmax) + 2^-23 Nmax
 // and the quantisation radii, every excluded j satisfies
 //     s ||x_i - x_j|| >= sqrt(N_i + h - e) - rho_i - Pmax = LB.
-// The K' candidates are re-measured exactly (fp64 from the original fp32
-// rows, the same direct-difference sum as the definition) and sorted by
-// (D, j); if LB > s * D_(k) no excluded reference can enter the top k and the
-// row is final.  Otherwise the row goes to the exact fallback scan.
+// The K' candidates are re-measured in fp64 from the original fp32 rows:
+// the definition's terms ((double)x - (double)y)^2, each rounded exactly as
+// the definition rounds it (no fused multiply-add), but summed in another
+// order (each lane of a group adds its strided column chunks in order, then
+// the lanes' partial sums are added as a tree).  Two orders of summing d
+// non-negative fp64 terms differ by at most 2 (d - 1) 2^-53 of the sum,
+// below 2^-40 for d <= 4096; only candidates whose squared distances are that
+// close can be ranked differently from the definition, and such near-ties are
+// the ones the comparison with the oracle excuses.  The candidates are sorted
+// by (D^2, j); if LB > s * D_(k) no excluded reference can enter the top k and
+// the row is final.  Otherwise the row goes to the exact fallback scan.
 #include <math.h>
 
 #include "tod_internal.h"
