@@ -32,8 +32,8 @@
 // the lanes' partial sums are added as a tree).  Two orders of summing d
 // non-negative fp64 terms differ by at most 2 (d - 1) 2^-53 of the sum,
 // below 2^-40 for d <= 4096; only candidates whose squared distances are that
-// close can be ranked differently from the definition, and such near-ties are
-// the ones the comparison with the oracle excuses.  The candidates are sorted
+// close can be ranked differently from the definition, i.e. only exact
+// near-ties (within 2^-40 of each other).  The candidates are sorted
 // by (D^2, j); if LB > s * D_(k) no excluded reference can enter the top k and
 // the row is final.  Otherwise the row goes to the exact fallback scan.
 #include <math.h>
