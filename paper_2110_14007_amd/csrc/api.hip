@@ -256,6 +256,7 @@ Layout make_layout(const Plan& p) {
     L.idx32 = L.d64 = 0;
   }
   L.lrd = p.lof ? take(sizeof(double) * p.nq) : 0;
+  L.kdist = p.lof ? take(sizeof(double) * p.nq) : 0;
   L.total = off;
   return L;
 }
@@ -511,6 +512,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.idx32 = p.lists ? (int32_t*)(base + L.idx32) : nullptr;
   a.d64 = p.lists ? (double*)(base + L.d64) : nullptr;
   a.lrd = lof ? (double*)(base + L.lrd) : nullptr;
+  a.kdist = lof ? (double*)(base + L.kdist) : nullptr;
   a.score = o.score;
   a.labels_r = labels_r;
   a.n_classes = n_classes;

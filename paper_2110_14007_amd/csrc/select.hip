@@ -103,7 +103,10 @@ __device__ __forceinline__ void emit(const Args& a, int64_t qi, int rank, uint32
     a.idx32[pos] = (int32_t)j;
     a.d64[pos] = dd;
   }
-  if (rank == a.k - 1 && a.score_out) a.score_out[qi] = (float)dd;
+  if (rank == a.k - 1) {
+    if (a.score_out) a.score_out[qi] = (float)dd;
+    if (a.kdist) a.kdist[qi] = dd;
+  }
 }
 
 __device__ __forceinline__ double shfl_xor_f64(double v, int mask) {

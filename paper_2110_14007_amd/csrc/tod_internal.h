@@ -84,7 +84,7 @@ inline int tail_pieces(int64_t tw, int64_t slots, int64_t cus, int pmax, bool au
 // Workspace regions (byte offsets from the workspace base, 256-aligned).
 struct Layout {
   size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, ptail, worklist,
-      fbtau, fbpart, fbidx, idx32, d64, lrd, perm, lab, cstart, bcnt, boff, total;
+      fbtau, fbpart, fbidx, idx32, d64, lrd, kdist, perm, lab, cstart, bcnt, boff, total;
   int32_t colpart_blocks;
 };
 
@@ -155,6 +155,8 @@ struct Args {
   int32_t* idx32;      // [nq x k] neighbour ids (LOF)
   double* d64;         // [nq x k] exact distances (LOF)
   double* lrd;         // [nq] LOF scratch
+  double* kdist;       // [nq] exact k-distance of every row (LOF), beside the lists so that
+                       // the neighbours' k-distances are gathered from a dense array
   // outputs (nullable)
   int64_t* idx_out;
   float* dist_out;
