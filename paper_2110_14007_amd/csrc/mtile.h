@@ -769,16 +769,21 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     static_assert(TR == 8 * W && W == 4, "direct staging: 8 rows and 8 seeds per wave");
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     const uint32_t lbase = lds_off(smem);
+    // The rows a wave stages depend on the wave only, so their addresses are
+    // formed in scalar registers (one wave index read through readfirstlane,
+    // used by the staging alone); only the lane's 16-byte offset is a vector
+    // value.
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
     auto dl_issue = [&](int64_t t0, int b) __attribute__((always_inline)) {
 #pragma unroll
       for (int i = 0; i < TR / W; ++i) {
-        const int r = wave + W * i;
+        const int r = wv + W * i;
         const int64_t gr = t0 + r < r_end32 ? t0 + r : r_end32 - 1;
         dma16(xr_bytes + gr * (int64_t)(DPAD * 2) + lane * 16, lbase + b * STAGE + r * ROWB);
       }
       if (lane < 2)  // rows t0 .. t0 + 31 all exist (t0 is a multiple of 32 below r_end)
-        dma16((const unsigned char*)(a.hn_r + t0 + 8 * wave) + lane * 16,
-              lbase + NBUF * STAGE + (b * TR + 8 * wave) * (int)sizeof(float));
+        dma16((const unsigned char*)(a.hn_r + t0 + 8 * wv) + lane * 16,
+              lbase + NBUF * STAGE + (b * TR + 8 * wv) * (int)sizeof(float));
     };
     if constexpr (NBUF == 3) {
       dl_issue(t_of(0), 0);
