@@ -744,9 +744,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // the scan order.
   int nscan = nst;
   if (pieces) {
-    // 32-bit: nst < 2^26 and parts <= 8
-    const int ib = (int)((uint32_t)(split * nst) / (uint32_t)a.parts);
-    nscan = (int)((uint32_t)((split + 1) * nst) / (uint32_t)a.parts) - ib;
+    // (64-bit products: up to 128 pieces with two runs of 64 splits.)
+    const int ib = (int)((int64_t)split * nst / a.parts);
+    nscan = (int)((int64_t)(split + 1) * nst / a.parts) - ib;
     st0 += ib;
     st0 = st0 >= nst ? st0 - nst : st0;
   }
