@@ -594,7 +594,34 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   }                                                                                         \
   if (!FOLD && tid < TR / 4) *reinterpret_cast<float4*>(hnb + (B) * TR + 4 * tid) = REGH;
 
-  // One stage: its sub-tiles from LDS buffer b.
+  // Direct staging (rows of 512 elements): each wave moves 8 whole rows (one
+  // 1 KiB row per instruction) and 8 seeds of a stage straight into LDS.
+  // The rows a wave stages depend on the wave only, so their addresses are
+  // formed in scalar registers (one wave index read through readfirstlane,
+  // used by the staging alone); only the lane's 16-byte offset is a vector
+  // value.  A stage starts at a multiple of 32 below the split's end, so all
+  // its 32 rows exist in the padded copy.  dl_row(i) issues row i (i < 8) or
+  // the seeds (i = 8) of the stage set by dl_t0 / dl_b.
+  const uint32_t lbase = lds_off(smem);
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  int64_t dl_t0 = 0;
+  int dl_b = 0;
+  auto dl_row = [&](int i) __attribute__((always_inline)) {
+    if (i < TR / W) {
+      const int r = wv + W * i;
+      dma16(xr_bytes + (dl_t0 + r) * (int64_t)(DPAD * 2) + lane * 16,
+            lbase + dl_b * STAGE + r * ROWB);
+    } else if (lane < 2) {
+      dma16((const unsigned char*)(a.hn_r + dl_t0 + 8 * wv) + lane * 16,
+            lbase + NBUF * STAGE + (dl_b * TR + 8 * wv) * (int)sizeof(float));
+    }
+  };
+  constexpr int kDlRows = TR / W + 1;  // staging loads per wave and stage
+
+  // One stage: its sub-tiles from LDS buffer b.  With direct staging the
+  // loads of the stage set by dl_t0 / dl_b are issued between the MFMAs of
+  // the chain (one after every third k-step), where the wave would otherwise
+  // wait for its own MFMAs.
   auto stage_body = [&](int64_t t0, int b) __attribute__((always_inline)) {
     const unsigned char* buf = stage + b * STAGE;
     const float* hn = hnb + b * TR;
@@ -617,23 +644,50 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     // the LDS reads of later k-steps then run under the MFMAs of earlier ones.
     auto group = [&](int g0) __attribute__((always_inline)) {
       constexpr std::integral_constant<int, 0> Z{};
-      V af[NG][KC];
       f32x16 acc[NG][NQ];
+      if constexpr (DL) {
+        // One sub-tile.  The staging loads are ordered against the LDS reads
+        // (asm with side effects), so the reads ahead of the chain are
+        // written out in the order they are to run: fragment c + kAhead is
+        // read as fragment c enters the chain, and after every third k-step
+        // one staging row is issued.
+        static_assert(NG == 1, "one sub-tile per stage");
+        V w[kAhead];
 #pragma unroll
-      for (int s = 0; s < NG; ++s) {
+        for (int c = 0; c < kAhead; ++c) w[c] = afrag(buf, g0, c);
+        acc[0][0] = seed(hn, g0);
 #pragma unroll
-        for (int c = 0; c < KC; ++c) af[s][c] = afrag(buf, g0 + s, c);
-        acc[s][0] = seed(hn, g0 + s);
+        for (int u = 1; u < NQ; ++u) acc[0][u] = acc[0][0];
 #pragma unroll
-        for (int u = 1; u < NQ; ++u) acc[s][u] = acc[s][0];
+        for (int c = 0; c < KC; ++c) {
+          const V cur = w[c % kAhead];
+          if (c + kAhead < KC) w[c % kAhead] = afrag(buf, g0, c + kAhead);
+#pragma unroll
+          for (int u = 0; u < NQ; ++u) acc[0][u] = mfma<ET>(cur, bq[u][c], acc[0][u]);
+          if (c % 3 == 1 && c / 3 < TR / W) dl_row(c / 3);
+        }
+      } else {
+        // (Addresses from the group's first row: the sub-tile offsets are
+        // then immediate offsets of the LDS reads.)
+        const unsigned char* gbuf = buf + g0 * (32 * ROWB);
+        const float* ghn = hn + 32 * g0;
+        V af[NG][KC];
+#pragma unroll
+        for (int s = 0; s < NG; ++s) {
+#pragma unroll
+          for (int c = 0; c < KC; ++c) af[s][c] = afrag(gbuf, s, c);
+          acc[s][0] = seed(ghn, s);
+#pragma unroll
+          for (int u = 1; u < NQ; ++u) acc[s][u] = acc[s][0];
+        }
+        // Every A fragment feeds the MFMAs of all NQ query groups.
+#pragma unroll
+        for (int c = 0; c < KC; ++c)
+#pragma unroll
+          for (int s = 0; s < NG; ++s)
+#pragma unroll
+            for (int u = 0; u < NQ; ++u) acc[s][u] = mfma<ET>(af[s][c], bq[u][c], acc[s][u]);
       }
-      // Every A fragment feeds the MFMAs of all NQ query groups.
-#pragma unroll
-      for (int c = 0; c < KC; ++c)
-#pragma unroll
-        for (int s = 0; s < NG; ++s)
-#pragma unroll
-          for (int u = 0; u < NQ; ++u) acc[s][u] = mfma<ET>(af[s][c], bq[u][c], acc[s][u]);
       if constexpr (kInterleave) {
         __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
 #pragma unroll
@@ -760,48 +814,46 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   };
 
   if constexpr (DL) {
-    // Rows of 512 elements: each wave moves 8 whole rows (one 1 KiB row per
-    // instruction) and 8 seeds of every stage straight into LDS, two stages
-    // ahead with three buffers, one stage ahead with two, 9 loads per wave
-    // per stage.  The compiler-visible wait first
-    // retires the query operand's loads, so that the compiler, which does
-    // not see the staging loads, has no load of its own left to wait for.
+    // Rows of 512 elements: two stages ahead with three buffers, one stage
+    // ahead with two.  The compiler-visible wait first retires the query
+    // operand's loads, so that the compiler, which does not see the staging
+    // loads, has no load of its own left to wait for.
     static_assert(TR == 8 * W && W == 4, "direct staging: 8 rows and 8 seeds per wave");
+    static_assert(KC >= 3 * (TR / W), "staging loads spread over the MFMA chain");
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    const uint32_t lbase = lds_off(smem);
-    // The rows a wave stages depend on the wave only, so their addresses are
-    // formed in scalar registers (one wave index read through readfirstlane,
-    // used by the staging alone); only the lane's 16-byte offset is a vector
-    // value.
-    const int wv = __builtin_amdgcn_readfirstlane(wave);
     auto dl_issue = [&](int64_t t0, int b) __attribute__((always_inline)) {
+      dl_t0 = t0;
+      dl_b = b;
 #pragma unroll
-      for (int i = 0; i < TR / W; ++i) {
-        const int r = wv + W * i;
-        const int64_t gr = t0 + r < r_end32 ? t0 + r : r_end32 - 1;
-        dma16(xr_bytes + gr * (int64_t)(DPAD * 2) + lane * 16, lbase + b * STAGE + r * ROWB);
-      }
-      if (lane < 2)  // rows t0 .. t0 + 31 all exist (t0 is a multiple of 32 below r_end)
-        dma16((const unsigned char*)(a.hn_r + t0 + 8 * wv) + lane * 16,
-              lbase + NBUF * STAGE + (b * TR + 8 * wv) * (int)sizeof(float));
+      for (int i = 0; i < kDlRows; ++i) dl_row(i);
+    };
+    // The seeds of stage (tn, bn) are loaded first (two lanes: a branch, kept
+    // out of the chain); a stage body issues the rows inside its chain, and a
+    // wave with no queries has no chain and issues them itself.
+    auto dl_body = [&](int64_t t0, int b, int64_t tn, int bn) __attribute__((always_inline)) {
+      dl_t0 = tn;
+      dl_b = bn;
+      dl_row(TR / W);
+      if (active) stage_body(t0, b);
+      else
+#pragma unroll
+        for (int i = 0; i < TR / W; ++i) dl_row(i);
     };
     if constexpr (NBUF == 3) {
       dl_issue(t_of(0), 0);
       dl_issue(t_of(1), 1);
-      dl_barrier<TR / W + 1>();
+      dl_barrier<kDlRows>();
       for (int it = 0; it < nscan; ++it) {
         // Buffer (it + 2) % 3 was last read in trip it - 1, before its barrier.
-        dl_issue(t_of(it + 2), (it + 2) % 3);
-        stage_body(t_of(it), it % 3);
-        dl_barrier<TR / W + 1>();
+        dl_body(t_of(it), it % 3, t_of(it + 2), (it + 2) % 3);
+        dl_barrier<kDlRows>();
       }
     } else {
       dl_issue(t_of(0), 0);
       dl_barrier<0>();
       for (int it = 0; it < nscan; ++it) {
         // Buffer (it + 1) & 1 was last read in trip it - 1, before its barrier.
-        dl_issue(t_of(it + 1), (it + 1) & 1);
-        stage_body(t_of(it), it & 1);
+        dl_body(t_of(it), it & 1, t_of(it + 1), (it + 1) & 1);
         dl_barrier<0>();
       }
     }
