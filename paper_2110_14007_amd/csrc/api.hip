@@ -593,7 +593,8 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
     stats->ref_splits = p.splits;
     stats->query_block = p.query_block;
     stats->blocks = p.blocks;
-    stats->rows_certified = (int64_t)host.certified;
+    // Every query row is either certified or on the worklist.
+    stats->rows_certified = p.nq - (int64_t)host.worklist_count;
     stats->rows_fallback = (int64_t)host.worklist_count;
     stats->tile_launches = launches;
     stats->reordered = p.order;
@@ -779,7 +780,9 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
     stats->ms_score = 0.0f;
     stats->ms_total = Timers::ms(e0, e_end);
     stats->pairs_candidate = g[L.groups];
-    stats->pairs_uncertain = (int64_t)host.uncertain;
+    int64_t unc = 0;
+    for (int i = 0; i < tod::kUncParts; ++i) unc += (int64_t)host.uncertain[i * tod::kUncStride];
+    stats->pairs_uncertain = unc;
     stats->pairs_in_range = total;
     stats->tail_parts = 1;
     stats->tail_rows = 0;

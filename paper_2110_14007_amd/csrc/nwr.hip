@@ -125,7 +125,9 @@ range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
   if (nx) exact_pass();
   if (lane == 0) {
     a.incnt[row] = kept;
-    if (unc) atomicAdd((unsigned long long*)&a.ctrl->uncertain, (unsigned long long)unc);
+    if (unc)
+      atomicAdd((unsigned long long*)&a.ctrl->uncertain[(blockIdx.x % kUncParts) * kUncStride],
+                (unsigned long long)unc);
   }
 }
 

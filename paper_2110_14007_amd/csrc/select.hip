@@ -210,10 +210,11 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (a.ctrl->nonfinite) return;
   const CertConst cc = cert_const(a);
-  // Each wave walks the block's queries with a grid stride and counts its
-  // certified rows locally (one atomic per wave: a counter bumped once per
-  // query serialises millions of same-address atomics).
-  uint64_t ncert = 0;
+  // Each wave walks the block's queries with a grid stride.  (Every row is
+  // either certified or put on the worklist, so the host derives the number
+  // of certified rows from the worklist count: no counter of their own, whose
+  // same-address atomics, one per wave, cost as much as the rest of the
+  // kernel at 10^5 rows.)
   for (int64_t ql = (int64_t)blockIdx.x * W + wave; ql < q_rows; ql += (int64_t)gridDim.x * W) {
     // With the grouped scan order the filter worked on positions: the query's
     // input row is perm[position], and so is every candidate's (mapped below,
@@ -319,7 +320,6 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         if (c < m && rank[r] >= 0 && rank[r] < k)
           emit(a, qi, rank[r], index_of(sl[wave][c]), sd2[wave][c]);
       }
-      ++ncert;
     } else if (lane == 0) {
       const uint32_t w = atomicAdd(&a.ctrl->worklist_count, 1u);
       a.worklist[w] = (int32_t)qi;
@@ -327,7 +327,174 @@ recheck_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     }
     wave_lds_sync();  // the next query reuses this wave's LDS rows
   }
-  if (lane == 0 && ncert) atomicAdd((unsigned long long*)&a.ctrl->certified, (unsigned long long)ncert);
+}
+
+// Recheck of short lists over short rows: one lane per candidate.
+//
+// With K' <= 32 entries and rows of at most 64 elements (a multiple of four),
+// a wave takes 64 / K' queries at once, K' lanes each, and lane g of a
+// query's group measures the query's g-th candidate alone.  Its exact D^2 is
+// then the definition's own sum: fp64, columns in order, no fused
+// multiply-add.  All K' candidates are measured at once, so the certificate
+// takes h = the K'-th key, the largest bound the list gives.  (The general
+// kernel above stops at the first m whose h certifies; a row it certifies is
+// certified here too, and the exact k nearest are the same.)  The group's
+// (D^2, j) pairs are sorted by a bitonic network across its lanes, after
+// which lane r of the group holds rank r.
+// Value of v in lane (lane ^ m) for m in {1, 2, 4, 8, 16}: DPP quad
+// permutations for 1 and 2, a bit-mask swizzle (within 32 lanes) otherwise;
+// neither goes through LDS memory.
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v, int m) {
+  switch (m) {
+    case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+    case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
+    case 4: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (4 << 10));
+    case 8: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (8 << 10));
+    default: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (16 << 10));
+  }
+}
+__device__ __forceinline__ uint64_t lane_xor64(uint64_t v, int m) {
+  return ((uint64_t)lane_xor((uint32_t)(v >> 32), m) << 32) | lane_xor((uint32_t)v, m);
+}
+
+// DC: the most 16-byte chunks of a row (d <= 4 DC).
+template <int KP, int W, int DC>
+__global__ void __launch_bounds__(W * 64)
+    __attribute__((amdgpu_waves_per_eu(DC <= 4 ? 4 : (DC == 8 ? 3 : 2))))
+recheck_lanes_kernel(Args a, int64_t q_begin, int64_t q_rows) {
+#pragma clang fp contract(off)
+  static_assert(KP == 16 || KP == 32, "groups of 16 or 32 lanes");
+  constexpr int G = 64 / KP;  // queries per wave
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int g = lane & (KP - 1), grp = lane / KP, g0 = lane - g;
+  if (a.ctrl->nonfinite) return;
+  const CertConst cc = cert_const(a);
+  const int d = a.d, k = a.k, nch = d >> 2;
+  const int64_t step = (int64_t)gridDim.x * W * G;
+  // A group past the block's rows repeats the wave's first query and writes
+  // nothing.
+  auto row_of = [&](int64_t qb) { return qb + grp < q_rows ? qb + grp : qb; };
+  // Lists of the row's splits (or of the pieces of a tail-split row).
+  auto lists_of = [&](int64_t ql, int& nlists) -> const uint64_t* {
+    const bool tl = ql >= a.tail_q0;
+    nlists = tl ? a.tail_parts : a.splits;
+    return tl ? a.ptail + (ql - a.tail_q0) * a.tail_parts * KP : a.partial + ql * a.splits * KP;
+  };
+  // A trip's first loads (its list entry, input row, squared norm and radius)
+  // are issued one trip ahead; its outputs are written one trip late, after
+  // the next trip's loads.  Stores count against the same in-order wait
+  // counter as loads, so a store ahead of a load would be waited for with it.
+  struct Ahead {
+    uint64_t v;
+    int64_t qi;
+    double ni, rho;
+  };
+  auto fetch = [&](int64_t qb) __attribute__((always_inline)) {
+    const int64_t ql = row_of(qb), qpos = q_begin + ql;
+    int nl;
+    Ahead x;
+    x.v = lists_of(ql, nl)[g];
+    x.qi = a.perm ? (int64_t)a.perm[qpos] : qpos;
+    x.ni = a.n64_q[qpos];
+    x.rho = a.rho_q[qpos];
+    return x;
+  };
+  bool plive = false, pok = false;
+  int64_t pqi = 0;
+  uint32_t pj = 0;
+  uint64_t pdb = 0;
+  double ptau = 0.0;
+  auto put = [&]() __attribute__((always_inline)) {
+    if (!plive) return;
+    if (pok) {
+      if (g < k) emit(a, pqi, g, pj, __longlong_as_double((long long)pdb));
+    } else if (g == 0) {
+      const uint32_t w = atomicAdd(&a.ctrl->worklist_count, 1u);
+      a.worklist[w] = (int32_t)pqi;
+      a.fbtau[w] = ptau;
+    }
+  };
+  int64_t qb = ((int64_t)blockIdx.x * W + wave) * G;
+  Ahead cur = {kEmpty, 0, 0.0, 0.0};
+  if (qb < q_rows) cur = fetch(qb);
+  for (; qb < q_rows; qb += step) {
+    Ahead nxt = cur;
+    if (qb + step < q_rows) nxt = fetch(qb + step);
+    const bool live = qb + grp < q_rows;
+    const int64_t qi = cur.qi;
+    // Final aggregation of the per-split (or per-piece) lists: lane g holds
+    // entry g of the running list; the next list is read reversed, so that
+    // the elementwise minimum holds the K' smallest of both as a bitonic
+    // sequence, which a bitonic merge sorts.  Groups with fewer lists than
+    // the wave's most merge empty ones.
+    int nlists;
+    const uint64_t* src = lists_of(row_of(qb), nlists);
+    uint64_t v = cur.v;
+    int nlw = nlists;
+#pragma unroll
+    for (int off = KP; off < 64; off <<= 1) nlw = max(nlw, __shfl_xor(nlw, off, 64));
+    for (int s = 1; s < nlw; ++s) {
+      v = umin64(v, s < nlists ? src[(int64_t)s * KP + (KP - 1 - g)] : kEmpty);
+#pragma unroll
+      for (int st = KP / 2; st > 0; st >>= 1) {
+        const uint64_t o = lane_xor64(v, st);
+        v = (g & st) ? umax64(v, o) : umin64(v, o);
+      }
+    }
+    // Every reference outside the list has a key >= the K'-th key.
+    const uint64_t hent = shfl64(v, g0 + KP - 1);
+    // With the grouped scan order the list holds positions: map to rows.
+    // (An empty slot measures row 0 and is then set to +inf: the loads stay
+    // outside divergent code, and the chunk tests on nch are uniform.)
+    const bool empty = v == kEmpty;
+    uint32_t j = empty ? 0u : index_of(v);
+    if (a.perm) j = (uint32_t)a.perm[j];
+    const float4* q4 = reinterpret_cast<const float4*>(a.xq + qi * d);
+    const float4* r4 = reinterpret_cast<const float4*>(a.xr + (int64_t)j * d);
+    float4 qv[DC], rv[DC];
+#pragma unroll
+    for (int c = 0; c < DC; ++c)
+      if (c < nch) {
+        qv[c] = q4[c];
+        rv[c] = r4[c];
+      }
+    put();  // the previous trip's outputs
+    double sum = 0.0;
+#pragma unroll
+    for (int c = 0; c < DC; ++c)
+      if (c < nch) sum = add_sq4(sum, qv[c], rv[c]);
+    const double d2 = empty ? (double)INFINITY : sum;
+    if (empty) j = index_of(kEmpty);
+    // Non-negative doubles order as their bit patterns.
+    uint64_t db = (uint64_t)__double_as_longlong(d2);
+    if (!a.no_recheck) {
+#pragma unroll
+      for (int size = 2; size <= KP; size <<= 1)
+#pragma unroll
+        for (int st = size >> 1; st > 0; st >>= 1) {
+          const uint64_t pd = lane_xor64(db, st);
+          const uint32_t pjx = lane_xor(j, st);
+          const bool keep_small = ((g & size) == 0) == ((g & st) == 0);
+          const bool mine_less = db < pd || (db == pd && j < pjx);
+          if (keep_small != mine_less) {
+            db = pd;
+            j = pjx;
+          }
+        }
+    }
+    // (no_recheck, a debugging switch, keeps the filter's order.)
+    const double tau2 = __longlong_as_double((long long)shfl64(db, g0 + k - 1));
+    bool ok = a.no_recheck ? true : certified(cc, cur.ni, cur.rho, hent, tau2);
+    if (a.force_fallback && !a.no_recheck) ok = false;
+    plive = live;
+    pok = ok;
+    pqi = qi;
+    pj = j;
+    pdb = db;
+    ptau = tau2;
+    cur = nxt;
+  }
+  put();
 }
 
 // ---------------------------------------------------------------------------
@@ -543,6 +710,19 @@ __global__ void __launch_bounds__(64) fallback_merge_kernel(Args a) {
 template <int KP>
 hipError_t launch_recheck_t(const Args& a, int64_t q_begin, int64_t q_rows, hipStream_t st) {
   constexpr int W = 4;
+  if constexpr (KP <= 32) {
+    if (a.d <= 64 && (a.d & 3) == 0) {
+      constexpr int G = 64 / KP;
+      int64_t g = (q_rows + W * G - 1) / (W * G);
+      if (g > 4096) g = 4096;
+      const auto kern = a.d <= 8    ? recheck_lanes_kernel<KP, W, 2>
+                        : a.d <= 16 ? recheck_lanes_kernel<KP, W, 4>
+                        : a.d <= 32 ? recheck_lanes_kernel<KP, W, 8>
+                                    : recheck_lanes_kernel<KP, W, 16>;
+      hipLaunchKernelGGL(kern, dim3((unsigned)g), dim3(W * 64), 0, st, a, q_begin, q_rows);
+      return hipGetLastError();
+    }
+  }
   int64_t g = (q_rows + W - 1) / W;
   if (g > 4096) g = 4096;
   hipLaunchKernelGGL((recheck_kernel<KP, W>), dim3((unsigned)g), dim3(W * 64), 0, st, a, q_begin,

@@ -88,7 +88,11 @@ struct Layout {
   int32_t colpart_blocks;
 };
 
-// Control block at the start of the workspace (device side).
+constexpr int kUncParts = 32, kUncStride = 16;
+
+// Control block at the start of the workspace (device side).  (Certified rows
+// are not counted here: every query row is either certified or on the
+// worklist.)
 struct Ctrl {
   uint32_t nonfinite;       // set to 1 if any input value is NaN/Inf
   uint32_t maxabs_bits;     // max |x - mu| over both sets, fp32 bits (non-negative)
@@ -96,12 +100,14 @@ struct Ctrl {
   uint64_t pmax_bits;       // max rho_j over references, fp64 bits
   uint32_t worklist_count;  // rows appended for exact recomputation
   uint32_t internal;        // set when a kernel finds an inconsistency it cannot recover from
-  uint64_t certified;       // rows certified by the shortlist test
   uint64_t fold_max_bits;   // max over references of the folded seed's error, fp64 bits
-  uint64_t uncertain;       // NWR: candidate pairs recomputed exactly
   uint32_t bad_label;       // classifier: a reference label outside [0, n_classes)
   uint32_t pad0;
-  uint64_t pad1;
+  // NWR: candidate pairs recomputed exactly, as kUncParts partial counts
+  // 128 bytes apart (the total is their sum).  Atomics on one address from
+  // every wave serialise: at 3 x 10^4 rows they took as long as the rest of
+  // the verification.
+  uint64_t uncertain[kUncParts * kUncStride];
 };
 
 // Everything a kernel needs to know about the problem.
