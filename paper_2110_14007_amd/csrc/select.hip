@@ -508,8 +508,7 @@ recheck_lanes_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 // k smallest of them per row.
 // ---------------------------------------------------------------------------
 constexpr int kFbThreads = 256;
-constexpr int kFbTop = 256;    // sorted best list occupies [0, kFbTop)
-constexpr int kFbSize = 1024;  // candidates are appended in [kFbTop, kFbSize)
+constexpr int kFbSize = 1024;  // sorted best k in [0, k), candidates appended after them
 constexpr int kFbSlab = 32;    // columns of the reference rows staged per pass
 
 __device__ __forceinline__ bool lex_less(uint64_t d1, uint32_t j1, uint64_t d2, uint32_t j2) {
@@ -522,10 +521,11 @@ __device__ __forceinline__ int fb_chunks(uint32_t count) {
   return p < 1 ? 1 : (p > (uint32_t)kFbMaxChunks ? kFbMaxChunks : (int)p);
 }
 
-__device__ void fb_sort(uint64_t* kd, uint32_t* kj) {
-  for (int size = 2; size <= kFbSize; size <<= 1) {
+// Sort the first n entries (n a power of two, at most kFbSize).
+__device__ void fb_sort(uint64_t* kd, uint32_t* kj, int n) {
+  for (int size = 2; size <= n; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = threadIdx.x; i < kFbSize / 2; i += kFbThreads) {
+      for (int i = threadIdx.x; i < n / 2; i += kFbThreads) {
         const int lo = 2 * stride * (i / stride) + (i % stride);
         const int hi = lo + stride;
         const bool asc = (lo & size) == 0;
@@ -624,14 +624,19 @@ __global__ void __launch_bounds__(kFbThreads) fallback_scan_kernel(Args a) {
         const uint64_t db = (uint64_t)__double_as_longlong(d2);
         if (lex_less(db, (uint32_t)j, thr_d, thr_j)) {
           const int slot = atomicAdd(&bufcnt, 1);
-          kd[kFbTop + slot] = db;
-          kj[kFbTop + slot] = (uint32_t)j;
+          kd[k + slot] = db;
+          kj[k + slot] = (uint32_t)j;
         }
       }
       __syncthreads();
       const bool last = base + kFbThreads >= j1;
-      if (bufcnt > kFbSize - kFbTop - kFbThreads || (last && bufcnt > 0)) {
-        fb_sort(kd, kj);
+      // Merge when another pass could overflow the buffer, and at the end;
+      // only the first next_pow2(k + appended) entries are sorted (the rest
+      // are empty).
+      if (bufcnt > kFbSize - k - kFbThreads || (last && bufcnt > 0)) {
+        int n = 2;
+        while (n < k + bufcnt) n <<= 1;
+        fb_sort(kd, kj, n);
         for (int i = k + tid; i < kFbSize; i += kFbThreads) {
           kd[i] = kEmpty;
           kj[i] = 0xffffffffu;
