@@ -60,27 +60,36 @@ count_kernel(const int32_t* __restrict__ lab, int64_t n, int32_t* __restrict__ b
   if (threadIdx.x < kOrdC) bcnt[(int64_t)blockIdx.x * kOrdC + threadIdx.x] = cnt[threadIdx.x];
 }
 
-// Group starts and, per block, the first position of each of its groups.
-__global__ void scan_kernel(const int32_t* __restrict__ bcnt, int nb, int32_t* __restrict__ boff,
-                            int32_t* __restrict__ cstart) {
+// Group starts and each block's first position in its group: one wave per
+// group sums the group's counts over the blocks, then (every total known)
+// forms the blocks' exclusive prefix sums 64 blocks at a time.
+__global__ void __launch_bounds__(kOrdC * 64)
+scan_kernel(const int32_t* __restrict__ bcnt, int nb, int32_t* __restrict__ boff,
+            int32_t* __restrict__ cstart) {
   __shared__ int32_t tot[kOrdC];
-  const int c = threadIdx.x;
-  if (c < kOrdC) {
-    int32_t t = 0;
-    for (int b = 0; b < nb; ++b) t += bcnt[(int64_t)b * kOrdC + c];
-    tot[c] = t;
-  }
+  const int c = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int32_t t = 0;
+  for (int b = lane; b < nb; b += 64) t += bcnt[(int64_t)b * kOrdC + c];
+  for (int off = 32; off > 0; off >>= 1) t += __shfl_xor(t, off, 64);
+  if (lane == 0) tot[c] = t;
   __syncthreads();
-  if (c < kOrdC) {
-    int32_t start = 0;
-    for (int i = 0; i < c; ++i) start += tot[i];
+  int32_t start = 0;
+  for (int i = 0; i < c; ++i) start += tot[i];
+  if (lane == 0) {
     cstart[c] = start;
     if (c == kOrdC - 1) cstart[kOrdC] = start + tot[c];
-    int32_t at = start;
-    for (int b = 0; b < nb; ++b) {
-      boff[(int64_t)b * kOrdC + c] = at;
-      at += bcnt[(int64_t)b * kOrdC + c];
+  }
+  int32_t at = start;
+  for (int b0 = 0; b0 < nb; b0 += 64) {
+    const int b = b0 + lane;
+    const int32_t v = b < nb ? bcnt[(int64_t)b * kOrdC + c] : 0;
+    int32_t incl = v;  // inclusive prefix sum over the wave
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t o = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += o;
     }
+    if (b < nb) boff[(int64_t)b * kOrdC + c] = at + incl - v;
+    at += __shfl(incl, 63, 64);
   }
 }
 
@@ -119,7 +128,7 @@ hipError_t launch_order(const Plan& p, const Args& a, hipStream_t st) {
   hipLaunchKernelGGL(assign_kernel, dim3((unsigned)((n + kAssignThreads - 1) / kAssignThreads)),
                      dim3(kAssignThreads), lds, st, a.xr, n, (int)p.d, a.lab);
   hipLaunchKernelGGL(count_kernel, dim3((unsigned)nb), dim3(256), 0, st, a.lab, n, a.bcnt);
-  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(64), 0, st, a.bcnt, nb, a.boff, a.cstart);
+  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kOrdC * 64), 0, st, a.bcnt, nb, a.boff, a.cstart);
   hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)nb), dim3(64), 0, st, a.lab, n, a.boff,
                      a.perm);
   return hipGetLastError();

@@ -171,9 +171,13 @@ __device__ __forceinline__ void atomic_max_nonneg(uint64_t* addr, double v) {
   atomicMax((unsigned long long*)addr, (unsigned long long)__double_as_longlong(v));
 }
 
-// One thread per row.  Rows in [n, n_pad) are zero-filled so that the tile
-// kernels may read whole 32-row tiles.  The reference maxima are reduced over
-// the wave first: one atomic per wave instead of two per row.
+// One thread per row, rows walked with a grid stride.  Rows in [n, n_pad)
+// are zero-filled so that the tile kernels may read whole 32-row tiles.  The
+// reference maxima are kept per thread and reduced over the workgroup at the
+// end: one atomic per maximum per workgroup, and at most 1024 workgroups
+// (same-address atomics serialise: one per 256 rows cost about half of this
+// kernel's time at 4 x 10^6 rows).  Rows of 8-element chunks are written 16
+// bytes at a time.
 //
 // Fold layout (fold != 0): columns [0, d) hold xhat, [d, dmain) zeros,
 // [dmain, dmain + 4) the seed parts p_1..p_4 in the filter precision and the
@@ -188,56 +192,72 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
                 float* __restrict__ hn, double* __restrict__ n64, double* __restrict__ rho,
                 int is_ref, int fold, int dmain, int scale_exp, double cfold,
                 const int32_t* __restrict__ perm) {
-  const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  double nsq = 0.0, rho_up = 0.0, ferr = 0.0;
-  if (row < n_pad) {
+  const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
+  const bool vec = (dpad & 7) == 0 && sizeof(T) * 8 % 16 == 0;
+  double mn = 0.0, mp = 0.0, mf = 0.0;  // this thread's maxima
+  for (int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; row < n_pad;
+       row += (int64_t)gridDim.x * blockDim.x) {
     T* out = xq + row * dpad;
     if (row >= n) {
       for (int t = 0; t < dpad; ++t) out[t] = (T)0.0f;
       if (hn) hn[row] = 0.0f;
       if (n64) n64[row] = 0.0;
       if (rho) rho[row] = 0.0;
-    } else {
-      const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
-      const float* in = x + (perm ? (int64_t)perm[row] : row) * d;
-      double r2 = 0.0, c2 = 0.0;
-      for (int t = 0; t < d; ++t) {
+      continue;
+    }
+    const float* in = x + (perm ? (int64_t)perm[row] : row) * d;
+    double nsq = 0.0, r2 = 0.0, c2 = 0.0, ferr = 0.0;
+    // Element t of the padded row (the sums advance in column order).
+    double v = 0.0, fsum = 0.0;
+    auto elem = [&](int t) -> T {
+      if (t < d) {
         const double c = s * ((double)in[t] - (double)mu32[t]);
         const T q = quantise<T>(c);
         const double qd = (double)(float)q;
-        out[t] = q;
         nsq += qd * qd;
         r2 += (c - qd) * (c - qd);
         c2 += c * c;
+        return q;
       }
-      if (fold) {
-        for (int t = d; t < dmain; ++t) out[t] = (T)0.0f;
-        double v = -0.5 * nsq / cfold;
-        double sum = 0.0;
-        for (int t = 0; t < 4; ++t) {
-          const T q = (T)(float)v;
-          const double qd = (double)(float)q;
-          out[dmain + t] = q;
-          sum += qd;  // parts of decreasing magnitude: the sum stays exact
-          v -= qd;    // exact: qd is v rounded to fewer bits
-        }
-        for (int t = dmain + 4; t < dpad; ++t) out[t] = (T)0.0f;
-        const double e = fabs(cfold * sum + 0.5 * nsq);
-        ferr = e * (1.0 + 0x1p-40) + 0x1p-60 * nsq;
-      } else {
-        for (int t = d; t < dpad; ++t) out[t] = (T)0.0f;
+      if (fold && t >= dmain && t < dmain + 4) {
+        if (t == dmain) v = -0.5 * nsq / cfold;
+        const T q = (T)(float)v;
+        const double qd = (double)(float)q;
+        fsum += qd;  // parts of decreasing magnitude: the sum stays exact
+        v -= qd;     // exact: qd is v rounded to fewer bits
+        return q;
       }
-      // Round the radius up: covers the fp64 rounding of c and of the sums.
-      rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
-      if (is_ref) hn[row] = -0.5f * (float)nsq;
-      if (n64) n64[row] = nsq;
-      if (rho) rho[row] = rho_up;
+      return (T)0.0f;
+    };
+    if (vec) {
+      for (int t0 = 0; t0 < dpad; t0 += 8) {
+        T buf[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) buf[e] = elem(t0 + e);
+#pragma unroll
+        for (int h = 0; h < (int)(sizeof(T) * 8 / 16); ++h)
+          reinterpret_cast<uint4*>(out + t0)[h] = reinterpret_cast<const uint4*>(buf)[h];
+      }
+    } else {
+      for (int t = 0; t < dpad; ++t) out[t] = elem(t);
     }
+    if (fold) {
+      const double e = fabs(cfold * fsum + 0.5 * nsq);
+      ferr = e * (1.0 + 0x1p-40) + 0x1p-60 * nsq;
+    }
+    // Round the radius up: covers the fp64 rounding of c and of the sums.
+    const double rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
+    if (is_ref) hn[row] = -0.5f * (float)nsq;
+    if (n64) n64[row] = nsq;
+    if (rho) rho[row] = rho_up;
+    mn = nsq > mn ? nsq : mn;
+    mp = rho_up > mp ? rho_up : mp;
+    mf = ferr > mf ? ferr : mf;
   }
   if (is_ref) {  // uniform: one atomic per maximum per workgroup
     __shared__ double red[kThreads / 64];
-    const double bn = block_max(nsq, red), bp = block_max(rho_up, red);
-    const double bf = block_max(ferr, red);
+    const double bn = block_max(mn, red), bp = block_max(mp, red);
+    const double bf = block_max(mf, red);
     if (threadIdx.x == 0) {
       atomic_max_nonneg(&ctrl->nmax_bits, bn);
       atomic_max_nonneg(&ctrl->pmax_bits, bp);
@@ -344,15 +364,19 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
     return hipGetLastError();
   }
   const double cf = fold_const(p.precision);
-  const int64_t blocks_r = (p.nr_pad + kThreads - 1) / kThreads;
-  hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_r), dim3(kThreads), 0, st, a.xr,
+  const auto grid_threads = [](int64_t rows) {
+    const int64_t g = (rows + kThreads - 1) / kThreads;
+    return (unsigned)(g < 1 ? 1 : (g > 1024 ? 1024 : g));
+  };
+  const unsigned blocks_r = grid_threads(p.nr_pad);
+  hipLaunchKernelGGL(quantise_kernel<T>, dim3(blocks_r), dim3(kThreads), 0, st, a.xr,
                      p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r, a.hn_r,
                      p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : a.rho_r, 1,
                      p.fold, p.dmain, p.scale_exp, cf, a.perm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.self) return e;
-  const int64_t blocks_q = (p.nq_pad + kThreads - 1) / kThreads;
-  hipLaunchKernelGGL(quantise_kernel<T>, dim3((unsigned)blocks_q), dim3(kThreads), 0, st, a.xq,
+  const unsigned blocks_q = grid_threads(p.nq_pad);
+  hipLaunchKernelGGL(quantise_kernel<T>, dim3(blocks_q), dim3(kThreads), 0, st, a.xq,
                      p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q, (float*)nullptr,
                      a.n64_q, a.rho_q, 0, p.fold, p.dmain, p.scale_exp, cf,
                      (const int32_t*)nullptr);
