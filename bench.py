@@ -443,6 +443,8 @@ def bench_knn(w, x_host, steps, warmup, precision, detector, score="kth"):
     launches = stats[0]["tile_launches"]
     pairs = float(n) * float(n)
     bind, views = tile_rooflines(prec, d, pairs, launches, avg("ms_tile"))
+    recheck = recheck_roofline(n, d, k, stats[0]["kprime"], stats[0]["ref_splits"],
+                               avg("ms_recheck"))
     return {
         "n": n, "d": d, "k": k, "detector": detector, "score": score, "prec": prec,
         "ms_step": ms_step, "value": n / (ms_step * 1e-3), "pairs_s": pairs / (ms_step * 1e-3),
@@ -452,7 +454,25 @@ def bench_knn(w, x_host, steps, warmup, precision, detector, score="kth"):
         "query_block": stats[0]["query_block"], "blocks": stats[0]["blocks"],
         "launches": launches, "launch_ms": avg("ms_tile") / launches,
         "rows_fallback": stats[0]["rows_fallback"], "bind": bind, "views": views,
+        "recheck": recheck,
     }
+
+
+def recheck_roofline(n, d, k, kprime, splits, ms):
+    """The recheck against the HBM peak on its algorithmic bytes per row: the
+    S lists (8 B per entry), the measured candidates' fp32 rows and the query's
+    own, its squared norm and radius, and k neighbours written (index and
+    distance, 12 B each) plus the k-th distance.  Lists of up to 32 entries
+    over rows of up to 64 elements (a multiple of 4) measure all K'
+    candidates; otherwise the first pass measures k + 8."""
+    lanes = kprime <= 32 and d <= 64 and d % 4 == 0
+    measured = kprime if lanes else min(k + 8, kprime)
+    per_row = splits * kprime * 8 + (measured + 1) * 4 * d + 16 + k * 12 + 8
+    gbs = n * per_row / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+    return {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBS, 4), "bytes_per_row": per_row,
+            "kernel": ("recheck_lanes<K'=%d>" if lanes else "recheck<K'=%d>") % kprime,
+            "ms": round(ms, 4)}
 
 
 def knn_roofline(wname, m):
@@ -502,6 +522,7 @@ def knn_line(args, w):
         "phase_ms": m["phase_ms"],
         "rows_fallback": m["rows_fallback"],
         "roofline": knn_roofline(w.name, m),
+        "recheck_roofline": m["recheck"],
     }
     return line, x_host
 
@@ -520,7 +541,8 @@ def sub_result(args, w, precision=None, label=None):
          "ms_per_step": round(m["ms_step"], 4), "points_per_s": round(m["value"], 1),
          "pairs_per_s": m["pairs_s"], "tile_ms": round(m["phase_ms"]["ms_tile"], 4),
          "phase_ms": m["phase_ms"], "rows_fallback": m["rows_fallback"],
-         "roofline": knn_roofline(w.name, m), "steps": args.sub_steps}
+         "roofline": knn_roofline(w.name, m), "recheck_roofline": m["recheck"],
+         "steps": args.sub_steps}
     if not args.no_cpu_baseline:
         if w.name == "C1":
             r["oracle"] = cpu_baseline(x_host, w.k, None, lof_full=True)
