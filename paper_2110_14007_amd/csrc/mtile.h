@@ -501,12 +501,21 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       }
     }
   };
-  auto max16 = [](const f32x16& v) {
+  // Maximum of the 16 accumulators as two partial maxima (7 max3 each): a
+  // group of sub-tiles then combines 2 NG values, which costs fewer
+  // instructions than combining NG finished maxima.
+  struct Max2 {
+    float f, g;
+  };
+  auto max16p = [](const f32x16& v) {
     const float a = max3f(v[0], v[1], v[2]), b = max3f(v[3], v[4], v[5]);
     const float c = max3f(v[6], v[7], v[8]), d = max3f(v[9], v[10], v[11]);
     const float e = max3f(v[12], v[13], v[14]);
-    const float f = max3f(a, b, c), g = max3f(d, e, v[15]);
-    return max3f(f, g, g);
+    return Max2{max3f(a, b, c), max3f(d, e, v[15])};
+  };
+  auto max16 = [&](const f32x16& v) {
+    const Max2 p = max16p(v);
+    return max3f(p.f, p.g, p.g);
   };
   // Merge the first kMerge queue entries of every lane into the lists, move
   // the rest (at most kQCap - kMerge) to the front and tighten the threshold.
@@ -709,11 +718,17 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
           for (int u = 0; u < NQ; ++u)
             mask(acc[s][u], t0u + 32u * (uint32_t)(g0 + s), q0u + 32u * (uint32_t)u);
       }
+      // (Sub-tiles past the split are fully masked.)
+      Max2 mp[NG][NQ];
+#pragma unroll
+      for (int s = 0; s < NG; ++s)
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) mp[s][u] = max16p(acc[s][u]);
       float ms[NG][NQ];
 #pragma unroll
       for (int s = 0; s < NG; ++s)
 #pragma unroll
-        for (int u = 0; u < NQ; ++u) ms[s][u] = max16(acc[s][u]);  // past the split: fully masked
+        for (int u = 0; u < NQ; ++u) ms[s][u] = max3f(mp[s][u].f, mp[s][u].g, mp[s][u].g);
       if constexpr (NQ > 1) {
         // One sub-tile, NQ query groups: insert each group's survivors from
         // its accumulators.
@@ -729,9 +744,17 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         if (__ballot(ms[0][1] > thr[1])) insert(One, acc[0][1], ts);
         return;
       }
-      float m = ms[0][0];
+      // Group maximum from the 2 NG partial maxima (the per-sub-tile maxima
+      // above are formed only where the slow path reads them).
+      float pv[2 * NG];
 #pragma unroll
-      for (int s = 1; s < NG; s += 2) m = max3f(m, ms[s][0], ms[s + 1 < NG ? s + 1 : s][0]);
+      for (int s = 0; s < NG; ++s) {
+        pv[2 * s] = mp[s][0].f;
+        pv[2 * s + 1] = mp[s][0].g;
+      }
+      float m = pv[0];
+#pragma unroll
+      for (int i = 1; i < 2 * NG; i += 2) m = max3f(m, pv[i], pv[i + 1 < 2 * NG ? i + 1 : i]);
       if (!__ballot(m > thr[0])) return;
       // Slow path: sub-tile by sub-tile.  Rows of several k-steps reuse the
       // group's accumulators, one copy of the insertion code per sub-tile (a
