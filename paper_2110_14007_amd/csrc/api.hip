@@ -191,6 +191,19 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
       p->dpad = p->dpad_t = 16;
       // fp16: |seed part| <= 8 2^(2E) / 2 / 2^15 must stay below 2^15.
       if (prec == TOD_PREC_FP16) p->scale_exp = 14;
+    } else {
+      // Longer rows: the seed -N_j/2 is the product of four parts of
+      // -N_j/(2c) (staged beside the rows, 8 bytes a row) with c, one MFMA
+      // per sub-tile, instead of 16 fp32 seeds read from LDS by every lane.
+      // fp16 parts: N_j / 2^16 <= d 2^(2E - 16) must stay below 2^15, i.e.
+      // d 2^(2E) <= 2^31.
+      p->seedprod = 1;
+      if (prec == TOD_PREC_FP16) {
+        int lg = 0;
+        while ((int64_t)1 << lg < d) ++lg;
+        const int e = (31 - lg) / 2;
+        p->scale_exp = e < 14 ? e : 14;
+      }
     }
   }
   // Grouped scan order: X against X through the register-list kernel with one
@@ -228,7 +241,7 @@ Layout make_layout(const Plan& p) {
   L.colpart = take(sizeof(double) * p.d * L.colpart_blocks);
   L.xq_r = take((size_t)p.nr_pad * p.dpad * p.esize);
   L.xq_q = p.self ? L.xq_r : take((size_t)p.nq_pad * p.dpad * p.esize);
-  L.hn_r = take(sizeof(float) * p.nr_pad);
+  L.hn_r = take((p.seedprod ? 8 : sizeof(float)) * p.nr_pad);
   L.n64_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
   L.rho_q = take(sizeof(double) * (p.self ? p.nr_pad : p.nq_pad));
   L.partial = take(sizeof(uint64_t) * p.query_block * p.splits * p.kprime);
@@ -482,6 +495,7 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.margin_scale = o.margin_scale;
   a.force_fallback = o.force_fallback ? 1 : 0;
   a.fold = p.fold;
+  a.seedprod = p.seedprod;
   a.dmain = p.dmain;
   a.scale_exp = p.scale_exp;
   a.no_recheck = o.no_recheck ? 1 : 0;

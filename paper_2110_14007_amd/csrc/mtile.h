@@ -271,14 +271,18 @@ __device__ __forceinline__ void merge_queues(uint64_t (&L)[R], const uint2* myq,
   clean_asc<R>(L);
 }
 
-// Row layouts.  Plain (FOLD = false): the row padded to DPAD (16, 32, 64 or
-// 128) and the accumulator seed -N_j/2 staged in LDS beside the rows.  Fold
-// (FOLD = true, rows of at most 8 elements, DPAD = 16): the seed is stored as
-// parts p_1..p_4 of -N_j/(2c) in columns 8..11 and the queries carry the
-// constant c there instead (built in registers), so that
-//     acc = sum_t xhat_it xhat_jt + c sum_p p_p = <xhat_i, xhat_j> - N_j/2
-// comes out of the single 16-wide MFMA step, which would otherwise multiply
-// zero padding.
+// Row layouts.  The accumulator seed -N_j/2 is formed by the MFMA from parts
+// p_1..p_4 of -N_j/(2c) in the filter precision against the constant c:
+//     acc = sum_t xhat_it xhat_jt + c sum_p p_p = <xhat_i, xhat_j> - N_j/2.
+// Plain (FOLD = false): the row padded to DPAD (16 ... 512); the parts (8
+// bytes a row) are staged in LDS beside the rows, and a sub-tile starts with
+// one seed MFMA: A row j = (p_1..p_4, 0 ...), B = c in its first four k rows.
+// That replaces 16 fp32 seeds per lane (four 16-byte LDS reads by every
+// lane, most of the LDS traffic at rows of 32 elements) with one 8-byte read
+// and one MFMA.  Fold (FOLD = true, rows of at most 8 elements, DPAD = 16):
+// the parts sit in columns 8..11 of the row and the queries carry c there,
+// so the single 16-wide MFMA step, which would otherwise multiply zero
+// padding, forms the seed too.
 template <int DPAD, bool FOLD>
 struct Layout {
   static constexpr int k16 = DPAD / 16;  // 16-wide k-steps
@@ -328,7 +332,7 @@ constexpr int queue_slots() { return NQ == 1 ? queue_cap<R>() : 16; }
 __host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int ns, int qcap,
                                                int nq) {
   return (size_t)stage_buffers(dpad, fold, nq) * 32 * ns * (dpad == 16 ? 32 : dpad * 2 + 16) +
-         (fold ? 0 : (size_t)stage_buffers(dpad, fold, nq) * 32 * ns * sizeof(float)) +
+         (fold ? 0 : (size_t)stage_buffers(dpad, fold, nq) * 32 * ns * sizeof(uint2)) +
          (size_t)w * nq * qcap * 64 * sizeof(uint2);
 }
 
@@ -369,8 +373,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   constexpr int NBUF = stage_buffers(DPAD, FOLD, NQ);
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* stage = smem;
-  float* hnb = (float*)(smem + NBUF * STAGE);  // plain layout: seeds of the staged rows
-  uint2* qbase = (uint2*)(smem + NBUF * STAGE + (FOLD ? 0 : NBUF * TR * sizeof(float)));
+  uint2* hnb = (uint2*)(smem + NBUF * STAGE);  // plain layout: seed parts of the staged rows
+  uint2* qbase = (uint2*)(smem + NBUF * STAGE + (FOLD ? 0 : NBUF * TR * sizeof(uint2)));
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, col = lane & 31;
@@ -453,8 +457,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   for (int i = 0; i < (DL ? 1 : NL); ++i) st[i] = make_uint4(0, 0, 0, 0);
 #pragma unroll
   for (int i = 0; i < (PF2 ? NL : 1); ++i) su[i] = make_uint4(0, 0, 0, 0);
-  static_assert(TR / 4 <= NT, "one float4 of seeds per thread");
-  float4 sth = make_float4(0.f, 0.f, 0.f, 0.f), suh = sth;
+  static_assert(TR / 2 <= NT, "the seed parts of two rows per thread");
+  uint4 sth = make_uint4(0, 0, 0, 0), suh = sth;
 
   // A fragment of sub-tile s, 16-wide k-step c: row col, elements 16c + 8h..+7.
   // 32-byte rows store the two halves of row r swapped where bits 2 and 3 of
@@ -464,22 +468,26 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   auto afrag = [&](const unsigned char* buf, int s, int c) {
     return *reinterpret_cast<const V*>(buf + (32 * s + col) * ROWB + 32 * c + ahalf);
   };
-  // Accumulator seeds of sub-tile s: -N_j/2 of rows 8g + 4h + 0..3 (plain
-  // layout); zero in the fold layout, where the MFMA adds them.
-  auto seed = [&](const float* hn, int s) {
+  // Seed MFMA operand B (plain layout): c in k rows 0..3, which lanes of
+  // half 0 hold; zero elsewhere.
+  V bseed;
+  {
+    const ET cf = (ET)(float)fold_const(std::is_same<ET, _Float16>::value ? TOD_PREC_FP16
+                                                                         : TOD_PREC_BF16);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bseed[e] = (h == 0 && e < 4) ? cf : (ET)0.0f;
+  }
+  // Accumulator seeds of sub-tile s: -N_j/2 of rows 8g + 4h + 0..3.  Plain
+  // layout: the seed MFMA on row col's parts (lanes of half 1 read them too;
+  // their B is zero); zero in the fold layout, where the data MFMA adds them.
+  auto seed = [&](const uint2* hn, int s) {
     f32x16 v;
-    if constexpr (FOLD) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) v[r] = 0.0f;
-    } else {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float4 t = *reinterpret_cast<const float4*>(hn + 32 * s + 8 * g + 4 * h);
-        v[4 * g + 0] = t.x;
-        v[4 * g + 1] = t.y;
-        v[4 * g + 2] = t.z;
-        v[4 * g + 3] = t.w;
-      }
+    for (int r = 0; r < 16; ++r) v[r] = 0.0f;
+    if constexpr (!FOLD) {
+      const uint2 raw = hn[32 * s + col];
+      const V ps = __builtin_bit_cast(V, make_uint4(raw.x, raw.y, 0u, 0u));
+      v = mfma<ET>(ps, bseed, v);
     }
     return v;
   };
@@ -590,9 +598,9 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       REG[i] = *reinterpret_cast<const uint4*>(xr_bytes + gr * (int64_t)(DPAD * 2) + cc * 16); \
     }                                                                                       \
   }                                                                                         \
-  if (!FOLD && tid < TR / 4) {                                                              \
-    const int64_t gr = (T0) + 4 * tid < r_end32 ? (T0) + 4 * tid : r_end32 - 4;             \
-    REGH = *reinterpret_cast<const float4*>(a.hn_r + gr);                                   \
+  if (!FOLD && tid < TR / 2) {                                                              \
+    const int64_t gr = (T0) + 2 * tid < r_end32 ? (T0) + 2 * tid : r_end32 - 2;             \
+    REGH = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint2*>(a.hn_r) + gr);     \
   }
 #define TOD_MT_PUT(B, REG, REGH)                                                             \
   _Pragma("unroll") for (int i = 0; i < NL; ++i) {                                          \
@@ -601,10 +609,11 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       *reinterpret_cast<uint4*>(stage + (B) * STAGE + (c / CPR) * ROWB +                      \
                                 ((c % CPR) ^ (SWZ ? swz(c / CPR) : 0)) * 16) = REG[i];      \
   }                                                                                         \
-  if (!FOLD && tid < TR / 4) *reinterpret_cast<float4*>(hnb + (B) * TR + 4 * tid) = REGH;
+  if (!FOLD && tid < TR / 2) *reinterpret_cast<uint4*>(hnb + (B) * TR + 2 * tid) = REGH;
 
   // Direct staging (rows of 512 elements): each wave moves 8 whole rows (one
-  // 1 KiB row per instruction) and 8 seeds of a stage straight into LDS.
+  // 1 KiB row per instruction) and the seed parts of 8 rows of a stage
+  // straight into LDS.
   // The rows a wave stages depend on the wave only, so their addresses are
   // formed in scalar registers (one wave index read through readfirstlane,
   // used by the staging alone); only the lane's 16-byte offset is a vector
@@ -620,9 +629,10 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
       const int r = wv + W * i;
       dma16(xr_bytes + (dl_t0 + r) * (int64_t)(DPAD * 2) + lane * 16,
             lbase + dl_b * STAGE + r * ROWB);
-    } else if (lane < 2) {
-      dma16((const unsigned char*)(a.hn_r + dl_t0 + 8 * wv) + lane * 16,
-            lbase + NBUF * STAGE + (dl_b * TR + 8 * wv) * (int)sizeof(float));
+    } else if (lane < 4) {  // the seed parts of 8 rows: 64 bytes
+      dma16((const unsigned char*)(reinterpret_cast<const uint2*>(a.hn_r) + dl_t0 + 8 * wv) +
+                lane * 16,
+            lbase + NBUF * STAGE + (dl_b * TR + 8 * wv) * (int)sizeof(uint2));
     }
   };
   constexpr int kDlRows = TR / W + 1;  // staging loads per wave and stage
@@ -633,7 +643,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   // wait for its own MFMAs.
   auto stage_body = [&](int64_t t0, int b) __attribute__((always_inline)) {
     const unsigned char* buf = stage + b * STAGE;
-    const float* hn = hnb + b * TR;
+    const uint2* hn = hnb + b * TR;
     if (!active) return;
     const uint32_t t0u = (uint32_t)t0;
     const uint32_t avail = endu - t0u;  // every scanned stage starts below r_end
@@ -661,10 +671,10 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         // read as fragment c enters the chain, and after every third k-step
         // one staging row is issued.
         static_assert(NG == 1, "one sub-tile per stage");
+        acc[0][0] = seed(hn, g0);  // its parts are read first
         V w[kAhead];
 #pragma unroll
         for (int c = 0; c < kAhead; ++c) w[c] = afrag(buf, g0, c);
-        acc[0][0] = seed(hn, g0);
 #pragma unroll
         for (int u = 1; u < NQ; ++u) acc[0][u] = acc[0][0];
 #pragma unroll
@@ -679,7 +689,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         // (Addresses from the group's first row: the sub-tile offsets are
         // then immediate offsets of the LDS reads.)
         const unsigned char* gbuf = buf + g0 * (32 * ROWB);
-        const float* ghn = hn + 32 * g0;
+        const uint2* ghn = hn + 32 * g0;
         V af[NG][KC];
 #pragma unroll
         for (int s = 0; s < NG; ++s) {
@@ -697,8 +707,11 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 #pragma unroll
             for (int u = 0; u < NQ; ++u) acc[s][u] = mfma<ET>(af[s][c], bq[u][c], acc[s][u]);
       }
+      // (Plain layout: one LDS read and one MFMA more per sub-tile, the seed's.)
+      constexpr int kSeed = FOLD ? 0 : 1;
       if constexpr (kInterleave) {
-        __builtin_amdgcn_sched_group_barrier(0x100, kAhead + (FOLD ? 0 : 4), 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, kAhead + kSeed, 0);
+        if constexpr (kSeed) __builtin_amdgcn_sched_group_barrier(0x008, kSeed, 0);
 #pragma unroll
         for (int c = 0; c < KC - kAhead; ++c) {
           __builtin_amdgcn_sched_group_barrier(0x008, NQ, 0);
@@ -706,8 +719,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         }
         __builtin_amdgcn_sched_group_barrier(0x008, NQ * kAhead, 0);
       } else {
-        __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + (FOLD ? 0 : 4)), 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, NG * NQ * KC, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, NG * (KC + kSeed), 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NG * (NQ * KC + kSeed), 0);
       }
       // Masks first (one branch per group), then the NG x NQ independent max
       // trees, which the scheduler interleaves.
@@ -841,7 +854,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     // ahead with two.  The compiler-visible wait first retires the query
     // operand's loads, so that the compiler, which does not see the staging
     // loads, has no load of its own left to wait for.
-    static_assert(TR == 8 * W && W == 4, "direct staging: 8 rows and 8 seeds per wave");
+    static_assert(TR == 8 * W && W == 4, "direct staging: 8 rows and their seed parts per wave");
     static_assert(KC >= 3 * (TR / W), "staging loads spread over the MFMA chain");
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     auto dl_issue = [&](int64_t t0, int b) __attribute__((always_inline)) {

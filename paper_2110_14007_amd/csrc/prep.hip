@@ -171,6 +171,25 @@ __device__ __forceinline__ void atomic_max_nonneg(uint64_t* addr, double v) {
   atomicMax((unsigned long long*)addr, (unsigned long long)__double_as_longlong(v));
 }
 
+// The seed -N/2 as four parts of v = -N/(2c) in the filter precision, split
+// greedily (p_1 = Q(v), p_2 = Q(v - p_1), ...; every residual is exact in
+// fp64, so the sum of the parts stays exact too); returns err >=
+// |c sum p + N/2|, rounded up.  The certificate adds the largest err over the
+// references.
+template <typename T>
+__device__ __forceinline__ double seed_parts(double nsq, double cfold, T (&q)[4]) {
+  double v = -0.5 * nsq / cfold, sum = 0.0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    q[t] = (T)(float)v;
+    const double qd = (double)(float)q[t];
+    sum += qd;
+    v -= qd;
+  }
+  const double e = fabs(cfold * sum + 0.5 * nsq);
+  return e * (1.0 + 0x1p-40) + 0x1p-60 * nsq;
+}
+
 // One thread per row, rows walked with a grid stride.  Rows in [n, n_pad)
 // are zero-filled so that the tile kernels may read whole 32-row tiles.  The
 // reference maxima are kept per thread and reduced over the workgroup at the
@@ -191,7 +210,7 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
                 const float* __restrict__ mu32, Ctrl* ctrl, T* __restrict__ xq,
                 float* __restrict__ hn, double* __restrict__ n64, double* __restrict__ rho,
                 int is_ref, int fold, int dmain, int scale_exp, double cfold,
-                const int32_t* __restrict__ perm) {
+                const int32_t* __restrict__ perm, int seedprod) {
   const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
   const bool vec = (dpad & 7) == 0 && sizeof(T) * 8 % 16 == 0;
   double mn = 0.0, mp = 0.0, mf = 0.0;  // this thread's maxima
@@ -200,7 +219,8 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
     T* out = xq + row * dpad;
     if (row >= n) {
       for (int t = 0; t < dpad; ++t) out[t] = (T)0.0f;
-      if (hn) hn[row] = 0.0f;
+      if (hn && seedprod) reinterpret_cast<uint2*>(hn)[row] = make_uint2(0u, 0u);
+      else if (hn) hn[row] = 0.0f;
       if (n64) n64[row] = 0.0;
       if (rho) rho[row] = 0.0;
       continue;
@@ -247,7 +267,13 @@ quantise_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int d, in
     }
     // Round the radius up: covers the fp64 rounding of c and of the sums.
     const double rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
-    if (is_ref) hn[row] = -0.5f * (float)nsq;
+    if (is_ref && seedprod) {
+      T q[4];
+      ferr = seed_parts<T>(nsq, cfold, q);
+      reinterpret_cast<uint2*>(hn)[row] = *reinterpret_cast<const uint2*>(q);
+    } else if (is_ref) {
+      hn[row] = -0.5f * (float)nsq;
+    }
     if (n64) n64[row] = nsq;
     if (rho) rho[row] = rho_up;
     mn = nsq > mn ? nsq : mn;
@@ -289,18 +315,20 @@ quantise_rows_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int 
                      const float* __restrict__ mu32, Ctrl* ctrl, T* __restrict__ xq,
                      float* __restrict__ hn, double* __restrict__ n64,
                      double* __restrict__ rho, int is_ref, int scale_exp,
-                     const int32_t* __restrict__ perm) {
+                     const int32_t* __restrict__ perm, int seedprod, double cfold) {
   const int lane = threadIdx.x & 63;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   const double s = scale_from_maxabs(ctrl->maxabs_bits, scale_exp);
   double wn = 0.0, wp = 0.0;  // this wave's maxima (the same in every lane)
+  double wf = 0.0;            // largest seed-part error (lane 0)
   for (int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6; row < n_pad;
        row += nwaves) {
     T* out = xq + row * dpad;
     if (row >= n) {
       for (int t = lane; t < dpad; t += 64) out[t] = (T)0.0f;
       if (lane == 0) {
-        if (hn) hn[row] = 0.0f;
+        if (hn && seedprod) reinterpret_cast<uint2*>(hn)[row] = make_uint2(0u, 0u);
+        else if (hn) hn[row] = 0.0f;
         if (n64) n64[row] = 0.0;
         if (rho) rho[row] = 0.0;
       }
@@ -326,7 +354,14 @@ quantise_rows_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int 
     // Round the radius up: covers the fp64 rounding of c and of the sums.
     const double rho_up = sqrt(r2) * (1.0 + 0x1p-40) + 0x1p-50 * sqrt(c2);
     if (lane == 0) {
-      if (is_ref) hn[row] = -0.5f * (float)nsq;
+      if (is_ref && seedprod) {
+        T q[4];
+        const double ferr = seed_parts<T>(nsq, cfold, q);
+        reinterpret_cast<uint2*>(hn)[row] = *reinterpret_cast<const uint2*>(q);
+        wf = ferr > wf ? ferr : wf;
+      } else if (is_ref) {
+        hn[row] = -0.5f * (float)nsq;
+      }
       if (n64) n64[row] = nsq;
       if (rho) rho[row] = rho_up;
     }
@@ -336,15 +371,18 @@ quantise_rows_kernel(const float* __restrict__ x, int64_t n, int64_t n_pad, int 
   if (is_ref) {  // uniform: one atomic per maximum per workgroup
     __shared__ double red[kThreads / 64];
     const double bn = block_max(wn, red), bp = block_max(wp, red);
+    const double bf = block_max(wf, red);
     if (threadIdx.x == 0) {
       atomic_max_nonneg(&ctrl->nmax_bits, bn);
       atomic_max_nonneg(&ctrl->pmax_bits, bp);
+      if (seedprod) atomic_max_nonneg(&ctrl->fold_max_bits, bf);
     }
   }
 }
 
 template <typename T>
 hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
+  const double cf = fold_const(p.precision);
   if (!p.fold && p.d >= 64) {
     // 4 waves per block; at most 1024 blocks (one atomic per maximum each).
     const auto grid_rows = [](int64_t rows) {
@@ -354,16 +392,15 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
     hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nr_pad)), dim3(kThreads), 0, st,
                        a.xr, p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r,
                        a.hn_r, p.self ? a.n64_q : (double*)nullptr,
-                       p.self ? a.rho_q : a.rho_r, 1, p.scale_exp, a.perm);
+                       p.self ? a.rho_q : a.rho_r, 1, p.scale_exp, a.perm, p.seedprod, cf);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.self) return e;
     hipLaunchKernelGGL(quantise_rows_kernel<T>, dim3(grid_rows(p.nq_pad)), dim3(kThreads), 0, st,
                        a.xq, p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q,
                        (float*)nullptr, a.n64_q, a.rho_q, 0, p.scale_exp,
-                       (const int32_t*)nullptr);
+                       (const int32_t*)nullptr, 0, cf);
     return hipGetLastError();
   }
-  const double cf = fold_const(p.precision);
   const auto grid_threads = [](int64_t rows) {
     const int64_t g = (rows + kThreads - 1) / kThreads;
     return (unsigned)(g < 1 ? 1 : (g > 1024 ? 1024 : g));
@@ -372,14 +409,14 @@ hipError_t launch_quantise(const Plan& p, const Args& a, hipStream_t st) {
   hipLaunchKernelGGL(quantise_kernel<T>, dim3(blocks_r), dim3(kThreads), 0, st, a.xr,
                      p.nr, p.nr_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_r, a.hn_r,
                      p.self ? a.n64_q : (double*)nullptr, p.self ? a.rho_q : a.rho_r, 1,
-                     p.fold, p.dmain, p.scale_exp, cf, a.perm);
+                     p.fold, p.dmain, p.scale_exp, cf, a.perm, p.seedprod);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.self) return e;
   const unsigned blocks_q = grid_threads(p.nq_pad);
   hipLaunchKernelGGL(quantise_kernel<T>, dim3(blocks_q), dim3(kThreads), 0, st, a.xq,
                      p.nq, p.nq_pad, (int)p.d, p.dpad, a.mu32, a.ctrl, (T*)a.xq_q, (float*)nullptr,
                      a.n64_q, a.rho_q, 0, p.fold, p.dmain, p.scale_exp, cf,
-                     (const int32_t*)nullptr);
+                     (const int32_t*)nullptr, 0);
   return hipGetLastError();
 }
 

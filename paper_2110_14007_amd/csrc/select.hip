@@ -65,14 +65,17 @@ __device__ CertConst cert_const(const Args& a) {
   c.pmax = __longlong_as_double((long long)a.ctrl->pmax_bits);
   c.s = scale_from_maxabs(a.ctrl->maxabs_bits, a.scale_exp);
   const double u = 0x1p-23;  // per-addition allowance (2x the fp32 unit roundoff)
-  // d products, the seed (one term, or four folded parts) and one spare.
-  const double t = (double)a.d + (a.fold ? 6.0 : 2.0);
+  // The seed as four parts against a constant: folded into the rows, or the
+  // product of the register-list tile's seed MFMA; same terms either way.
+  const bool parts = a.fold || a.seedprod;
+  // d products, the seed (one term, or four parts) and one spare.
+  const double t = (double)a.d + (parts ? 6.0 : 2.0);
   c.gam = t * u / (1.0 - t * u);
   c.ms = (double)a.margin_scale;
-  // Seed weight in the sum of |terms|: N_j/2 for an fp32 seed; the folded
-  // parts' magnitudes sum to at most (N_j/2)(1 + 2^-7) (bf16 parts; fp16 less).
-  c.seedw = a.fold ? 2.0 + 0x1p-6 : 2.0;
-  c.fold_err = a.fold ? 2.0 * __longlong_as_double((long long)a.ctrl->fold_max_bits) : 0.0;
+  // Seed weight in the sum of |terms|: N_j/2 for an fp32 seed; the parts'
+  // magnitudes sum to at most (N_j/2)(1 + 2^-7) (bf16 parts; fp16 less).
+  c.seedw = parts ? 2.0 + 0x1p-6 : 2.0;
+  c.fold_err = parts ? 2.0 * __longlong_as_double((long long)a.ctrl->fold_max_bits) : 0.0;
   // Terms that do not depend on the row: u Nmax, the folded seed error and
   // the subnormal allowance.
   c.derr = u * c.nmax + c.fold_err + (double)a.d * 0x1p-120;

@@ -32,6 +32,8 @@ struct Plan {
   int32_t waves_per_group; // waves per workgroup of the tile kernel
   int32_t tile_kind;   // 0: LDS-list tile kernel (tile.h); 1: register-list MFMA kernel (mtile.h)
   int32_t fold;        // 1: rows carry the accumulator seed as extra columns (mtile.h layout)
+  int32_t seedprod;    // 1: the register-list tile forms the seed -N_j/2 by one MFMA of four
+                       // filter-precision parts of -N_j/(2c) against c (hn_r holds the parts)
   int32_t dmain;       // fold layout: columns [0, dmain) hold the row, [dmain, dmain + 4) the seed
   int32_t scale_exp;   // E: the scaled, centred rows satisfy max |s (x - mu)| < 2^E
   int32_t self;        // query set == reference set (one quantised copy)
@@ -123,6 +125,7 @@ struct Args {
   float margin_scale;
   int32_t force_fallback, no_recheck;
   int32_t fold, dmain, scale_exp;
+  int32_t seedprod;  // see Plan::seedprod
   // workspace views
   Ctrl* ctrl;
   double* mu64;
@@ -130,7 +133,8 @@ struct Args {
   double* colpart;
   void* xq_r;       // quantised references [nr_pad x dpad]
   void* xq_q;       // quantised queries [nq_pad x dpad] (== xq_r when self)
-  float* hn_r;      // -0.5 * fl32(||xhat_j||^2) per reference [nr_pad]
+  float* hn_r;      // -0.5 * fl32(||xhat_j||^2) per reference [nr_pad]; with seedprod the
+                    // four seed parts of reference j (filter precision, 8 bytes) instead
   double* n64_q;    // ||xhat_i||^2 per query (fp64) [nq_pad]
   double* rho_q;    // quantisation radius per query, rounded up [nq_pad]
   double* rho_r;    // quantisation radius per reference when the sets differ (NWR), else null

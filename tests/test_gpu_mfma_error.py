@@ -82,14 +82,17 @@ def run(env, bf16, abits, bbits, c0):
     return out.cpu().numpy().astype(np.float64)
 
 
-def check(env, bf16, abits, bbits, c0, what):
-    """Assert the error model on all 1,024 outputs; return the worst ratio."""
+def check(env, bf16, abits, bbits, c0, what, t=None):
+    """Assert the error model on all 1,024 outputs; return the worst ratio.
+    t: the number of terms the bound counts (default K + 1, every product
+    and the seed; a layout whose zero products add nothing may pass fewer)."""
     got = run(env, bf16, abits, bbits, c0)
     A = bits_to_f64(abits, bf16)
     B = bits_to_f64(bbits, bf16)
     K = A.shape[1]
     c0 = np.asarray(c0, dtype=np.float32).astype(np.float64)
-    t = K + 1
+    if t is None:
+        t = K + 1
     gam = (t + 1) * U / (1 - (t + 1) * U)
     worst = 0.0
     worst24 = 0.0
@@ -174,7 +177,8 @@ def test_folded_seed(env, bf16):
     """Rows of at most 8 elements: one 16-wide k-step whose columns 8..11
     carry the seed -N_j / (2 c) as four parts (each the rounding of what the
     earlier parts left) and the queries the constant c there, so that
-    acc = <xq, xr> - N_j / 2 comes out of the single MFMA."""
+    acc = <xq, xr> - N_j / 2 comes out of the single MFMA.  Checked against
+    the certificate's count t = d + 6 (the four zero columns add nothing)."""
     rng = np.random.default_rng(9400 + bf16)
     c = 32768.0 if not bf16 else 1.0
     scale = 2.0 ** 13 if not bf16 else 1.0
@@ -194,7 +198,40 @@ def test_folded_seed(env, bf16):
     b[:8] = q
     b[8:12] = c
     check(env, bf16, quantise(a, bf16), quantise(b, bf16), np.zeros((32, 32), np.float32),
-          "folded seed")
+          "folded seed", t=8 + 6)
+
+
+@pytest.mark.parametrize("bf16", [0, 1], ids=["f16", "bf16"])
+@pytest.mark.parametrize("d", [32, 512])
+def test_seed_product(env, bf16, d):
+    """Rows of more than 8 elements: the sub-tile's chain starts with a seed
+    k-step whose columns 0..3 carry the four parts of -N_j / (2 c) against
+    the constant c (the other twelve columns zero), followed by the d / 16
+    data k-steps.  Checked against the certificate's own count for this
+    layout, t = d + 6 (d products, four parts, a spare; the zero products add
+    nothing), with the scale the planner gives fp16 rows of d elements
+    (d 2^(2E) <= 2^31)."""
+    rng = np.random.default_rng(9500 + bf16 + d)
+    c = 32768.0 if not bf16 else 1.0
+    lg = (d - 1).bit_length()
+    scale = 2.0 ** min(14, (31 - lg) // 2) if not bf16 else 1.0
+    r = rng.uniform(-1, 1, (32, d)) * scale
+    q = rng.uniform(-1, 1, (d, 32)) * scale
+    R = bits_to_f64(quantise(r, bf16), bf16)
+    a = np.zeros((32, 16 + d))
+    a[:, 16:] = R
+    for i in range(32):
+        rest = -float(np.sum(R[i] * R[i])) / 2.0 / c
+        for p in range(4):
+            part = bits_to_f64(quantise(np.array([rest]), bf16), bf16)[0]
+            assert math.isfinite(part)
+            a[i, p] = part
+            rest -= part
+    b = np.zeros((16 + d, 32))
+    b[:4] = c
+    b[16:] = q
+    check(env, bf16, quantise(a, bf16), quantise(b, bf16), np.zeros((32, 32), np.float32),
+          "seed product, d = %d" % d, t=d + 6)
 
 
 @pytest.mark.parametrize("bf16", [0, 1], ids=["f16", "bf16"])
