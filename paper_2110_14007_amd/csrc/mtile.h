@@ -209,6 +209,11 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
 // Reference row (0..31 within the sub-tile) of accumulator r in this lane
 // (32x32 MFMA output layout: column = lane % 32).
 __device__ __forceinline__ int out_row(int r, int h) { return 8 * (r >> 2) + 4 * h + (r & 3); }
+// The part of out_row that does not depend on the lane.  Paths that form row
+// ids take the lane's part 4h through an opaque copy and add this constant:
+// otherwise the compiler keeps the 16 values out_row(r, h) in registers for
+// the whole kernel.
+__host__ __device__ constexpr int out_row_c(int r) { return 8 * (r >> 2) + (r & 3); }
 
 // Merge the first kMerge entries of every lane's queue (fewer where cnt is
 // smaller) into its pair's list; all 64 lanes take part.
@@ -292,7 +297,8 @@ struct Layout {
   static constexpr int rowb = DPAD == 16 ? 32 : DPAD * 2 + 16;
   static constexpr int cpr = DPAD / 8;  // 16-byte chunks per row
   // Sub-tiles per stage: the stage pair, seeds and four queues stay under
-  // 80 KiB so that at least two workgroups share a CU.
+  // 80 KiB so that at least two workgroups share a CU.  (Folded rows with
+  // 16-entry lists take stages of four: see launch_mtile.)
   static constexpr int ns = DPAD == 16 ? 8 : (DPAD == 32 ? 4 : (DPAD == 64 ? 2 : 1));
   // Rows of 256 or more elements keep a 32-query operand of DPAD/2 VGPRs
   // per lane: such kernels run one wave per SIMD.
@@ -341,16 +347,18 @@ __host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int n
 // lets the compiler keep the MFMA accumulators in VGPRs (no AGPR copies
 // around every sub-tile).  16-entry lists on 16-element rows fit three waves
 // (at most 168 registers; their 48 KiB of LDS also admits three workgroups
-// per CU).  64-entry lists and wider rows need more registers and run one
-// wave per SIMD.
-template <int DPAD, int R>
+// per CU), and four on folded rows (at most 128 registers, stages of four
+// sub-tiles: 40 KiB of LDS, four workgroups per CU; the unfolded row's seed
+// MFMA and parts would spill there).  64-entry lists and wider rows need more
+// registers and run one wave per SIMD.
+template <int DPAD, bool FOLD, int R>
 __host__ __device__ constexpr int min_waves() {
-  return R >= 32 || DPAD >= 256 ? 1 : (DPAD == 16 && R <= 8 ? 3 : 2);
+  return R >= 32 || DPAD >= 256 ? 1 : (DPAD == 16 && R <= 8 ? (FOLD ? 4 : 3) : 2);
 }
 
 template <typename ET, int DPAD, bool FOLD, int R, int W, int NS, int NG, int NQ>
 __global__ void __launch_bounds__(W * 64)
-    __attribute__((amdgpu_waves_per_eu(min_waves<DPAD, R>())))
+    __attribute__((amdgpu_waves_per_eu(min_waves<DPAD, FOLD, R>())))
 mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   using V = typename Frag<ET>::V;
   using LY = Layout<DPAD, FOLD>;
@@ -502,9 +510,11 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
     const uint32_t rem = ts < endu ? endu - ts : 0u;
     if (diag || rem < 32u) {
       const int lim = rem < 32u ? (int)rem : 32;
+      int hb = 4 * h;
+      asm volatile("" : "+v"(hb));
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = out_row(r, h);
+        const int row = hb + out_row_c(r);
         if (row >= lim || (diag && row == col)) v[r] = -INFINITY;
       }
     }
@@ -555,6 +565,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   auto insert = [&](auto U, const f32x16 v, uint32_t ts) __attribute__((always_inline)) {
     constexpr int u = decltype(U)::value;
     uint2* const myq = myq0 + u * kQCap * 64;
+    uint32_t tb = ts + 4u * (uint32_t)h;  // row id of accumulator r: tb + out_row_c(r)
+    asm volatile("" : "+v"(tb));
     if constexpr (kQCap == 16) {
       typedef float f32x8 __attribute__((ext_vector_type(8)));
       const f32x8 lo = __builtin_shufflevector(v, v, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -568,8 +580,8 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         if (__ballot(cnt[u] > kQCap - 8)) flush(U);
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-          myq[cnt[u] * 64] =
-              make_uint2(__float_as_uint(cur[r]), (uint32_t)(ts + out_row(8 * hf + r, h)));
+          myq[cnt[u] * 64] = make_uint2(__float_as_uint(cur[r]),
+                                        tb + 16u * (uint32_t)hf + (uint32_t)out_row_c(r));
           cnt[u] += cur[r] > thr[u] ? 1 : 0;
         }
       }
@@ -581,7 +593,7 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
         if (__ballot(mq > thr[u])) {
 #pragma unroll
           for (int r = 4 * q; r < 4 * q + 4; ++r) {
-            myq[cnt[u] * 64] = make_uint2(__float_as_uint(v[r]), (uint32_t)(ts + out_row(r, h)));
+            myq[cnt[u] * 64] = make_uint2(__float_as_uint(v[r]), tb + (uint32_t)out_row_c(r));
             cnt[u] += v[r] > thr[u] ? 1 : 0;
           }
         }
@@ -950,12 +962,18 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 // k-step or two), two (the whole stage) for rows of 64, one otherwise.  Two
 // independent MFMA chains at 64 took the C3 tile from 198 to 184 ms.
 //
+// Folded rows with 16-entry lists run four waves per SIMD (min_waves): their
+// stages hold four sub-tiles, so that a workgroup's LDS (stage pair and
+// queues) is 40 KiB and four workgroups share a CU.  At 4 x 10^6 rows this
+// took the tile from 674 to 648 ms (three waves per SIMD, stages of eight).
+//
 // Tail split: a block of G workgroups on a GPU that runs S of them at once
 // ends with a round of G mod S workgroups that leaves most of the GPU idle.
 // With one reference split, those workgroups' scans are cut into P pieces on
 // P times as many workgroups (tail_pieces picks P), in a second launch whose
 // lists go to the tail region.
-template <typename ET, int DPAD, bool FOLD, int R, int W = 4, int NS = Layout<DPAD, FOLD>::ns,
+template <typename ET, int DPAD, bool FOLD, int R, int W = 4,
+          int NS = (FOLD && R <= 8 ? 4 : Layout<DPAD, FOLD>::ns),
           int NG = (DPAD <= 32 ? 4 : (DPAD == 64 ? 2 : 1)), int NQ = query_groups(DPAD, FOLD, R)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st, TileTail* tail) {
