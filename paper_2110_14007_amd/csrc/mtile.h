@@ -347,9 +347,9 @@ __host__ __device__ constexpr size_t lds_bytes(int dpad, bool fold, int w, int n
 // lets the compiler keep the MFMA accumulators in VGPRs (no AGPR copies
 // around every sub-tile).  16-entry lists on 16-element rows fit three waves
 // (at most 168 registers; their 48 KiB of LDS also admits three workgroups
-// per CU), and four on folded rows (at most 128 registers, stages of four
-// sub-tiles: 40 KiB of LDS, four workgroups per CU; the unfolded row's seed
-// MFMA and parts would spill there).  64-entry lists and wider rows need more
+// per CU), and four on folded rows (at most 128 registers; 16-wave
+// workgroups, see launch_mtile; the unfolded row's seed MFMA and parts would
+// spill there).  64-entry lists and wider rows need more
 // registers and run one wave per SIMD.
 template <int DPAD, bool FOLD, int R>
 __host__ __device__ constexpr int min_waves() {
@@ -962,18 +962,22 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 // k-step or two), two (the whole stage) for rows of 64, one otherwise.  Two
 // independent MFMA chains at 64 took the C3 tile from 198 to 184 ms.
 //
-// Folded rows with 16-entry lists run four waves per SIMD (min_waves): their
-// stages hold four sub-tiles, so that a workgroup's LDS (stage pair and
-// queues) is 40 KiB and four workgroups share a CU.  At 4 x 10^6 rows this
-// took the tile from 674 to 648 ms (three waves per SIMD, stages of eight).
+// Folded rows with 16-entry lists run four waves per SIMD (min_waves) in one
+// workgroup of 16 waves per CU, 512 queries, with stages of 16 sub-tiles:
+// the stage pair (32 KiB) and the 16 queues (128 KiB) fill the CU's 160 KiB,
+// and every staged row serves 512 queries.  At 4 x 10^6 rows: 666 ms with
+// three waves per SIMD (4 waves a workgroup, stages of eight), 647 ms with
+// four (stages of four, four workgroups per CU), 591 ms with 8-wave
+// workgroups and stages of eight, 580 ms in this form (622 ms with stages
+// of eight).
 //
 // Tail split: a block of G workgroups on a GPU that runs S of them at once
 // ends with a round of G mod S workgroups that leaves most of the GPU idle.
 // With one reference split, those workgroups' scans are cut into P pieces on
 // P times as many workgroups (tail_pieces picks P), in a second launch whose
 // lists go to the tail region.
-template <typename ET, int DPAD, bool FOLD, int R, int W = 4,
-          int NS = (FOLD && R <= 8 ? 4 : Layout<DPAD, FOLD>::ns),
+template <typename ET, int DPAD, bool FOLD, int R, int W = (FOLD && R <= 8 ? 16 : 4),
+          int NS = (FOLD && R <= 8 ? 16 : Layout<DPAD, FOLD>::ns),
           int NG = (DPAD <= 32 ? 4 : (DPAD == 64 ? 2 : 1)), int NQ = query_groups(DPAD, FOLD, R)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st, TileTail* tail) {
