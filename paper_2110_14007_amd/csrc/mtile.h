@@ -969,15 +969,19 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 // three waves per SIMD (4 waves a workgroup, stages of eight), 647 ms with
 // four (stages of four, four workgroups per CU), 591 ms with 8-wave
 // workgroups and stages of eight, 580 ms in this form (622 ms with stages
-// of eight).
+// of eight).  Rows of 64 elements with 32-entry lists (28-slot queues) take
+// 8-wave workgroups, one per CU, with stages of four sub-tiles (150 KiB of
+// LDS): at 10^6 rows 180 -> 163 ms.  Rows of 32 elements keep 4-wave
+// workgroups: 8 waves took that tile from 2.17 to 3.1-3.6 ms.
 //
 // Tail split: a block of G workgroups on a GPU that runs S of them at once
 // ends with a round of G mod S workgroups that leaves most of the GPU idle.
 // With one reference split, those workgroups' scans are cut into P pieces on
 // P times as many workgroups (tail_pieces picks P), in a second launch whose
 // lists go to the tail region.
-template <typename ET, int DPAD, bool FOLD, int R, int W = (FOLD && R <= 8 ? 16 : 4),
-          int NS = (FOLD && R <= 8 ? 16 : Layout<DPAD, FOLD>::ns),
+template <typename ET, int DPAD, bool FOLD, int R,
+          int W = (FOLD && R <= 8 ? 16 : (DPAD == 64 && !FOLD && R == 16) ? 8 : 4),
+          int NS = (FOLD && R <= 8 ? 16 : (DPAD == 64 && !FOLD && R == 16) ? 4 : Layout<DPAD, FOLD>::ns),
           int NG = (DPAD <= 32 ? 4 : (DPAD == 64 ? 2 : 1)), int NQ = query_groups(DPAD, FOLD, R)>
 hipError_t launch_mtile(const Plan& p, const Args& a, int64_t q_begin, int64_t q_rows,
                         hipStream_t st, TileTail* tail) {
