@@ -10,6 +10,8 @@ Functions:
   knn_self(x, k, rows=None)               -> kNN of X against itself, self excluded
   lof(idx, dist)                          -> (lof, lrd, kdist), fp64 [n]
   lof_rows(x, k, rows)                    -> (lof, lrd, kdist) for the listed rows
+  lof_ties(x, k)                          -> (lof, lrd, kdist, count): LOF on Breunig's
+                                             tie-inclusive k-distance neighbourhoods
   knn_score(dist, method="kth")           -> kNN outlier score from the k neighbour distances:
                                              k-th (default), mean, median or sum
   knn_vote(idx, labels, n_classes)        -> kNN classifier: majority label, ties to the smallest
@@ -294,6 +296,45 @@ def lof(idx, dist):
     if rc != 0:
         raise ValueError("oracle_lof failed (rc=%d)" % rc)
     return out[0], out[1], out[2]
+
+
+def lof_ties(x, k: int):
+    """LOF on Breunig et al.'s k-distance neighbourhoods, which keep every point
+    tied at the k-distance (so a neighbourhood can hold more than k points);
+    each point's own row excluded.  LOF is one of Table 1's detectors and, like
+    LOCI, a user of neighbours within range (Section 5.3): N_k(p) is the range
+    query around p at radius kdist(p).
+
+      D2(p, o)   fp64 sum over the columns in order of ((double)x_pt - (double)x_ot)^2
+      kd2(p)     the k-th smallest D2(p, o) over o != p
+      N_k(p)   = {o != p : D2(p, o) <= kd2(p)}
+      kdist(p) = sqrt(kd2(p)),  D(p, o) = sqrt(D2(p, o))
+      reach(p, o) = max(kdist(o), D(p, o))
+      lrd(p)   = 1 / (sum_{o in N_k(p)} reach(p, o) / |N_k(p)| + 1e-10)
+      LOF(p)   = (sum_{o in N_k(p)} lrd(o) / |N_k(p)|) / lrd(p)
+
+    Plain n x n evaluation (memory n^2 fp64): for small point sets.
+    Returns (lof, lrd, kdist, count) with count[p] = |N_k(p)|."""
+    d2 = sq_dist_matrix(x)
+    n = d2.shape[0]
+    k = int(k)
+    if not 1 <= k < n:
+        raise ValueError("lof_ties needs 1 <= k < n")
+    np.fill_diagonal(d2, np.inf)  # o != p
+    kd2 = np.sort(d2, axis=1)[:, k - 1]
+    kdist = np.sqrt(kd2)
+    members = [np.nonzero(d2[p] <= kd2[p])[0] for p in range(n)]
+    count = np.array([m.size for m in members], dtype=np.int64)
+    lrd = np.empty(n, dtype=np.float64)
+    for p in range(n):
+        m = members[p]
+        reach = np.maximum(kdist[m], np.sqrt(d2[p, m]))
+        lrd[p] = 1.0 / (reach.sum() / m.size + 1e-10)
+    lof_v = np.empty(n, dtype=np.float64)
+    for p in range(n):
+        m = members[p]
+        lof_v[p] = (lrd[m].sum() / m.size) / lrd[p]
+    return lof_v, lrd, kdist, count
 
 
 def lof_rows(x, k: int, rows, threads: int = 0):
