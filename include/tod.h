@@ -10,7 +10,8 @@
  *     lower index;
  *   - the kNN-OD outlier score (distance to the k-th neighbour, Table 1);
  *   - the LOF outlier score (Table 1; Breunig et al. 2000, with exactly k
- *     neighbours and lrd = 1 / (mean reach-distance + 1e-10)).
+ *     neighbours and lrd = 1 / (mean reach-distance + 1e-10)), or, through
+ *     tod_lof_ties, on Breunig's tie-inclusive k-distance neighbourhoods.
  *
  * It follows the paper's provable quantization (Section 5.2): inputs are
  * quantised (fp32 / fp16 / bf16 after centring and power-of-two scaling),
@@ -56,8 +57,9 @@ typedef enum {
   TOD_ERR_UNSUPPORTED = 4, /* k > 256, d > 4096, or more than 2^31 - 1 rows */
   TOD_ERR_HIP = 5,         /* a HIP launch or runtime call failed; see tod_last_error() */
   TOD_ERR_INTERNAL = 6,
-  TOD_ERR_CAPACITY = 7     /* tod_nwr, tod_loci: more pairs in range than the output capacity
-                            * (tod_nwr still writes the row offsets and the total) */
+  TOD_ERR_CAPACITY = 7     /* tod_nwr, tod_loci, tod_lof_ties: more pairs in range than the
+                            * output capacity (tod_nwr still writes the row offsets and the
+                            * total) */
 } tod_status;
 
 /* Precision of the shortlist filter (the exact recheck always works from the
@@ -127,9 +129,10 @@ typedef struct {
                           /* ms_recheck includes the merge of the split lists, which runs
                            * inside the recheck kernel (there is no separate ms_merge) */
   int32_t reordered;      /* 1 if the scan used the grouped row order (see tod_options.reorder) */
-  int64_t pairs_candidate; /* tod_nwr: pairs the filter could not rule out of range */
-  int64_t pairs_uncertain; /* tod_nwr: candidates whose range test needed the exact distance */
-  int64_t pairs_in_range;  /* tod_nwr: pairs within the threshold */
+  int64_t pairs_candidate; /* range queries (tod_nwr, tod_loci, tod_lof_ties): pairs the filter
+                            * could not rule out of range */
+  int64_t pairs_uncertain; /* range queries: candidates whose test needed the exact distance */
+  int64_t pairs_in_range;  /* range queries: pairs within the threshold */
   int32_t tail_parts;      /* parts the last partly filled round was scanned in (1: none) */
   int64_t tail_rows;       /* query rows scanned in parts, summed over the blocks */
   int32_t list_runs;       /* 2 if each shortlist was built as two runs of K'/2 entries (the
@@ -221,6 +224,40 @@ tod_status tod_knn_score(const float* x, int64_t n, int64_t d, int32_t k,
 tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_options* opts,
                    void* workspace, size_t ws_bytes, void* stream, float* lof_out,
                    float* knn_score_out, int64_t* idx_out, float* dist_out, tod_stats* stats);
+
+/*
+ * LOF on Breunig et al.'s k-distance neighbourhoods (Table 1's LOF; a user
+ * of neighbours within range, Section 5.3): every point tied at the
+ * k-distance belongs, so a neighbourhood can hold more than k points.  For
+ * every row p of X (its own row excluded):
+ *   kd2(p)   = the k-th smallest D2(p, o), o != p
+ *   N_k(p)   = {o != p : D2(p, o) <= kd2(p)}
+ *   reach(p, o) = max(sqrt(kd2(o)), sqrt(D2(p, o)))
+ *   lrd(p)   = 1 / (mean over N_k(p) of reach(p, o) + 1e-10)
+ *   LOF(p)   = mean over N_k(p) of lrd(o), divided by lrd(p)
+ * D2 is the fp64 squared distance summed over the columns in order without
+ * fused multiply-adds; membership is decided exactly in it (as tod_nwr
+ * decides range membership).  Where no distance ties the k-distance, N_k(p)
+ * is the k nearest and the result is tod_lof's.
+ * Steps: the exact kNN lists (as tod_knn, self excluded), kd2 from them, the
+ * neighbourhoods by the range query at each row's own radius (tod_nwr's
+ * fp16 / bf16 range filter with exact verification), then lrd and LOF.
+ *   capacity         pairs (p, o) the workspace holds, summed over p; at
+ *                    least n k (no ties)
+ *   lof_out[n]       fp32 LOF scores (computed in fp64)
+ *   count_out[n]     optional: |N_k(p)| (int32)
+ * Workspace: tod_lof_ties_workspace_size(n, d, k, capacity, opts) bytes (0:
+ * invalid sizes or options).  Requires d <= 512 and an fp16 / bf16 / AUTO
+ * precision (TOD_ERR_UNSUPPORTED otherwise); opts->exclude_self is ignored
+ * (always on).  TOD_ERR_CAPACITY if the neighbourhoods hold more than
+ * capacity pairs: stats->pairs_in_range (when stats is given) then holds the
+ * number needed, and lof_out is unspecified.
+ */
+size_t tod_lof_ties_workspace_size(int64_t n, int64_t d, int32_t k, int64_t capacity,
+                                   const tod_options* opts);
+tod_status tod_lof_ties(const float* x, int64_t n, int64_t d, int32_t k, int64_t capacity,
+                        const tod_options* opts, void* workspace, size_t ws_bytes, void* stream,
+                        float* lof_out, int32_t* count_out, tod_stats* stats);
 
 /*
  * kNN-OD scores of new points xq[nq x d] against the fitted set xr[nr x d]

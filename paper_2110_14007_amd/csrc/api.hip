@@ -634,7 +634,10 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
 tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t d,
                    double phi, const tod_options* opts_in, void* ws, size_t ws_bytes,
                    void* stream, int64_t* row_ptr_out, int64_t capacity, int64_t* idx_out,
-                   float* dist_out, int64_t* total_out, tod_stats* stats) {
+                   float* dist_out, int64_t* total_out, tod_stats* stats,
+                   const double* phi2_row = nullptr) {
+  // phi2_row: a squared radius per query row (device, finite, >= 0) in place
+  // of phi (LOF on tie-inclusive neighbourhoods).
   g_last_error.clear();
   tod_options o;
   tod_status st = resolve_options(opts_in, &o);
@@ -644,6 +647,7 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
   if (!xq || !xr) return fail(TOD_ERR_INVALID_ARG, "null input pointer");
   if (!row_ptr_out) return fail(TOD_ERR_INVALID_ARG, "null row_ptr output");
   if (!ws) return fail(TOD_ERR_INVALID_ARG, "null workspace");
+  if (phi2_row) phi = 0.0;
   if (!(phi >= 0.0) || isinf(phi)) return fail(TOD_ERR_INVALID_ARG, "phi must be finite and >= 0");
   if (idx_out && capacity < 0) return fail(TOD_ERR_INVALID_ARG, "capacity must be >= 0");
   if (dist_out && !idx_out) return fail(TOD_ERR_INVALID_ARG, "dist_out needs idx_out");
@@ -693,6 +697,7 @@ tod_status run_nwr(const float* xq, int64_t nq, const float* xr, int64_t nr, int
   a.rho_q = (double*)(base + L.rho_q);
   a.rho_r = (double*)(base + L.rho_r);
   a.phi = phi;
+  a.phi2_row = phi2_row;
   a.ccount = (int32_t*)(base + L.ccount);
   a.coff = (int64_t*)(base + L.coff);
   a.incnt = (int32_t*)(base + L.incnt);
@@ -950,6 +955,134 @@ tod_status run_loci(const float* x, int64_t n, int64_t d, const double* radii, i
   return TOD_OK;
 }
 
+// LOF on tie-inclusive neighbourhoods: the exact kNN lists, each row's
+// squared k-distance, the neighbourhoods as CSR (a range query per row at
+// that radius), lrd and LOF.  Workspace: the CSR offsets and ids, the lists,
+// the squared k-distances and lrd, then a region the kNN call and the range
+// query use in turn.
+struct LofTiesLayout {
+  size_t row_ptr, nbr, lists, kd2, lrd, inner;
+};
+
+LofTiesLayout lof_ties_layout(int64_t n, int32_t k, int64_t capacity) {
+  LofTiesLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  L.row_ptr = take(sizeof(int64_t) * (size_t)(n + 1));
+  L.nbr = take(sizeof(int64_t) * (size_t)capacity);
+  L.lists = take(sizeof(int64_t) * (size_t)n * (size_t)k);
+  L.kd2 = take(sizeof(double) * (size_t)n);
+  L.lrd = take(sizeof(double) * (size_t)n);
+  L.inner = off;
+  return L;
+}
+
+// Bytes of the shared region: the kNN call's workspace (X against itself)
+// or the range query's with candidate room for every pair of the
+// neighbourhoods, a quarter more for the filter's uncertain ones and 2^20
+// (one fill pass for all rows), whichever is larger; 0 if invalid.
+size_t lof_ties_inner_bytes(int64_t n, int64_t d, int32_t k, int64_t capacity,
+                            const tod_options& o) {
+  Plan p;
+  const char* why;
+  if (tod::make_plan(n, n, d, k, 0, 1, o, &p, &why) != TOD_OK) return 0;
+  const size_t knn = tod::make_layout(p).total;
+  const size_t nwr = nwr_ws_bytes(n, n, d, o, 1, capacity + capacity / 4 + ((int64_t)1 << 20));
+  if (nwr == 0) return 0;
+  return knn > nwr ? knn : nwr;
+}
+
+tod_status check_lof_ties(int64_t n, int64_t d, int32_t k, int64_t capacity,
+                          const tod_options& o) {
+  tod_status st = check_sizes(n, n, d, k, 1);
+  if (st != TOD_OK) return st;
+  if (d > 512)
+    return fail(TOD_ERR_UNSUPPORTED, "tod_lof_ties supports rows of at most 512 elements");
+  if (o.precision == TOD_PREC_FP32)
+    return fail(TOD_ERR_UNSUPPORTED,
+                "tod_lof_ties filters in fp16 or bf16 (its range query is MFMA only)");
+  if (capacity < n * (int64_t)k)
+    return fail(TOD_ERR_INVALID_ARG, "capacity must be >= n k (every neighbourhood holds k points)");
+  return TOD_OK;
+}
+
+tod_status run_lof_ties(const float* x, int64_t n, int64_t d, int32_t k, int64_t capacity,
+                        const tod_options* opts_in, void* ws, size_t ws_bytes, void* stream,
+                        float* lof_out, int32_t* count_out, tod_stats* stats) {
+  g_last_error.clear();
+  tod_options o;
+  tod_status st = resolve_options(opts_in, &o);
+  if (st != TOD_OK) return st;
+  o.exclude_self = 1;
+  if (stats && stats->struct_size != sizeof(tod_stats))
+    return fail(TOD_ERR_INVALID_ARG, "tod_stats.struct_size does not match this library");
+  if (!x) return fail(TOD_ERR_INVALID_ARG, "null input pointer");
+  if (!lof_out) return fail(TOD_ERR_INVALID_ARG, "null LOF output");
+  if (!ws) return fail(TOD_ERR_INVALID_ARG, "null workspace");
+  if ((uintptr_t)ws & 255) return fail(TOD_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  st = check_lof_ties(n, d, k, capacity, o);
+  if (st != TOD_OK) return st;
+  const LofTiesLayout L = lof_ties_layout(n, k, capacity);
+  const size_t inner = lof_ties_inner_bytes(n, d, k, capacity, o);
+  if (inner == 0) return fail(TOD_ERR_INVALID_ARG, "sizes or options the planner rejects");
+  if (ws_bytes < L.inner + inner)
+    return fail(TOD_ERR_WORKSPACE, "workspace too small for " + std::to_string(capacity) +
+                                       " pairs: need " + std::to_string(L.inner + inner) +
+                                       " bytes, got " + std::to_string(ws_bytes));
+  char* base = (char*)ws;
+  int64_t* row_ptr = (int64_t*)(base + L.row_ptr);
+  int64_t* nbr = (int64_t*)(base + L.nbr);
+  int64_t* lists = (int64_t*)(base + L.lists);
+  double* kd2 = (double*)(base + L.kd2);
+  double* lrd = (double*)(base + L.lrd);
+  hipStream_t s = (hipStream_t)stream;
+  // 1. Exact kNN lists (X against itself, self excluded).
+  st = run(x, n, x, n, d, k, &o, 1, 0, base + L.inner, ws_bytes - L.inner, stream, lists,
+           nullptr, nullptr, nullptr, nullptr, 0, nullptr, stats);
+  if (st != TOD_OK) return st;
+  Timers tm;
+  tm.on = stats != nullptr;
+  hipEvent_t e0 = tm.mark(s);
+  // 2. Each row's squared k-distance in the range query's exact arithmetic.
+  hipError_t he = tod::launch_ties_radius(x, n, (int)d, k, lists, kd2, s);
+  if (he != hipSuccess) return hip_fail(he, "k-distance launch");
+  hipEvent_t e1 = tm.mark(s);
+  // 3. The neighbourhoods: the range query at each row's own radius.
+  tod_stats rs;
+  memset(&rs, 0, sizeof(rs));
+  rs.struct_size = sizeof(tod_stats);
+  int64_t total = 0;
+  st = run_nwr(x, n, x, n, d, 0.0, &o, base + L.inner, ws_bytes - L.inner, stream, row_ptr,
+               capacity, nbr, nullptr, &total, stats ? &rs : nullptr, kd2);
+  if (stats) {
+    stats->pairs_candidate = rs.pairs_candidate;
+    stats->pairs_uncertain = rs.pairs_uncertain;
+    stats->pairs_in_range = total;
+  }
+  if (st != TOD_OK) return st;
+  // 4. lrd and LOF over the neighbourhoods.
+  hipEvent_t e2 = tm.mark(s);
+  he = tod::launch_lof_ties(x, n, (int)d, row_ptr, nbr, kd2, lrd, lof_out, count_out, s);
+  if (he != hipSuccess) return hip_fail(he, "LOF launch");
+  hipEvent_t e3 = tm.mark(s);
+  if (stats) {
+    he = hipStreamSynchronize(s);
+    if (he != hipSuccess) return hip_fail(he, "LOF synchronize");
+    const float t_rad = Timers::ms(e0, e1), t_lof = Timers::ms(e2, e3);
+    stats->ms_prep += rs.ms_prep;
+    stats->ms_tile += rs.ms_tile;
+    stats->ms_recheck += rs.ms_recheck + t_rad;
+    stats->ms_score = t_lof;
+    stats->ms_total += t_rad + rs.ms_total + t_lof;
+    stats->tile_launches += rs.tile_launches;
+  }
+  return TOD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1155,6 +1288,24 @@ tod_status tod_loci(const float* x, int64_t n, int64_t d, const double* radii, i
   return run_loci(x, n, d, radii, n_radii, alpha, n_min, k_sigma, capacity, opts, workspace,
                   ws_bytes, stream, score_out, flag_out, n_alpha_out, n_r_out, mdef_out,
                   sigma_mdef_out, stats);
+}
+
+size_t tod_lof_ties_workspace_size(int64_t n, int64_t d, int32_t k, int64_t capacity,
+                                   const tod_options* opts) {
+  tod_options o;
+  if (resolve_options(opts, &o) != TOD_OK) return 0;
+  o.exclude_self = 1;
+  if (check_lof_ties(n, d, k, capacity, o) != TOD_OK) return 0;
+  const size_t inner = lof_ties_inner_bytes(n, d, k, capacity, o);
+  if (inner == 0) return 0;
+  return lof_ties_layout(n, k, capacity).inner + inner;
+}
+
+tod_status tod_lof_ties(const float* x, int64_t n, int64_t d, int32_t k, int64_t capacity,
+                        const tod_options* opts, void* workspace, size_t ws_bytes, void* stream,
+                        float* lof_out, int32_t* count_out, tod_stats* stats) {
+  return run_lof_ties(x, n, d, k, capacity, opts, workspace, ws_bytes, stream, lof_out,
+                      count_out, stats);
 }
 
 tod_status tod_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, const tod_options* opts,

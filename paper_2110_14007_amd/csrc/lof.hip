@@ -71,7 +71,108 @@ lof_kernel(int64_t n, int k, int P, const int32_t* __restrict__ idx,
   }
 }
 
+// ---------------------------------------------------------------------------
+// LOF on tie-inclusive k-distance neighbourhoods (tod_lof_ties; Breunig et
+// al.'s N_k(p), which keeps every point tied at the k-distance, so that it can
+// hold more than k points; Section 5.3's range operator finds it):
+//   kd2(p)   = the k-th smallest D2(p, o), o != p
+//   N_k(p)   = {o != p : D2(p, o) <= kd2(p)}     (a range query per row)
+//   reach(p, o) = max(sqrt(kd2(o)), sqrt(D2(p, o)))
+//   lrd(p)   = 1 / (sum_N reach / |N_k(p)| + 1e-10)
+//   LOF(p)   = (sum_N lrd(o) / |N_k(p)|) / lrd(p)
+// D2 is the definition's fp64 sum over the columns in order (exact_d2), the
+// same arithmetic as the range query's exact test, so that a point tied with
+// the k-th neighbour in that arithmetic lands in N_k(p) and no list entry
+// falls out of it.  One wave per point; the per-lane partial sums are added
+// in a fixed butterfly (run-to-run identical).
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ double wave_sum(double v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// kd2[p] = the largest D2(p, o) over p's k exact neighbours, i.e. the k-th
+// smallest (the largest, should the list order disagree with the column-order
+// sum in the last bit).
+__global__ void __launch_bounds__(256)
+ties_radius_kernel(const float* __restrict__ x, int64_t n, int d, int k,
+                   const int64_t* __restrict__ lists, double* __restrict__ kd2) {
+#pragma clang fp contract(off)
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t p = (int64_t)blockIdx.x * 4 + wave;
+  if (p >= n) return;  // uniform per wave
+  const float* xp = x + p * (int64_t)d;
+  double m = 0.0;
+  for (int i = lane; i < k; i += 64) {
+    const int64_t o = lists[p * k + i];
+    const double v = exact_d2(xp, x + o * (int64_t)d, d);
+    m = v > m ? v : m;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const double t = __shfl_xor(m, o, 64);
+    m = t > m ? t : m;
+  }
+  if (lane == 0) kd2[p] = m;
+}
+
+__global__ void __launch_bounds__(256)
+lrd_ties_kernel(const float* __restrict__ x, int64_t n, int d, const int64_t* __restrict__ row_ptr,
+                const int64_t* __restrict__ nbr, const double* __restrict__ kd2,
+                double* __restrict__ lrd) {
+#pragma clang fp contract(off)
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t p = (int64_t)blockIdx.x * 4 + wave;
+  if (p >= n) return;  // uniform per wave
+  const float* xp = x + p * (int64_t)d;
+  const int64_t beg = row_ptr[p], end = row_ptr[p + 1];
+  double sum = 0.0;
+  for (int64_t e = beg + lane; e < end; e += 64) {
+    const int64_t o = nbr[e];
+    const double dpo = sqrt(exact_d2(xp, x + o * (int64_t)d, d));
+    const double ko = sqrt(kd2[o]);
+    sum = sum + (ko > dpo ? ko : dpo);  // reach(p, o)
+  }
+  sum = wave_sum(sum);
+  if (lane == 0) lrd[p] = 1.0 / (sum / (double)(end - beg) + 1e-10);
+}
+
+__global__ void __launch_bounds__(256)
+lof_ties_kernel(int64_t n, const int64_t* __restrict__ row_ptr, const int64_t* __restrict__ nbr,
+                const double* __restrict__ lrd, float* __restrict__ lof,
+                int32_t* __restrict__ count) {
+#pragma clang fp contract(off)
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t p = (int64_t)blockIdx.x * 4 + wave;
+  if (p >= n) return;  // uniform per wave
+  const int64_t beg = row_ptr[p], end = row_ptr[p + 1];
+  double sum = 0.0;
+  for (int64_t e = beg + lane; e < end; e += 64) sum = sum + lrd[nbr[e]];
+  sum = wave_sum(sum);
+  if (lane == 0) {
+    lof[p] = (float)((sum / (double)(end - beg)) / lrd[p]);
+    if (count) count[p] = (int32_t)(end - beg);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_ties_radius(const float* x, int64_t n, int d, int k, const int64_t* lists,
+                              double* kd2, hipStream_t st) {
+  hipLaunchKernelGGL(ties_radius_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, st, x, n, d,
+                     k, lists, kd2);
+  return hipGetLastError();
+}
+
+hipError_t launch_lof_ties(const float* x, int64_t n, int d, const int64_t* row_ptr,
+                           const int64_t* nbr, const double* kd2, double* lrd, float* lof,
+                           int32_t* count, hipStream_t st) {
+  const unsigned g = (unsigned)((n + 3) / 4);
+  hipLaunchKernelGGL(lrd_ties_kernel, dim3(g), dim3(256), 0, st, x, n, d, row_ptr, nbr, kd2, lrd);
+  hipLaunchKernelGGL(lof_ties_kernel, dim3(g), dim3(256), 0, st, n, row_ptr, nbr,
+                     (const double*)lrd, lof, count);
+  return hipGetLastError();
+}
 
 hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t st) {
   // Points per workgroup: P k <= kFlat terms fit in LDS and P <= kThreads

@@ -1,6 +1,6 @@
 // Neighbours within range (Section 5.3): exact verification of the filter's
-// uncertain pairs (Section 5.2 step iii, "recalculate only where the
-// verification fails") and assembly of the CSR output.
+// uncertain pairs (Section 5.2 step iii: exact recomputation only for the
+// pairs the low-precision check cannot decide) and assembly of the CSR output.
 //
 // After the fill pass (rtile.h) the candidate buffer holds, for each query
 // row of the batch, its candidates in increasing reference index; bit 31
@@ -13,8 +13,10 @@
 //           distance, computed as in the definition: fp64, columns in order,
 //           ((double)x - (double)y)^2 added one at a time with no fused
 //           multiply-add, so the in-range decision D2 <= phi^2 is the same
-//           bit for bit as a plain fp64 evaluation.  Kept candidates get
-//           their distance (or 0), dropped ones -1; the row's count is stored.
+//           bit for bit as a plain fp64 evaluation (against phi^2, or the
+//           row's own squared radius when one is given per row).  Kept
+//           candidates get their distance (or 0), dropped ones -1; the row's
+//           count is stored.
 //   scan    row offsets = exclusive prefix sums of the counts (continuing
 //           from the previous batch's last offset).
 //   emit    one wave per row: kept candidates are compacted in order (ballot
@@ -39,7 +41,7 @@ constexpr int kScanChunk = kScanT * kScanPer;
 // tile's (rtile.h) with N_j <= -2 hn_r[j] (1 + 2^-22) and rho_j in place of
 // Nmax and Pmax.
 __device__ __forceinline__ int pair_test(const Args& a, double s, double gam, double ni,
-                                         double rho_i, uint32_t j, float acc) {
+                                         double rho_i, double phi, uint32_t j, float acc) {
   const double ms = (double)a.margin_scale;
   const double u = 0x1p-23;
   const double nj = -2.0 * (double)a.hn_r[j] * (1.0 + 0x1p-22);
@@ -47,7 +49,7 @@ __device__ __forceinline__ int pair_test(const Args& a, double s, double gam, do
   const double r = ms * (rho_i + a.rho_r[j]);
   const double t = -2.0 * (double)acc;
   const double slack = 1e-12 * (ni + fabs(t) + e);
-  const double ps = s * a.phi;
+  const double ps = s * phi;
   const double hi = ni + t + e + slack;
   if (hi >= 0.0 && sqrt(hi) + r < ps * (1.0 - 4e-9)) return 1;
   const double lo = ni + t - e - slack;
@@ -76,7 +78,10 @@ range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
   const int64_t beg = a.coff[row * a.splits] - a.cbase;
   const int64_t end = a.coff[(row + 1) * a.splits] - a.cbase;
   const float* qrow = a.xq + row * (int64_t)a.d;
-  const double phi2 = a.phi * a.phi;
+  // The row's radius: one for all rows, or the row's own squared radius (its
+  // root only feeds the filter's margins, never the exact test).
+  const double phi2 = a.phi2_row ? a.phi2_row[row] : a.phi * a.phi;
+  const double phi = a.phi2_row ? sqrt(phi2) : a.phi;
   const double s = scale_from_maxabs(a.ctrl->maxabs_bits, a.scale_exp);
   const double tt = (double)a.d + 2.0;
   const double gam = tt * 0x1p-23 / (1.0 - tt * 0x1p-23);
@@ -108,7 +113,8 @@ range_verify_kernel(Args a, int64_t b0, int64_t rows, int32_t want_dist) {
     // Uncertain for the tile: first the per-pair test (not under
     // force_fallback, which recomputes every candidate).
     int pt = 0;
-    if (live && (c >> 31) && !a.force_fallback) pt = pair_test(a, s, gam, ni, rho_i, j, a.cand_d[p]);
+    if (live && (c >> 31) && !a.force_fallback)
+      pt = pair_test(a, s, gam, ni, rho_i, phi, j, a.cand_d[p]);
     const bool u = live && (c >> 31) && pt == 0;
     const bool need = live && (u || (want_dist && pt >= 0));
     // Decided without the exact distance: in range for certain (distance

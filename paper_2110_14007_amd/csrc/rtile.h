@@ -69,7 +69,9 @@ __device__ __forceinline__ void range_thresholds(const Args& a, int64_t q, float
   const double err = ms * (gam * (ni + 2.0 * nmax) * (1.0 + 1e-6) + u * nmax +
                            (double)a.d * 0x1p-120);
   const double r = ms * (a.rho_q[q] + pmax);
-  const double ps = s * a.phi;
+  // A per-row squared radius enters through its fp64 square root; the 4e-9
+  // slack below covers that rounding many times over.
+  const double ps = s * (a.phi2_row ? sqrt(a.phi2_row[q]) : a.phi);
   const double bo = ps * (1.0 + 4e-9) + r;
   const double tout = bo * bo + err - ni + 1e-12 * (bo * bo + ni + err);
   aout = round_down_f32(-0.5 * tout);

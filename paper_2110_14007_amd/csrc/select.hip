@@ -501,14 +501,14 @@ recheck_lanes_kernel(Args a, int64_t q_begin, int64_t q_rows) {
 }
 
 // ---------------------------------------------------------------------------
-// Exact fallback ("recalculate on the subset where the verification fails",
-// Section 5.2): a brute-force fp64 scan of every reference for the rows in the
-// worklist.  The scan is spread over (row, reference chunk) pairs so that a
-// handful of failing rows still fills the GPU: with c failing rows each row is
-// cut into P = clamp(kFbGrid / c, 1, kFbMaxChunks) chunks.  A chunk keeps its
-// k smallest (D^2, j) in LDS; with P == 1 it is the answer, otherwise the P
-// sorted chunk lists go to the workspace and fallback_merge_kernel picks the
-// k smallest of them per row.
+// Exact fallback (Section 5.2: the rows the verification cannot certify are
+// computed again at full precision): a brute-force fp64 scan of every
+// reference for the rows in the worklist.  The scan is spread over (row,
+// reference chunk) pairs so that a handful of failing rows still fills the
+// GPU: with c failing rows each row is cut into P = clamp(kFbGrid / c, 1,
+// kFbMaxChunks) chunks.  A chunk keeps its k smallest (D^2, j) in LDS; with
+// P == 1 it is the answer, otherwise the P sorted chunk lists go to the
+// workspace and fallback_merge_kernel picks the k smallest of them per row.
 // ---------------------------------------------------------------------------
 constexpr int kFbThreads = 256;
 constexpr int kFbSize = 1024;  // sorted best k in [0, k), candidates appended after them

@@ -178,6 +178,8 @@ struct Args {
   int32_t* pred_out;        // classifier: predicted classes [nq]
   // neighbours within range (rtile.h, nwr.hip)
   double phi;          // the range threshold (a distance)
+  const double* phi2_row;  // null, or a squared radius per query row [nq]: the range test of
+                           // row q is then D2 <= phi2_row[q] (exact fp64), phi unused
   int32_t* ccount;     // count pass: candidates per (query, split) [nq_pad x S]
   int64_t* coff;       // their exclusive prefix sums [nq x S + 1]
   int64_t cbase;       // candidate offset of the first row of the current query batch
@@ -303,6 +305,14 @@ hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t
                           hipStream_t s);
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t s);
+// LOF on tie-inclusive neighbourhoods (lof.hip): each row's squared
+// k-distance from its exact kNN list, then lrd and LOF over the CSR
+// neighbourhoods of the range query at that radius.
+hipError_t launch_ties_radius(const float* x, int64_t n, int d, int k, const int64_t* lists,
+                              double* kd2, hipStream_t s);
+hipError_t launch_lof_ties(const float* x, int64_t n, int d, const int64_t* row_ptr,
+                           const int64_t* nbr, const double* kd2, double* lrd, float* lof,
+                           int32_t* count, hipStream_t s);
 // kNN score aggregates (mean, median, sum) and the classifier's majority vote
 // from the exact lists.
 hipError_t launch_score(const Plan& p, const Args& a, hipStream_t s);

@@ -29,7 +29,7 @@ PRECISION_NAMES = {v: k for k, v in PRECISIONS.items()}
 SCORES = {"kth": 0, "largest": 0, "mean": 1, "median": 2, "sum": 3}
 
 SYMBOLS = ("tod_default_options", "tod_workspace_size", "tod_knn", "tod_knn_noalloc",
-           "tod_knn_score", "tod_lof",
+           "tod_knn_score", "tod_lof", "tod_lof_ties_workspace_size", "tod_lof_ties",
            "tod_knn_decision", "tod_knn_classify", "tod_abod", "tod_cof", "tod_nwr_workspace_size",
            "tod_nwr", "tod_loci_workspace_size", "tod_loci",
            "tod_plan", "tod_plan_workspace",
@@ -111,6 +111,10 @@ def _load():
     lib.tod_knn_score.restype = ctypes.c_int
     lib.tod_lof.argtypes = [vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp, vp, st_p]
     lib.tod_lof.restype = ctypes.c_int
+    lib.tod_lof_ties_workspace_size.argtypes = [i64, i64, i32, i64, opt_p]
+    lib.tod_lof_ties_workspace_size.restype = sz
+    lib.tod_lof_ties.argtypes = [vp, i64, i64, i32, i64, opt_p, vp, sz, vp, vp, vp, st_p]
+    lib.tod_lof_ties.restype = ctypes.c_int
     lib.tod_knn_decision.argtypes = [vp, i64, vp, i64, i64, i32, opt_p, vp, sz, vp, vp, vp, vp,
                                       st_p]
     lib.tod_knn_decision.restype = ctypes.c_int
@@ -376,6 +380,44 @@ def tod_lof(x, k: int, opts=None, workspace=None, stream=None, stats=None,
                       ctypes.byref(stats) if stats is not None else None)
     _check(st, "tod_lof")
     return (lof, score, idx, dist) if return_lists else (lof, score)
+
+
+def tod_lof_ties_workspace_size(n: int, d: int, k: int, capacity: int, opts=None) -> int:
+    return int(_lib.tod_lof_ties_workspace_size(int(n), int(d), int(k), int(capacity),
+                                                ctypes.byref(opts) if opts is not None else None))
+
+
+def tod_lof_ties(x, k: int, opts=None, capacity=None, grow: bool = True, workspace=None,
+                 stream=None, stats=None):
+    """LOF on tie-inclusive k-distance neighbourhoods -> (lof fp32 [n], count int32 [n]).
+
+    ``capacity`` is the number of (point, neighbour) pairs the workspace is
+    sized for (default n k + n + 2^16); if the neighbourhoods hold more and
+    ``grow`` is set, the workspace is resized to the count the library
+    reports and the call is made once more, else TodError(TOD_ERR_CAPACITY)
+    is raised.
+    """
+    torch = _torch()
+    _dev_matrix(x, "x")
+    n, d = x.shape
+    lof = torch.empty((n,), dtype=torch.float32, device=x.device)
+    count = torch.empty((n,), dtype=torch.int32, device=x.device)
+    st = stats if stats is not None else new_stats()
+    optp = ctypes.byref(opts) if opts is not None else None
+    cap = int(capacity) if capacity is not None else n * int(k) + n + (1 << 16)
+    for _ in range(2):
+        need = tod_lof_ties_workspace_size(n, d, k, cap, opts)
+        if need == 0:  # arguments the size query rejects: let the call report why
+            need = 256
+        wsbuf, wsp, wsn = _ws(workspace, need, x.device)
+        rc = _lib.tod_lof_ties(_p(x), n, d, int(k), cap, optp, wsp, wsn, _stream(stream),
+                               _p(lof), _p(count), ctypes.byref(st))
+        if rc != TOD_ERR_CAPACITY or not grow:
+            break
+        cap = int(st.pairs_in_range)
+    _check(rc, "tod_lof_ties")
+    del wsbuf
+    return lof, count
 
 
 def tod_knn_decision(xq, xr, k: int, opts=None, workspace=None, stream=None, stats=None,

@@ -254,3 +254,38 @@ def test_loci_options_and_workspace(tod):
     for args in ((0, 8, 3, 100), (1000, 8, 0, 100000), (1000, 8, 33, 100000),
                  (1000, 8, 3, 999), ((1 << 20) + 1, 8, 3, 1 << 22)):
         assert tod.tod_loci_workspace_size(*args) == 0
+
+
+def _lof_ties(tod, n=100, d=8, k=5, cap=1000, opts=None, ws=FAKE, ws_bytes=1 << 30, x=FAKE,
+              lof=FAKE):
+    lib = tod.raw_library()
+    return lib.tod_lof_ties(x, n, d, k, cap, ctypes.byref(opts) if opts else None, ws, ws_bytes,
+                            None, lof, None, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=0), 1), (dict(d=0), 1), (dict(k=0), 1), (dict(k=100), 1),  # k > n - 1
+    (dict(cap=499), 1),  # below n k
+    (dict(x=None), 1), (dict(lof=None), 1), (dict(ws=None), 1),
+    (dict(d=513), 4), (dict(k=257, n=1000, cap=1 << 20), 4),
+    (dict(ws=ctypes.c_void_p(0x100010)), 3), (dict(ws_bytes=4096), 3),
+    (dict(x=ctypes.c_void_p(0x100004)), 1),
+])
+def test_lof_ties_invalid_arguments_rejected(tod, kw, status):
+    assert _lof_ties(tod, **kw) == status
+    assert tod.last_error() != ""
+
+
+def test_lof_ties_options_and_workspace_size(tod):
+    assert _lof_ties(tod, opts=tod.options(precision="fp32")) == tod.TOD_ERR_UNSUPPORTED
+    small = tod.tod_lof_ties_workspace_size(1000, 16, 5, 5000)
+    big = tod.tod_lof_ties_workspace_size(1000, 16, 5, 500000)
+    assert 0 < small < big
+    # CSR ids (8 bytes) plus candidate room for a quarter more (8 bytes each)
+    assert big - small >= (500000 - 5000) * 8
+    # at least the kNN call's own workspace for X against itself
+    assert small > tod.tod_workspace_size(1000, 1000, 16, 5, 0, tod.options(exclude_self=True))
+    assert tod.tod_lof_ties_workspace_size(1000, 600, 5, 5000) == 0
+    assert tod.tod_lof_ties_workspace_size(1000, 16, 5, 4999) == 0
+    assert tod.tod_lof_ties_workspace_size(10, 16, 10, 100) == 0
+    assert tod.tod_lof_ties_workspace_size(1000, 16, 5, 5000, tod.options(precision="fp32")) == 0
