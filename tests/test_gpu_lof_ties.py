@@ -155,3 +155,19 @@ def test_c2_full_size_matches_exactly_k(env):
     lof_k, _ = tod.tod_lof(a, w.k)
     torch.cuda.synchronize()
     np.testing.assert_allclose(lof, lof_k.cpu().numpy(), rtol=1e-6)
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_degenerate_sets(env, prec):
+    # All points equal: every other point ties at k-distance 0, so each
+    # neighbourhood holds all n - 1 others and LOF = 1 (lrd = 1e10 everywhere).
+    x = np.full((50, 5), 3.25, np.float32)
+    lof, count, _ = check(env, x, 3, precision=prec)
+    assert np.all(count == 49)
+    np.testing.assert_allclose(lof, 1.0, rtol=1e-6)
+    # Two points, k = 1; and k = n - 1 (every neighbourhood is all the others).
+    rng = np.random.default_rng(11)
+    check(env, rng.standard_normal((2, 7)).astype(np.float32), 1, precision=prec)
+    _, count, _ = check(env, rng.standard_normal((40, 9)).astype(np.float32), 39,
+                        precision=prec)
+    assert np.all(count == 39)
