@@ -239,9 +239,12 @@ tod_status tod_lof(const float* x, int64_t n, int64_t d, int32_t k, const tod_op
  * fused multiply-adds; membership is decided exactly in it (as tod_nwr
  * decides range membership).  Where no distance ties the k-distance, N_k(p)
  * is the k nearest and the result is tod_lof's.
- * Steps: the exact kNN lists (as tod_knn, self excluded), kd2 from them, the
- * neighbourhoods by the range query at each row's own radius (tod_nwr's
- * fp16 / bf16 range filter with exact verification), then lrd and LOF.
+ * Steps: the exact kNN lists with k + 1 entries (as tod_knn, self excluded;
+ * k entries when k = n - 1), kd2 from the first k; if every row's (k+1)-th
+ * neighbour is farther than kd2 (by more than the summation orders can
+ * differ), no point ties and the neighbourhoods are the k-lists; otherwise
+ * they come from the range query at each row's own radius (tod_nwr's
+ * fp16 / bf16 range filter with exact verification).  Then lrd and LOF.
  *   capacity         pairs (p, o) the workspace holds, summed over p; at
  *                    least n k (no ties)
  *   lof_out[n]       fp32 LOF scores (computed in fp64)

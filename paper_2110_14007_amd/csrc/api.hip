@@ -955,14 +955,19 @@ tod_status run_loci(const float* x, int64_t n, int64_t d, const double* radii, i
   return TOD_OK;
 }
 
-// LOF on tie-inclusive neighbourhoods: the exact kNN lists, each row's
-// squared k-distance, the neighbourhoods as CSR (a range query per row at
-// that radius), lrd and LOF.  Workspace: the CSR offsets and ids, the lists,
-// the squared k-distances and lrd, then a region the kNN call and the range
-// query use in turn.
+// LOF on tie-inclusive neighbourhoods: the exact kNN lists with one entry
+// more than k (when another point exists), each row's squared k-distance and
+// whether a point can tie with it, the neighbourhoods as CSR (the k-lists if
+// no row can have a tie, else a range query per row at its radius), lrd and
+// LOF.  Workspace: the CSR offsets and ids, the lists, the squared
+// k-distances and lrd, the tie flag, then a region the kNN call and the
+// range query use in turn.
 struct LofTiesLayout {
-  size_t row_ptr, nbr, lists, kd2, lrd, inner;
+  size_t row_ptr, nbr, lists, kd2, lrd, tie, inner;
 };
+
+// Neighbours per list: k + 1 when another point exists (it rules ties out).
+int32_t lof_ties_k1(int64_t n, int32_t k) { return (int64_t)k < n - 1 ? k + 1 : k; }
 
 LofTiesLayout lof_ties_layout(int64_t n, int32_t k, int64_t capacity) {
   LofTiesLayout L;
@@ -974,9 +979,10 @@ LofTiesLayout lof_ties_layout(int64_t n, int32_t k, int64_t capacity) {
   };
   L.row_ptr = take(sizeof(int64_t) * (size_t)(n + 1));
   L.nbr = take(sizeof(int64_t) * (size_t)capacity);
-  L.lists = take(sizeof(int64_t) * (size_t)n * (size_t)k);
+  L.lists = take(sizeof(int64_t) * (size_t)n * (size_t)lof_ties_k1(n, k));
   L.kd2 = take(sizeof(double) * (size_t)n);
   L.lrd = take(sizeof(double) * (size_t)n);
+  L.tie = take(sizeof(int32_t));
   L.inner = off;
   return L;
 }
@@ -989,7 +995,7 @@ size_t lof_ties_inner_bytes(int64_t n, int64_t d, int32_t k, int64_t capacity,
                             const tod_options& o) {
   Plan p;
   const char* why;
-  if (tod::make_plan(n, n, d, k, 0, 1, o, &p, &why) != TOD_OK) return 0;
+  if (tod::make_plan(n, n, d, lof_ties_k1(n, k), 0, 1, o, &p, &why) != TOD_OK) return 0;
   const size_t knn = tod::make_layout(p).total;
   const size_t nwr = nwr_ws_bytes(n, n, d, o, 1, capacity + capacity / 4 + ((int64_t)1 << 20));
   if (nwr == 0) return 0;
@@ -1039,25 +1045,40 @@ tod_status run_lof_ties(const float* x, int64_t n, int64_t d, int32_t k, int64_t
   int64_t* lists = (int64_t*)(base + L.lists);
   double* kd2 = (double*)(base + L.kd2);
   double* lrd = (double*)(base + L.lrd);
+  int32_t* tie = (int32_t*)(base + L.tie);
+  const int32_t k1 = lof_ties_k1(n, k);
   hipStream_t s = (hipStream_t)stream;
-  // 1. Exact kNN lists (X against itself, self excluded).
-  st = run(x, n, x, n, d, k, &o, 1, 0, base + L.inner, ws_bytes - L.inner, stream, lists,
+  // 1. Exact kNN lists (X against itself, self excluded), k1 entries.
+  st = run(x, n, x, n, d, k1, &o, 1, 0, base + L.inner, ws_bytes - L.inner, stream, lists,
            nullptr, nullptr, nullptr, nullptr, 0, nullptr, stats);
   if (st != TOD_OK) return st;
   Timers tm;
   tm.on = stats != nullptr;
   hipEvent_t e0 = tm.mark(s);
-  // 2. Each row's squared k-distance in the range query's exact arithmetic.
-  hipError_t he = tod::launch_ties_radius(x, n, (int)d, k, lists, kd2, s);
+  // 2. Each row's squared k-distance in the range query's exact arithmetic,
+  //    and whether any row can have a point tied with it.
+  hipError_t he = tod::launch_ties_radius(x, n, (int)d, k, k1, lists, kd2, tie, s);
+  int32_t any_tie = 0;
+  if (he == hipSuccess)
+    he = hipMemcpyAsync(&any_tie, tie, sizeof(any_tie), hipMemcpyDeviceToHost, s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
   if (he != hipSuccess) return hip_fail(he, "k-distance launch");
   hipEvent_t e1 = tm.mark(s);
-  // 3. The neighbourhoods: the range query at each row's own radius.
+  // 3. The neighbourhoods: the k-lists where no tie is possible, else the
+  //    range query at each row's own radius.
   tod_stats rs;
   memset(&rs, 0, sizeof(rs));
   rs.struct_size = sizeof(tod_stats);
   int64_t total = 0;
-  st = run_nwr(x, n, x, n, d, 0.0, &o, base + L.inner, ws_bytes - L.inner, stream, row_ptr,
-               capacity, nbr, nullptr, &total, stats ? &rs : nullptr, kd2);
+  if (!any_tie) {
+    he = tod::launch_ties_lists(n, k, k1, lists, row_ptr, nbr, s);
+    if (he != hipSuccess) return hip_fail(he, "neighbourhood launch");
+    total = n * (int64_t)k;
+    st = TOD_OK;
+  } else {
+    st = run_nwr(x, n, x, n, d, 0.0, &o, base + L.inner, ws_bytes - L.inner, stream, row_ptr,
+                 capacity, nbr, nullptr, &total, stats ? &rs : nullptr, kd2);
+  }
   if (stats) {
     stats->pairs_candidate = rs.pairs_candidate;
     stats->pairs_uncertain = rs.pairs_uncertain;

@@ -94,26 +94,51 @@ __device__ __forceinline__ double wave_sum(double v) {
 
 // kd2[p] = the largest D2(p, o) over p's k exact neighbours, i.e. the k-th
 // smallest (the largest, should the list order disagree with the column-order
-// sum in the last bit).
+// sum in the last bit).  The lists hold k1 = k + 1 neighbours when another
+// point exists: a row whose (k+1)-th neighbour is farther than kd2 by more
+// than the two summation orders can differ (relative 1e-11, against at most
+// (d + 2) 2^-52 for d <= 4096) has no point tied at its k-distance, so its
+// neighbourhood is its k-list; any other row sets *tie.
 __global__ void __launch_bounds__(256)
-ties_radius_kernel(const float* __restrict__ x, int64_t n, int d, int k,
-                   const int64_t* __restrict__ lists, double* __restrict__ kd2) {
+ties_radius_kernel(const float* __restrict__ x, int64_t n, int d, int k, int k1,
+                   const int64_t* __restrict__ lists, double* __restrict__ kd2,
+                   int32_t* __restrict__ tie) {
 #pragma clang fp contract(off)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t p = (int64_t)blockIdx.x * 4 + wave;
   if (p >= n) return;  // uniform per wave
   const float* xp = x + p * (int64_t)d;
-  double m = 0.0;
-  for (int i = lane; i < k; i += 64) {
-    const int64_t o = lists[p * k + i];
+  double m = 0.0, nxt = INFINITY;
+  for (int i = lane; i < k1; i += 64) {
+    const int64_t o = lists[p * k1 + i];
     const double v = exact_d2(xp, x + o * (int64_t)d, d);
-    m = v > m ? v : m;
+    if (i < k) m = v > m ? v : m;
+    else nxt = v;
   }
   for (int o = 32; o > 0; o >>= 1) {
     const double t = __shfl_xor(m, o, 64);
     m = t > m ? t : m;
+    const double u = __shfl_xor(nxt, o, 64);
+    nxt = u < nxt ? u : nxt;
   }
-  if (lane == 0) kd2[p] = m;
+  if (lane == 0) {
+    kd2[p] = m;
+    if (k1 > k && !(nxt * (1.0 - 1e-11) > m)) *tie = 1;
+  }
+}
+
+__global__ void tie_clear_kernel(int32_t* tie) {
+  if (threadIdx.x == 0) *tie = 0;
+}
+
+// Neighbourhoods of a set with no ties at the k-distance: the first k entries
+// of every (k1-entry) list, as CSR.
+__global__ void __launch_bounds__(256)
+ties_lists_kernel(int64_t n, int k, int k1, const int64_t* __restrict__ lists,
+                  int64_t* __restrict__ row_ptr, int64_t* __restrict__ nbr) {
+  const int64_t f = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (f < n * k) nbr[f] = lists[(f / k) * k1 + f % k];
+  if (f <= n) row_ptr[f] = f * k;
 }
 
 __global__ void __launch_bounds__(256)
@@ -157,10 +182,19 @@ lof_ties_kernel(int64_t n, const int64_t* __restrict__ row_ptr, const int64_t* _
 
 }  // namespace
 
-hipError_t launch_ties_radius(const float* x, int64_t n, int d, int k, const int64_t* lists,
-                              double* kd2, hipStream_t st) {
+hipError_t launch_ties_radius(const float* x, int64_t n, int d, int k, int k1,
+                              const int64_t* lists, double* kd2, int32_t* tie, hipStream_t st) {
+  hipLaunchKernelGGL(tie_clear_kernel, dim3(1), dim3(64), 0, st, tie);
   hipLaunchKernelGGL(ties_radius_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, st, x, n, d,
-                     k, lists, kd2);
+                     k, k1, lists, kd2, tie);
+  return hipGetLastError();
+}
+
+hipError_t launch_ties_lists(int64_t n, int k, int k1, const int64_t* lists, int64_t* row_ptr,
+                             int64_t* nbr, hipStream_t st) {
+  const int64_t cnt = n * k > n + 1 ? n * k : n + 1;
+  hipLaunchKernelGGL(ties_lists_kernel, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, n,
+                     k, k1, lists, row_ptr, nbr);
   return hipGetLastError();
 }
 

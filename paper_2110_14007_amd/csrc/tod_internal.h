@@ -306,10 +306,14 @@ hipError_t launch_recheck(const Plan& p, const Args& a, int64_t q_begin, int64_t
 hipError_t launch_fallback(const Plan& p, const Args& a, hipStream_t s);
 hipError_t launch_lof(const Plan& p, const Args& a, hipStream_t s);
 // LOF on tie-inclusive neighbourhoods (lof.hip): each row's squared
-// k-distance from its exact kNN list, then lrd and LOF over the CSR
-// neighbourhoods of the range query at that radius.
-hipError_t launch_ties_radius(const float* x, int64_t n, int d, int k, const int64_t* lists,
-                              double* kd2, hipStream_t s);
+// k-distance from its exact kNN list (k1 = k + 1 entries, the last one to
+// rule ties out; *tie set where one is possible), the neighbourhoods as the
+// k-lists when no row has a possible tie, then lrd and LOF over the CSR
+// neighbourhoods (else those of the range query at each row's radius).
+hipError_t launch_ties_radius(const float* x, int64_t n, int d, int k, int k1,
+                              const int64_t* lists, double* kd2, int32_t* tie, hipStream_t s);
+hipError_t launch_ties_lists(int64_t n, int k, int k1, const int64_t* lists, int64_t* row_ptr,
+                             int64_t* nbr, hipStream_t s);
 hipError_t launch_lof_ties(const float* x, int64_t n, int d, const int64_t* row_ptr,
                            const int64_t* nbr, const double* kd2, double* lrd, float* lof,
                            int32_t* count, hipStream_t s);

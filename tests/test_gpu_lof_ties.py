@@ -93,8 +93,9 @@ def test_golden(env, which, prec):
 def test_integer_points(env, n, d, k, hi, prec):
     rng = np.random.default_rng(9000 + n + d + k)
     x = rng.integers(0, hi, size=(n, d)).astype(np.float32)
-    _, count, _ = check(env, x, k, precision=prec)
+    _, count, st = check(env, x, k, precision=prec)
     assert np.any(count > k)  # the data do tie
+    assert st["pairs_candidate"] > 0  # so the range query ran
 
 
 @pytest.mark.parametrize("k", [4, 5, 9, 12])
@@ -119,8 +120,11 @@ def test_continuous_equals_exactly_k(env, prec):
     # No ties: N_k(p) is the k nearest, and the scores are tod_lof's.
     torch, tod, _ = env
     x, _ = workloads.generate("C1", n=2500)
-    lof, count, _ = check(env, x, 10, precision=prec)
+    lof, count, st = check(env, x, 10, precision=prec)
     assert np.all(count == 10)
+    # Every 11th neighbour is farther than the 10th: the k-lists are the
+    # neighbourhoods and the range query does not run.
+    assert st["pairs_candidate"] == 0
     a = torch.from_numpy(x).cuda()
     lof_k, _ = tod.tod_lof(a, 10, tod.options(precision=prec))
     torch.cuda.synchronize()
@@ -151,6 +155,7 @@ def test_c2_full_size_matches_exactly_k(env):
     say("lof_ties C2 full size")
     lof, count, st = run(env, x, w.k)
     assert np.all(count == w.k)
+    assert st["pairs_candidate"] == 0 and st["pairs_in_range"] == len(x) * w.k
     a = torch.from_numpy(x).cuda()
     lof_k, _ = tod.tod_lof(a, w.k)
     torch.cuda.synchronize()
