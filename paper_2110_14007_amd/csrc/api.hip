@@ -212,6 +212,7 @@ tod_status make_plan(int64_t nq, int64_t nr, int64_t d, int32_t k, int32_t lof, 
   const bool want = o.reorder > 0 || (o.reorder == 0 && nr >= kOrderMinRows);
   // (With runs, the tile scans the whole set in pieces whatever S is.)
   p->order = (self && p->tile_kind == 1 && (p->splits == 1 || p->runs > 1) && want) ? 1 : 0;
+  p->groups = order_groups(nr, d);
   // Tail split of the register-list tile with one reference split (not with
   // runs: their pieces already halve every workgroup's scan).
   p->tail_parts = 1;
@@ -256,11 +257,12 @@ Layout make_layout(const Plan& p) {
     const int32_t nb = order_blocks(p.nr);
     L.perm = take(sizeof(int32_t) * p.nr_pad);
     L.lab = take(sizeof(int32_t) * p.nr);
-    L.cstart = take(sizeof(int32_t) * (kOrdC + 1));
-    L.bcnt = take(sizeof(int32_t) * (size_t)nb * kOrdC);
-    L.boff = take(sizeof(int32_t) * (size_t)nb * kOrdC);
+    L.oseed = take(sizeof(float) * 16 * (size_t)p.groups);
+    L.cstart = take(sizeof(int32_t) * (size_t)(p.groups + 1));
+    L.bcnt = take(sizeof(int32_t) * (size_t)nb * p.groups);
+    L.boff = take(sizeof(int32_t) * (size_t)nb * p.groups);
   } else {
-    L.perm = L.lab = L.cstart = L.bcnt = L.boff = 0;
+    L.perm = L.lab = L.oseed = L.cstart = L.bcnt = L.boff = 0;
   }
   if (p.lists) {
     L.idx32 = take(sizeof(int32_t) * p.nq * p.k);
@@ -520,6 +522,8 @@ tod_status run(const float* xq, int64_t nq, const float* xr, int64_t nr, int64_t
   a.fbidx = (uint32_t*)(base + L.fbidx);
   a.perm = p.order ? (int32_t*)(base + L.perm) : nullptr;
   a.lab = p.order ? (int32_t*)(base + L.lab) : nullptr;
+  a.groups = p.groups;
+  a.oseed = p.order ? (float*)(base + L.oseed) : nullptr;
   a.cstart = p.order ? (int32_t*)(base + L.cstart) : nullptr;
   a.bcnt = p.order ? (int32_t*)(base + L.bcnt) : nullptr;
   a.boff = p.order ? (int32_t*)(base + L.boff) : nullptr;

@@ -836,11 +836,16 @@ mtile_kernel(Args a, int64_t q_begin, int64_t q_rows) {
   const int nst = (int)((r_end - r_begin + TR - 1) / TR);
   int st0 = 0;
   if (a.cstart) {
+    // The last group starting at or before p0 (starts ascend; an empty group
+    // shares its start with the next one).
     const int p0 = (int)(q_begin + (int64_t)blockIdx.x * (W * 32 * NQ));
-    int g = 0;
-#pragma unroll
-    for (int i = 1; i < kOrdC; ++i) g = a.cstart[i] <= p0 ? i : g;
-    st0 = (int)((a.cstart[g] - r_begin) / TR);
+    int lo = 0, hi = a.groups;  // cstart[lo] <= p0 < cstart[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (a.cstart[mid] <= p0) lo = mid;
+      else hi = mid;
+    }
+    st0 = (int)((a.cstart[lo] - r_begin) / TR);
   }
   // Tail split: piece `split` of `parts` takes the stages [ib, ib + nscan) of
   // the scan order.

@@ -42,6 +42,7 @@ struct Plan {
   int32_t lists;       // int32 / fp64 neighbour lists kept in the workspace (LOF, score
                        // aggregates, classifier)
   int32_t order;       // 1: grouped scan order (order.hip), X against X only
+  int32_t groups;      // seed groups of the grouped order (order_groups)
   int32_t runs = 1;    // 2: the register-list tile scans the references in 2 S pieces of the
                        // scan order with lists of K' / 2; each query's K' slots per split
                        // then hold two ascending runs (rows of 256+ elements, K' = 128)
@@ -86,7 +87,8 @@ inline int tail_pieces(int64_t tw, int64_t slots, int64_t cus, int pmax, bool au
 // Workspace regions (byte offsets from the workspace base, 256-aligned).
 struct Layout {
   size_t ctrl, mu64, mu32, colpart, xq_r, xq_q, hn_r, n64_q, rho_q, partial, ptail, worklist,
-      fbtau, fbpart, fbidx, idx32, d64, lrd, kdist, perm, lab, cstart, bcnt, boff, total;
+      fbtau, fbpart, fbidx, idx32, d64, lrd, kdist, perm, lab, oseed, cstart, bcnt, boff,
+      total;
   int32_t colpart_blocks;
 };
 
@@ -159,7 +161,9 @@ struct Args {
   // grouped scan order (all null when the input order is kept)
   int32_t* perm;       // position -> input row [nr]
   int32_t* lab;        // input row -> group [nr]
-  int32_t* cstart;     // first position of each group [kOrdC + 1]
+  int32_t groups;      // seed groups of the grouped order
+  float* oseed;        // the seed rows of rows of at most 16 elements [groups x 16]
+  int32_t* cstart;     // first position of each group [groups + 1]
   int32_t* bcnt;       // rows per group in each block of kOrdRows rows
   int32_t* boff;       // first position of each block's rows of each group
   int32_t* idx32;      // [nq x k] neighbour ids (LOF)
@@ -208,11 +212,13 @@ __host__ __device__ constexpr double fold_const(int precision) {
   return precision == TOD_PREC_FP16 ? 32768.0 : 1.0;
 }
 
-// Grouped scan order: groups, rows per counting block, and the smallest
-// reference set the planner groups by default.
-constexpr int kOrdC = 16;
+// Grouped scan order: the most seed groups (their count, a power of two, is
+// order_groups'), rows per counting block, and the smallest reference set the
+// planner groups by default.
+constexpr int kOrdMaxC = 1024;
 constexpr int kOrdRows = 1024;
 constexpr int64_t kOrderMinRows = 4096;
+int32_t order_groups(int64_t nr, int64_t d);
 int32_t order_blocks(int64_t nr);
 hipError_t launch_order(const Plan& p, const Args& a, hipStream_t s);
 
