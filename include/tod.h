@@ -96,9 +96,10 @@ typedef struct {
   int32_t force_fallback;/* debug: treat every row as uncertified (exact recomputation) */
   int32_t no_recheck;    /* debug: return the filter's shortlist order without verification */
   int32_t reorder;       /* scan order of an X-against-X call (tod_knn with xq == xr, tod_knn_score,
-                          * tod_lof): 0 = planner, 1 = on, -1 = off.  On: the rows are grouped by a
-                          * 16-seed partition (nearest of 16 evenly spaced rows) and every query
-                          * block first scans the references of its own group, so the filter's
+                          * tod_lof): 0 = planner, 1 = on, -1 = off.  On: the rows are grouped by
+                          * their nearest of G evenly spaced rows (G = 16, or for rows of at most
+                          * 16 elements one per 8192 rows, up to 1024) and every query block
+                          * first scans the references of its own group, so the filter's
                           * thresholds tighten early.  Results are identical either way. */
   int32_t score;         /* tod_score: the kNN outlier score of tod_knn_score, tod_knn_decision
                           * and tod_lof's knn_score_out */
