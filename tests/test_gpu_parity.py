@@ -301,3 +301,22 @@ def test_reorder_default(env):
     xq = big[:500].copy()
     _, _, st = run_knn(env, xq, big, 5, precision="fp16", ref_splits=1)
     assert not st["reordered"]  # separate query set: input order
+
+
+# Rows of at most 16 elements take one seed group per 8192 rows (32 groups at
+# 300,000 rows, 64 at 600,000): the order must still change nothing, and
+# sampled rows must match the oracle.
+@pytest.mark.parametrize("n,d", [(300000, 8), (600000, 3)])
+def test_reorder_many_groups(env, n, d):
+    _, _, oracle = env
+    rng = np.random.default_rng(n + d)
+    x = rng.random((n, d), dtype=np.float64).astype(np.float32)
+    say("reorder many groups", n, d)
+    on = run_lof(env, x, 5, precision="fp16", reorder=1, ref_splits=1)
+    off = run_lof(env, x, 5, precision="fp16", reorder=-1, ref_splits=1)
+    assert on[4]["reordered"] and not off[4]["reordered"]
+    for u, v in zip(on[:4], off[:4]):
+        np.testing.assert_array_equal(u, v)
+    rows = np.sort(rng.choice(n, 256, replace=False))
+    oidx, odist = oracle.knn_self(x, 5, rows=rows)
+    compare_knn(x, x, rows, on[2][rows], on[3][rows], oidx, odist)
