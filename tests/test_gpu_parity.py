@@ -260,7 +260,7 @@ def test_forced_fallback_chunks(env, nq, nr, d, k):
 # out group by group, each workgroup starts its scan at its own group, and the
 # recheck maps positions back to input rows.  One reference split is forced:
 # the order applies only then.
-@pytest.mark.parametrize("case", ["line", "lattice", "ints", "dups", "C1", "tiny"])
+@pytest.mark.parametrize("case", ["line", "lattice", "ints", "dups", "C1", "tiny", "d11"])
 def test_reorder_matches_oracle(env, case):
     rng = np.random.default_rng(41)
     if case == "line":
@@ -274,6 +274,8 @@ def test_reorder_matches_oracle(env, case):
         x, k, ties = np.concatenate([base, base[::3], base[::7]]), 6, False
     elif case == "C1":
         x, k, ties = workloads.generate("C1")[0], 10, True
+    elif case == "d11":  # rows padded to 12 columns in the group assignment
+        x, k, ties = rng.standard_normal((5000, 11)).astype(np.float32), 7, True
     else:
         x, k, ties = rng.standard_normal((70, 5)).astype(np.float32), 9, True
     say("reorder", case, x.shape, k)
